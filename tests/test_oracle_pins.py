@@ -1,0 +1,353 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+CPU only.  Each test names the passage it pins and the closed form, identity,
+brute force or library routine that is independent of the oracle's own code.
+"""
+
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import method as M
+from oracle import numerics as nx
+from oracle import records as R
+from oracle import traffic as TR
+import synth
+
+
+# ------------------------------------------------------------ cumulants --
+
+def test_mean_and_population_covariance_match_library():
+    """eq. (cgf-cumulants) and App. B: kappa_1 is the mean, kappa_2 the 1/n covariance."""
+    Kb = synth.make_keys_block(64, 64, "gauss", 7).astype(np.float64)
+    np.testing.assert_allclose(M.block_mean(Kb), np.mean(Kb, axis=0), rtol=0, atol=1e-14)
+    np.testing.assert_allclose(M.block_covariance(Kb), np.cov(Kb.T, bias=True), rtol=0, atol=1e-13)
+    # and not the 1/(n-1) estimator
+    assert not np.allclose(M.block_covariance(Kb), np.cov(Kb.T, bias=False), atol=1e-6)
+
+
+def test_zero_variance_block_estimate_is_exact():
+    """eq. (trunc): Sigma_b = 0 makes the second-order estimate exact, ln m_b = ln n + c q.k."""
+    d, L, c = 64, 64, 1.0 / 8.0
+    rng = np.random.default_rng(3)
+    K = np.concatenate([synth.make_keys_block(L, d, "const", 11 + i) for i in range(4)]).astype(np.float64)
+    q = rng.standard_normal((2, d))
+    T = 4 * L - 5                                           # partial tail block too
+    counts, means, factors = M.block_statistics(K, T, L, r=3)
+    est = M.log_mass_estimate(q, counts, means, factors, c)
+    exact = M.exact_block_log_mass(q, K, T, L, c)
+    np.testing.assert_allclose(est, exact, rtol=0, atol=1e-12)
+    closed = np.log(counts)[:, None] + c * (K[::L][: len(counts)] @ q.T)
+    np.testing.assert_allclose(est, closed, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("n,d,r", [(64, 64, 64), (64, 128, 63), (32, 16, 16)])
+def test_full_rank_factors_reproduce_quadratic_form(n, d, r):
+    """eq. (gram) with r >= rank(Sigma_b): sum_i (xi_i . q)^2 = q^T Sigma_b q."""
+    Kb = synth.make_keys_block(n, d, "gauss", 5).astype(np.float64)
+    Sigma = np.cov(Kb.T, bias=True)                         # library, not the oracle
+    q = np.random.default_rng(9).standard_normal((3, d))
+    for xi in (M.scaled_eigenvectors(M.block_covariance(Kb), r), M.scaled_eigenvectors_gram(Kb, r)):
+        quad = ((xi @ q.T) ** 2).sum(axis=0)
+        ref = np.einsum("gd,de,ge->g", q, Sigma, q)
+        np.testing.assert_allclose(quad, ref, rtol=1e-11, atol=0)
+
+
+def test_gram_trick_equals_covariance_eigh():
+    """Sec. 5.6 Gram trick: same nonzero eigenvalues, same scaled eigenvectors (sign fixed)."""
+    for seed in range(5):
+        Kb = synth.make_keys_block(64, 128, "gauss", 100 + seed).astype(np.float64)
+        a = M.scaled_eigenvectors(M.block_covariance(Kb), 8)
+        b = M.scaled_eigenvectors_gram(Kb, 8)
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-10)
+        lam_cov = np.sort(np.linalg.eigvalsh(np.cov(Kb.T, bias=True)))[::-1][:63]
+        Kc = Kb - Kb.mean(0)
+        lam_gram = np.sort(np.linalg.eigvalsh(Kc @ Kc.T / 64))[::-1][:63]
+        np.testing.assert_allclose(lam_cov, lam_gram, rtol=1e-9, atol=1e-12)
+        np.testing.assert_allclose((a ** 2).sum(1), lam_cov[:8], rtol=1e-10)
+
+
+def test_rank_cap_is_n_minus_one():
+    """Sec. 7.6.1: a block of L keys has covariance rank at most L - 1; factors beyond are 0."""
+    Kb = synth.make_keys_block(16, 64, "gauss", 21).astype(np.float64)
+    xi = M.scaled_eigenvectors(M.block_covariance(Kb), 20)
+    norms = np.linalg.norm(xi, axis=1)
+    assert np.all(norms[:15] > 1e-3)
+    assert np.all(norms[15:] < 1e-6)
+
+
+def test_low_rank_factors_are_best_rank_r():
+    """eq. (lowrank): sum_i xi_i xi_i^T is the best rank-r approximation (Eckart-Young via SVD)."""
+    Kb = synth.make_keys_block(64, 128, "spiked", 31).astype(np.float64)
+    Kc = Kb - Kb.mean(0)
+    U, S, Vt = np.linalg.svd(Kc / math.sqrt(64), full_matrices=False)    # library SVD
+    best = (Vt[:4].T * S[:4] ** 2) @ Vt[:4]
+    xi = M.scaled_eigenvectors(M.block_covariance(Kb), 4)
+    np.testing.assert_allclose(xi.T @ xi, best, rtol=0, atol=1e-11)
+
+
+def test_gaussian_cgf_has_no_higher_cumulants():
+    """eq. (cgf-expansion): for Gaussian keys ln E[exp(c q.x)] = c q.mu + c^2/2 q^T Sigma q.
+
+    The estimate is fed the population mean and a factorisation of Sigma; the
+    reference is a Monte-Carlo average over 2^18 samples (CLT error ~2e-3).
+    """
+    rng = np.random.default_rng(12)
+    d, c = 64, 1.0 / 8.0
+    A = rng.standard_normal((d, 6)) * 0.35
+    Sigma = A @ A.T + 0.05 * np.eye(d)
+    mu = rng.standard_normal(d) * 0.3
+    q = rng.standard_normal((1, d))
+    scale = math.sqrt(0.5 / (c * c * float(q[0] @ Sigma @ q[0])))   # c^2 q^T Sigma q = 0.5
+    q = q * scale
+    xi = np.linalg.cholesky(Sigma).T                      # Sigma = xi^T xi, d rows
+    est = M.log_mass_estimate(q, np.array([1]), mu[None], xi[None], c)[0, 0]
+    x = rng.multivariate_normal(mu, Sigma, size=1 << 18)
+    mc = math.log(np.mean(np.exp(c * (x @ q[0]))))
+    assert abs(est - mc) < 1e-2
+    assert abs(est - (c * q[0] @ mu + 0.25)) < 1e-12
+
+
+def test_second_order_estimate_unbiased_on_gaussian_blocks():
+    """Sec. 5.2: on Gaussian blocks the truncated estimate tracks the exact log-mass in expectation.
+
+    Mean of (estimate - exact ln m_b) over 4096 blocks of 64 keys is O(1/n) (~1e-3);
+    a dropped or mis-signed term would move it by >= 0.25.
+    """
+    rng = np.random.default_rng(13)
+    d, L, c, nblk = 32, 64, 1.0 / math.sqrt(32), 4096
+    A = rng.standard_normal((d, 4)) * 0.5
+    Sigma = A @ A.T + 0.1 * np.eye(d)
+    q = rng.standard_normal((1, d))
+    q = q * math.sqrt(0.5 / (c * c * float(q[0] @ Sigma @ q[0])))
+    Lc = np.linalg.cholesky(Sigma)
+    K = (rng.standard_normal((nblk * L, d)) @ Lc.T) + rng.standard_normal(d) * 0.2
+    T = nblk * L
+    counts, means, factors = M.block_statistics(K, T, L, r=d)
+    est = M.log_mass_estimate(q, counts, means, factors, c)[:, 0]
+    exact = M.exact_block_log_mass(q, K, T, L, c)[:, 0]
+    gap = float(np.mean(est - exact))
+    assert abs(gap) < 1e-2, gap
+    # the first-order (mean-pool) score misses the curvature by ~0.25 on average
+    first = M.log_mass_estimate(q, counts, means, factors[:, :0], c)[:, 0]
+    assert float(np.mean(exact - first)) > 0.2
+
+
+# -------------------------------------------------------- selection rule --
+
+def _brute_force_best(P_list, nc, s):
+    best, best_set = None, None
+    for S in itertools.combinations(range(nc), s):
+        kept = np.zeros(len(P_list[0]), dtype=bool)
+        kept[list(S)] = True
+        loss = sum(P[~kept].sum() for P in P_list)
+        if best is None or loss < best - 1e-15:
+            best, best_set = loss, S
+    return best, best_set
+
+
+def test_mha_topk_by_mass_minimises_dropped_mass():
+    """App. A, MHA case: keeping the top-k blocks by mass minimises tau (brute force over C(15,4))."""
+    L, d, c = 8, 16, 0.5
+    rng = np.random.default_rng(41)
+    K = rng.standard_normal((15 * L, d))
+    V = rng.standard_normal((15 * L, d))
+    q = rng.standard_normal((1, d))
+    T = 15 * L
+    P, _ = M.block_mixture(q[0], K, V, T, L, c)
+    _, best = _brute_force_best([P], 15, 4)
+    sigma = M.osa_group_scores(q, K, T, L, c)
+    sel = M.select_top(sigma, 15, 4)
+    assert tuple(sel.tolist()) == tuple(sorted(best))
+    # same set as sorting the exact log-masses directly
+    lm = M.exact_block_log_mass(q, K, T, L, c)[:, 0]
+    assert set(sel.tolist()) == set(np.argsort(-lm)[:4].tolist())
+
+
+def test_gqa_additive_score_minimises_summed_dropped_mass():
+    """eq. (prop-gqa) under A3: top-k by sum_g m_b^g / Z^g minimises sum_g tau_g (C(8,3) subsets)."""
+    L, d, c, G = 8, 16, 0.6, 2
+    rng = np.random.default_rng(42)
+    K = rng.standard_normal((8 * L, d))
+    V = rng.standard_normal((8 * L, d))
+    q = rng.standard_normal((G, d))
+    T = 8 * L
+    Ps = [M.block_mixture(q[g], K, V, T, L, c)[0] for g in range(G)]
+    _, best = _brute_force_best(Ps, 8, 3)
+    sel = M.select_top(M.osa_group_scores(q, K, T, L, c), 8, 3)
+    assert tuple(sel.tolist()) == tuple(sorted(best))
+    # group score equals the normalised mass sum of eq. (prop-gqa)
+    np.testing.assert_allclose(np.exp(M.osa_group_scores(q, K, T, L, c)), sum(Ps), rtol=1e-12)
+
+
+def test_select_top_ties_padding_and_candidates():
+    """Reading of the top-s rule: ties to the lower index, ascending output, -1 padding."""
+    sigma = np.array([0.5, 1.0, 1.0, 0.2, 1.0, -3.0])
+    assert M.select_top(sigma, 6, 2).tolist() == [1, 2]
+    assert M.select_top(sigma, 6, 4).tolist() == [0, 1, 2, 4]
+    assert M.select_top(sigma, 3, 5).tolist() == [0, 1, 2, -1, -1]
+    assert M.select_top(sigma, 0, 3).tolist() == [-1, -1, -1]
+    assert M.candidate_count(1024, 64, 64) == 15
+    assert M.candidate_count(1000, 64, 64) == 15            # block 14 straddles the window start
+    assert M.candidate_count(1000, 64, 0) == 16             # w = 0: the partial tail is a candidate
+    assert M.candidate_count(500, 64, 512) == 0             # T <= w: dense window only
+    U = M.union_tokens(1000, 64, 100, [3, 14])
+    expect = sorted(set(range(900, 1000)) | set(range(192, 256)) | set(range(896, 900)))
+    assert U.tolist() == expect
+
+
+def test_planted_block_is_top_by_exact_and_estimated_mass(golden_dir):
+    """Tiny single-head workload: the planted block is the argmax of the exact and estimated masses."""
+    with open(os.path.join(golden_dir, "c1_seed.txt")) as f:
+        seed = int(f.read().split()[0])
+    prob = synth.make_problem("c1", seed=seed)
+    cfg = prob["cfg"]
+    q = prob["q"][0].numpy().astype(np.float64)
+    K = prob["k"][0, 0].numpy().astype(np.float64)
+    c = 1.0 / math.sqrt(cfg["d"])
+    exact = M.exact_block_log_mass(q, K, cfg["T"], cfg["L"], c)[:15, 0]
+    stats = M.block_statistics(K, cfg["T"], cfg["L"], cfg["r"])
+    est = M.log_mass_estimate(q, *stats, c)[:15, 0]
+    planted = prob["planted"][(0, 0)]
+    assert int(np.argmax(exact)) == planted
+    assert int(np.argmax(est)) == planted
+
+
+# ---------------------------------------------------- attention identities --
+
+def _sdpa(q, K, V, c):
+    """Dense attention by torch's library routine, float64 on the CPU."""
+    qt = torch.from_numpy(q)[None, :, None, :]              # [1, G, 1, d]
+    G = q.shape[0]
+    Kt = torch.from_numpy(K)[None, None].expand(1, G, -1, -1)
+    Vt = torch.from_numpy(V)[None, None].expand(1, G, -1, -1)
+    o = torch.nn.functional.scaled_dot_product_attention(qt, Kt, Vt, scale=c)
+    return o[0, :, 0].numpy()
+
+
+def test_full_selection_is_dense_attention():
+    """eq. (oracle-true) with tau = 0: s >= #candidates keeps every token -> dense attention."""
+    rng = np.random.default_rng(51)
+    T, L, d, G, c = 700, 64, 32, 3, 1.0 / math.sqrt(32)
+    K = rng.standard_normal((T, d))
+    V = rng.standard_normal((T, d))
+    q = rng.standard_normal((G, d))
+    for w in (0, 64, 100, 1000):
+        res = M.decode_unit(q, K, V, T, L, r=2, s=20, w=w, c=c, mean_dtype="f32", factor_dtype="f32")
+        np.testing.assert_allclose(res["out"], _sdpa(q, K, V, c), rtol=0, atol=1e-12)
+        s = c * q @ K.T
+        np.testing.assert_allclose(res["lse"], np.log(np.exp(s).sum(1)), rtol=1e-13)
+
+
+def test_kept_output_two_ways_and_exact_error_identity():
+    """eq. (oracle-true) and eq. (oracle-exact) at w = 0.
+
+    The union softmax equals sum_{b in S} P_b v^c_b / (1 - tau), and
+    o* - o_hat_S equals (1/(1 - tau)) sum_{b not in S} P_b (v^c_b - o*).
+    """
+    rng = np.random.default_rng(52)
+    T, L, d, c = 10 * 16, 16, 24, 0.4
+    K = rng.standard_normal((T, d))
+    V = rng.standard_normal((T, d))
+    q = rng.standard_normal((1, d))
+    S = [1, 4, 5, 9]
+    kept = np.zeros(10, dtype=bool)
+    kept[S] = True
+    P, cent = M.block_mixture(q[0], K, V, T, L, c)
+    o_hat, tau = M.kept_output(P, cent, kept)
+    U = M.union_tokens(T, L, 0, S)
+    out, _ = M.sparse_attention(q, K, V, U, c)
+    np.testing.assert_allclose(out[0], o_hat, rtol=0, atol=1e-12)
+    o_star = _sdpa(q, K, V, c)[0]
+    np.testing.assert_allclose(o_star - o_hat, M.drop_error(P, cent, kept), rtol=0, atol=1e-12)
+    assert 0 < tau < 1
+
+
+def test_empty_union_gives_zero_and_minus_inf():
+    out, lse = M.sparse_attention(np.ones((2, 4)), np.ones((3, 4)), np.ones((3, 4)), np.array([], int), 1.0)
+    assert np.all(out == 0) and np.all(np.isneginf(lse))
+
+
+# --------------------------------------------------------- traffic tables --
+
+def _read_table(path):
+    rows = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            parts = line.split()
+            rows[parts[0]] = [None if p == "-" else float(p) for p in parts[1:]]
+    return rows
+
+
+def test_bandwidth_table_reproduces(golden_dir):
+    """Table "bandwidth": every branch, total and ratio of every row."""
+    rows = _read_table(os.path.join(golden_dir, "bandwidth_table.txt"))
+    args = dict(T=32768, H=4, D=128, L=32, k=16, w=256)
+    spec = {
+        "dense": ("dense", {}), "osa": ("osa", {}),
+        "nsa_mlp": ("nsa_mlp", {}), "nsa_meanpool": ("nsa_meanpool", {}), "nsa_quest": ("nsa_quest", {}),
+        "cobs_full_r4_bf16": ("cobs_full", dict(r=4, quant="bf16")),
+        "cobs_full_r6_bf16": ("cobs_full", dict(r=6, quant="bf16")),
+        "cobs_full_r4_fp4": ("cobs_full", dict(r=4, quant="fp4")),
+        "cobs_full_r6_fp4": ("cobs_full", dict(r=6, quant="fp4")),
+        "cobs_sub85_r4_fp4": ("cobs_subspace", dict(r=4, quant="fp4", sub_dim=84.875)),
+    }
+    dense = TR.per_layer_traffic("dense", **args)["total"] / TR.KIB
+    nsa = TR.per_layer_traffic("nsa_mlp", **args)["total"] / TR.KIB
+    for name, (meth, kw) in spec.items():
+        t = TR.per_layer_traffic(meth, **args, **kw)
+        keys, vals, win, fine, tot, less, more = rows[name]
+        got = [t[k] / TR.KIB for k in ("summary_keys", "summary_values", "window", "fine", "total")]
+        want = [0 if v is None else v for v in (keys, vals, win, fine, tot)]
+        assert [round(x) for x in got] == [round(x) for x in want], name
+        if less is not None:
+            assert round(dense / got[4], 2) == less, name
+        if more is not None:
+            assert round(got[4] / nsa, 2) == more, name
+
+
+def test_quant_table_bytes(golden_dir):
+    """Table "quant": factor bytes per descriptor and the reduction versus bf16."""
+    with open(os.path.join(golden_dir, "quant_bytes.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            r, dim, b16, b4, red = line.split()
+            assert TR.factor_bytes(int(r), int(dim), "bf16") == int(b16)
+            assert TR.factor_bytes(int(r), int(dim), "fp4") == int(b4)
+            assert round(int(b16) / int(b4), 1) == float(red)
+
+
+def test_subspace_dimension_averages(golden_dir):
+    """Figure "subspace-perlayer": averages 68 and 84.875 (about 1.25x)."""
+    dark, full = [], []
+    with open(os.path.join(golden_dir, "subspace_dims.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            _, a, b = line.split()
+            dark.append(int(a))
+            full.append(int(a) + int(b))
+    assert sum(dark) / 16 == 68
+    assert sum(full) / 16 == 84.875
+    assert abs(84.875 / 68 - 1.25) < 0.01
+
+
+def test_record_algorithmic_bytes_match_descriptor_accounting():
+    """Table "quant" byte rule applied to the record: count + mean + factors (+ scales)."""
+    assert R.algorithmic_bytes(128, 4, "f32", "f32") == 2564
+    assert R.algorithmic_bytes(128, 4, "bf16", "bf16") == 1284
+    assert R.algorithmic_bytes(128, 4, "bf16", "e2m1") == 4 + 256 + 272
+    assert R.algorithmic_bytes(128, 4, "e2m1", "e2m1") == 4 + 68 + 272
+    assert R.algorithmic_bytes(64, 2, "f32", "f32") == 772
+    for md in R.DTYPES:
+        for fd in R.DTYPES:
+            lay = R.layout(128, 4, md, fd)
+            assert lay["total"] % 16 == 0
+            assert lay["total"] - R.algorithmic_bytes(128, 4, md, fd) < 16
