@@ -1,0 +1,188 @@
+/*
+ * cobs.h - C ABI of the COBS decode-step library for AMD Instinct MI355X (gfx950).
+ *
+ * COBS (Cumulant Order Block Sparse Attention) selects, per KV head and per
+ * decode step, the KV-cache blocks with the largest estimated attention mass
+ * and attends only to them plus a sliding window.  Notation of the paper:
+ * a query q in R^d attends over keys/values k_t, v_t of T cached tokens,
+ * split into contiguous blocks of L tokens (Sec. 2); G query heads share
+ * one KV head (GQA); c is the attention scale (the paper absorbs it into q).
+ *
+ * Stages (one decode step of one layer, for every batch row and KV head):
+ *   1. block statistics: count n_b, mean kbar_b, top-r scaled eigenvectors
+ *      xi_i of the population covariance (Sec. 5.3 eq. lowrank, Gram trick of
+ *      Sec. 5.6), stored as fp32, bf16 or FP4 E2M1 (Sec. 5.5);
+ *   2. second-order log-mass estimate per block and query head
+ *        l_b^g = ln n_b + c q_g.kbar_b + (c^2/2) sum_i (xi_i . q_g)^2
+ *      (eq. trunc with eq. gram), GQA group score
+ *        sigma_b = ln sum_g exp(l_b^g - ln sum_b' exp(l_b'^g))
+ *      (log of eq. gqa-secondorder);
+ *   3. top-s candidate blocks by sigma (ties to the lower block index);
+ *   4. softmax attention over the union of the selected blocks and the last w
+ *      tokens, each token once (eq. oracle-true), split over workgroups and
+ *      merged through log-sum-exp.
+ *
+ * Conventions
+ *   - Every tensor pointer is a DEVICE pointer unless stated otherwise; the
+ *     caller owns every buffer, the workspace included.  The library allocates
+ *     no device memory, keeps no state between calls and never synchronises.
+ *   - Every call validates its arguments on the host before any launch and
+ *     returns COBS_ERR_INVALID_ARG / COBS_ERR_UNSUPPORTED without touching the
+ *     GPU; otherwise it enqueues its kernels on `stream` (a hipStream_t; NULL
+ *     is the default stream) and returns COBS_OK, or COBS_ERR_HIP if a launch
+ *     failed.  It never aborts.
+ *   - seq_lens[b] (device int32) is the number of valid tokens T of batch row
+ *     b.  Values are clamped to [0, max_seq_len] on the device; a row with
+ *     T = 0 selects nothing and yields out = 0, lse = -inf.
+ *   - Blocks: NB(T) = ceil(T/L); block b holds n_b = min(L, T - bL) tokens.
+ *     A block is a selection candidate iff bL < T - w (it has a token before
+ *     the window).
+ *   - Query head j belongs to KV head j / G (contiguous groups), G = Hq / Hkv.
+ *   - Workspace: `ws` must hold cobs_workspace_bytes(cfg, op) bytes, be 256-byte
+ *     aligned and be zero-filled before its first use; every call leaves its
+ *     arrival counters zero again on completion, so the same workspace can be
+ *     reused by later calls on the same stream.  Calls that share a workspace
+ *     must not overlap in time (different streams race).
+ *   - Results are deterministic: identical inputs give bitwise identical
+ *     outputs (no floating-point atomics; fixed reduction orders).
+ */
+#ifndef COBS_H
+#define COBS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  COBS_OK = 0,
+  COBS_ERR_INVALID_ARG = 1, /* null pointer, inconsistent shape, bad stride ...   */
+  COBS_ERR_UNSUPPORTED = 2, /* valid but outside what the kernels implement       */
+  COBS_ERR_WORKSPACE = 3,   /* ws too small or misaligned                          */
+  COBS_ERR_HIP = 4          /* a HIP launch or runtime call failed                 */
+} cobs_status_t;
+
+typedef enum { COBS_F32 = 0, COBS_BF16 = 1, COBS_E2M1 = 2 } cobs_dtype_t;
+
+typedef enum {
+  COBS_OP_BUILD = 0,  /* cobs_build_block_stats */
+  COBS_OP_SELECT = 1, /* cobs_select            */
+  COBS_OP_DECODE = 2, /* cobs_sparse_decode     */
+  COBS_OP_STEP = 3    /* cobs_decode_step       */
+} cobs_op_t;
+
+/* Problem description shared by every call (host struct, passed by pointer). */
+typedef struct {
+  int32_t batch;         /* B >= 1                                                  */
+  int32_t num_q_heads;   /* Hq, a multiple of num_kv_heads; G = Hq/Hkv in {1,2,4,8,16} */
+  int32_t num_kv_heads;  /* Hkv >= 1                                                */
+  int32_t head_dim;      /* d in {64, 128}                                          */
+  int32_t max_seq_len;   /* T_max, cache capacity in tokens, a multiple of block_size */
+  int32_t block_size;    /* L = 64 (the only size the kernels implement)            */
+  int32_t rank;          /* r in [0, 16]; 0 gives the first-order (mean-pool) score */
+  int32_t budget;        /* s >= 0 selected blocks per (batch row, KV head)         */
+  int32_t window;        /* w >= 0 most recent tokens always attended               */
+  cobs_dtype_t kv_dtype;     /* K/V cache element type: COBS_F32 or COBS_BF16          */
+  cobs_dtype_t mean_dtype;   /* stored block mean: F32, BF16 or E2M1                  */
+  cobs_dtype_t factor_dtype; /* stored scaled eigenvectors: F32, BF16 or E2M1         */
+  float softmax_scale;   /* c; 0 selects 1/sqrt(d)                                  */
+} cobs_config_t;
+
+/* KV cache of one layer.
+ * Contiguous mode (block_table == NULL): element (b, h, t, i) of K lives at
+ *   k + b*stride_b + h*stride_h + t*stride_t + i   (strides in elements, i < d
+ *   contiguous), likewise V with the same strides.  stride_t >= d.
+ * Paged mode (block_table != NULL): block_table is a device int32 array
+ *   [B, T_max/L] of page ids; page p of the K pool holds [Hkv, L, d] contiguous
+ *   elements, so (b, h, t, i) lives at
+ *   k + ((block_table[b*(T_max/L) + t/L]*Hkv + h)*L + t%L)*d + i.
+ *   Strides are ignored; page ids must lie in [0, num_pages).                    */
+typedef struct {
+  const void* k;
+  const void* v;
+  int64_t stride_b, stride_h, stride_t;
+  const int32_t* block_table;
+  int64_t num_pages;
+} cobs_kv_t;
+
+/* Descriptor record of one block (Sec. 5.3 / 5.5), little-endian, 16-byte aligned:
+ *   0        int32   n_b
+ *   4        float   scale of the E2M1 mean (0 for F32/BF16 means)
+ *   8        8 zero bytes
+ *   16       float   scale of factor i, i < r (E2M1 factors only), zero padded to 16 B
+ *   M        mean: d elements of mean_dtype
+ *   M+|mean| factors: r vectors of d elements of factor_dtype, vector-major
+ *   size     rounded up to 16 B
+ * Element sizes: F32 4 B, BF16 2 B, E2M1 one nibble (element 2j in the low nibble
+ * of byte j).  E2M1 vectors use scale = fp32(max|x|)/6, y = x/scale in fp32,
+ * round to nearest of {0,.5,1,1.5,2,3,4,6} with ties to the even code, |y| <= 6,
+ * no negative zero, scale 0 for an all-zero vector.  A block with n_b < L stores
+ * zero factors.  Summaries of one layer: [B, Hkv, T_max/L] records.
+ * Returns 0 if cfg is invalid.                                                     */
+size_t cobs_record_bytes(const cobs_config_t* cfg);
+
+/* Workspace bytes needed by `op` for this configuration (0 if none or invalid). */
+size_t cobs_workspace_bytes(const cobs_config_t* cfg, cobs_op_t op);
+
+/* Block statistics (Sec. 5.3, Gram trick of Sec. 5.6, storage of Sec. 5.5).
+ * For every batch row b and KV head h, (re)build the records of blocks
+ * first_block <= j < first_block + num_blocks that exist at T = seq_lens[b]
+ * (j < ceil(T/L)); other records are left untouched.  A full block gets
+ * its count, mean and top-r factors (fixed-count block power iteration on the
+ * L x L Gram matrix of the centred keys, Rayleigh-Ritz, xi = Kc^T w / sqrt(n),
+ * sign fixed so the largest-magnitude entry is positive); a partial block gets
+ * its count, mean and zero factors.
+ *   summaries: device [B, Hkv, T_max/L, cobs_record_bytes(cfg)] bytes, written. */
+cobs_status_t cobs_build_block_stats(const cobs_config_t* cfg, const cobs_kv_t* kv,
+                                     const int32_t* seq_lens, int32_t first_block,
+                                     int32_t num_blocks, void* summaries, void* ws,
+                                     size_t ws_bytes, void* stream);
+
+/* Block selection (eq. trunc, eq. gram, eq. gqa-secondorder, top-s).
+ *   q:         device fp32 [B, Hq, d], unscaled queries.
+ *   summaries: device records as built above (read only).
+ *   sel:       device int32 [B, Hkv, budget], written: the min(s, #candidates)
+ *              best candidate blocks in ascending order, then -1.
+ *   scores:    optional device fp32 [B, Hkv, T_max/L], written: sigma_b for
+ *              candidates, -inf for every other index.                         */
+cobs_status_t cobs_select(const cobs_config_t* cfg, const float* q, const void* summaries,
+                          const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
+                          size_t ws_bytes, void* stream);
+
+/* Block-sparse decode attention (eq. oracle-true over the kept-token union).
+ *   sel:  device int32 [B, Hkv, budget] block ids.  The longest prefix that is
+ *         strictly ascending with every entry in [0, #candidates) is used; the
+ *         entries after it (e.g. -1 padding) are ignored.
+ *   out:  device fp32 [B, Hq, d], written.
+ *   lse:  optional device fp32 [B, Hq], written: ln sum_{t in U} exp(c q.k_t).  */
+cobs_status_t cobs_sparse_decode(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                 const int32_t* seq_lens, const int32_t* sel, float* out,
+                                 float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* One decode step: refresh the record of the block holding token T-1 (the
+ * caller has already written the new token's K/V at position T-1 and counted
+ * it in seq_lens), then select and attend.  Equivalent to
+ * cobs_build_block_stats on block (T-1)/L, cobs_select and cobs_sparse_decode.
+ *   summaries: in/out.   sel: optional device int32 [B, Hkv, budget] output.    */
+cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                               const int32_t* seq_lens, void* summaries, int32_t* sel,
+                               float* out, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* FP4 E2M1 encoder used for descriptor storage (Sec. 5.5), exposed so the
+ * rounding rule can be checked on its own.
+ *   x:      device fp32 [num_vectors, dim], dim even, 2 <= dim <= 4096.
+ *   codes:  device uint8 [num_vectors, dim/2], written (element 2j low nibble).
+ *   scales: device fp32 [num_vectors], written.                                 */
+cobs_status_t cobs_pack_e2m1(const float* x, int64_t num_vectors, int32_t dim, uint8_t* codes,
+                             float* scales, void* stream);
+
+/* Static string for a status code. */
+const char* cobs_status_string(cobs_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COBS_H */

@@ -1,0 +1,310 @@
+// C ABI of the COBS decode-step library: argument validation, workspace
+// layout, launch configuration.  Every entry point validates on the host
+// before enqueuing anything on the caller's stream and never synchronises.
+#include <math.h>
+
+#include <algorithm>
+
+#include "cobs.h"
+#include "cobs_kernels.h"
+
+using namespace cobs;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int dtype_code(cobs_dtype_t t) { return (int)t; }
+
+// Shape checks shared by every entry point.
+cobs_status_t check_config(const cobs_config_t* c) {
+  if (!c) return COBS_ERR_INVALID_ARG;
+  if (c->batch < 1 || c->num_kv_heads < 1 || c->num_q_heads < 1) return COBS_ERR_INVALID_ARG;
+  if (c->num_q_heads % c->num_kv_heads != 0) return COBS_ERR_INVALID_ARG;
+  if (c->head_dim < 1 || c->block_size < 1 || c->max_seq_len < 1) return COBS_ERR_INVALID_ARG;
+  if (c->rank < 0 || c->budget < 0 || c->window < 0) return COBS_ERR_INVALID_ARG;
+  if (c->kv_dtype != COBS_F32 && c->kv_dtype != COBS_BF16) return COBS_ERR_INVALID_ARG;
+  for (cobs_dtype_t t : {c->mean_dtype, c->factor_dtype})
+    if (t != COBS_F32 && t != COBS_BF16 && t != COBS_E2M1) return COBS_ERR_INVALID_ARG;
+  if (!(c->softmax_scale >= 0.0f) || !isfinite(c->softmax_scale)) return COBS_ERR_INVALID_ARG;
+  if (c->max_seq_len % c->block_size != 0) return COBS_ERR_INVALID_ARG;
+  const int g = c->num_q_heads / c->num_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return COBS_ERR_UNSUPPORTED;
+  if (c->head_dim != 64 && c->head_dim != 128) return COBS_ERR_UNSUPPORTED;
+  if (c->block_size != kL) return COBS_ERR_UNSUPPORTED;
+  if (c->rank > kMaxRank) return COBS_ERR_UNSUPPORTED;
+  if (c->max_seq_len / c->block_size > kMaxBlocksPerSeq) return COBS_ERR_UNSUPPORTED;
+  return COBS_OK;
+}
+
+struct Derived {
+  int B, hq, hkv, G, d, tmax, nbmax, r, s, w, units;
+  int mdt, fdt, kv_f32;
+  float c;
+  RecLayout lay;
+  int bpw, nch;         // selector: blocks per workgroup, workgroups per unit
+  int spw, nwg;         // decode: segments per workgroup, workgroups per unit
+  size_t sel_ell, sel_part, sel_cnt, sel_bytes;
+  size_t dec_part, dec_cnt, dec_bytes;
+  size_t step_sel, step_bytes;   // decode step: select region, decode region, selection
+};
+
+Derived derive(const cobs_config_t* c) {
+  Derived v;
+  v.B = c->batch;
+  v.hq = c->num_q_heads;
+  v.hkv = c->num_kv_heads;
+  v.G = v.hq / v.hkv;
+  v.d = c->head_dim;
+  v.tmax = c->max_seq_len;
+  v.nbmax = v.tmax / kL;
+  v.r = c->rank;
+  v.s = c->budget;
+  v.w = c->window;
+  v.units = v.B * v.hkv;
+  v.mdt = dtype_code(c->mean_dtype);
+  v.fdt = dtype_code(c->factor_dtype);
+  v.kv_f32 = c->kv_dtype == COBS_F32;
+  v.c = c->softmax_scale > 0.0f ? c->softmax_scale : 1.0f / sqrtf((float)v.d);
+  v.lay = rec_layout(v.d, v.r, v.mdt, v.fdt);
+
+  // selector: enough workgroups to cover the chip, at least 16 blocks each
+  v.bpw = 16;
+  while (v.bpw < 256 && (int64_t)v.units * ((v.nbmax + v.bpw - 1) / v.bpw) > 2048) v.bpw *= 2;
+  v.nch = (v.nbmax + v.bpw - 1) / v.bpw;
+  // decode: segments = selected blocks + blocks touched by the window
+  const int nwin_max = v.w == 0 ? 0 : std::min(v.nbmax, (v.w + kL - 1) / kL + 1);
+  const int nseg = v.s + nwin_max;
+  v.spw = 4;
+  while (v.spw < 64 && (int64_t)v.units * ((nseg + v.spw - 1) / v.spw) > 4096) v.spw *= 2;
+  v.nwg = std::max(1, (nseg + v.spw - 1) / v.spw);
+
+  size_t off = 0;
+  v.sel_ell = off;  off = round_up(off + sizeof(float) * (size_t)v.units * v.G * v.nbmax, kAlign);
+  v.sel_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nch * v.G * 2, kAlign);
+  v.sel_cnt = off;  off = round_up(off + sizeof(unsigned) * (size_t)v.units, kAlign);
+  v.sel_bytes = off;
+  off = 0;
+  v.dec_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nwg * v.G * (v.d + 2), kAlign);
+  v.dec_cnt = off;  off = round_up(off + sizeof(unsigned) * (size_t)v.units, kAlign);
+  v.dec_bytes = off;
+  v.step_sel = v.sel_bytes + v.dec_bytes;
+  v.step_bytes = round_up(v.step_sel + sizeof(int32_t) * (size_t)v.units * v.s, kAlign);
+  return v;
+}
+
+cobs_status_t check_kv(const cobs_kv_t* kv, const Derived& v) {
+  if (!kv || !kv->k || !kv->v) return COBS_ERR_INVALID_ARG;
+  if (!aligned(kv->k, 16) || !aligned(kv->v, 16)) return COBS_ERR_INVALID_ARG;
+  if (kv->block_table) {
+    if (kv->num_pages < 1) return COBS_ERR_INVALID_ARG;
+    return COBS_OK;
+  }
+  const int64_t vec = v.kv_f32 ? 4 : 8;          // elements per 16-byte load
+  if (kv->stride_t < v.d || kv->stride_h < 0 || kv->stride_b < 0) return COBS_ERR_INVALID_ARG;
+  if (kv->stride_t % vec || kv->stride_h % vec || kv->stride_b % vec) return COBS_ERR_INVALID_ARG;
+  return COBS_OK;
+}
+
+KvView make_view(const cobs_kv_t* kv, const Derived& v) {
+  KvView x;
+  x.k = kv->k;
+  x.v = kv->v;
+  x.sb = kv->stride_b;
+  x.sh = kv->stride_h;
+  x.st = kv->stride_t;
+  x.table = kv->block_table;
+  x.num_pages = kv->num_pages;
+  x.nbmax = v.nbmax;
+  x.hkv = v.hkv;
+  x.d = v.d;
+  return x;
+}
+
+cobs_status_t check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return COBS_OK;
+  if (!ws || ws_bytes < need || !aligned(ws, kAlign)) return COBS_ERR_WORKSPACE;
+  return COBS_OK;
+}
+
+cobs_status_t hip_status(hipError_t e) { return e == hipSuccess ? COBS_OK : COBS_ERR_HIP; }
+
+cobs_status_t run_build(const Derived& v, const cobs_kv_t* kv, const int32_t* seq_lens, int first,
+                        int count, bool tail, void* summaries, hipStream_t st) {
+  BuildParams p;
+  p.kv = make_view(kv, v);
+  p.seq_lens = seq_lens;
+  p.rec = static_cast<uint8_t*>(summaries);
+  p.hkv = v.hkv;
+  p.tmax = v.tmax;
+  p.nbmax = v.nbmax;
+  p.r = v.r;
+  p.mdt = v.mdt;
+  p.fdt = v.fdt;
+  p.first_block = first;
+  p.tail_mode = tail ? 1 : 0;
+  p.kv_f32 = v.kv_f32;
+  p.lay = v.lay;
+  if (!tail && count == 0) return COBS_OK;
+  dim3 grid(tail ? 1 : count, v.hkv, v.B);
+  return hip_status(launch_build(p, v.d, grid, st));
+}
+
+cobs_status_t run_select(const Derived& v, const float* q, const void* summaries,
+                         const int32_t* seq_lens, int32_t* sel, float* scores, uint8_t* ws,
+                         hipStream_t st) {
+  SelectParams p;
+  p.q = q;
+  p.rec = static_cast<const uint8_t*>(summaries);
+  p.seq_lens = seq_lens;
+  p.sel = sel;
+  p.scores = scores;
+  p.ell = reinterpret_cast<float*>(ws + v.sel_ell);
+  p.part = reinterpret_cast<float*>(ws + v.sel_part);
+  p.cnt = reinterpret_cast<unsigned*>(ws + v.sel_cnt);
+  p.hkv = v.hkv;
+  p.hq = v.hq;
+  p.nbmax = v.nbmax;
+  p.tmax = v.tmax;
+  p.r = v.r;
+  p.s = v.s;
+  p.w = v.w;
+  p.mdt = v.mdt;
+  p.fdt = v.fdt;
+  p.nch = v.nch;
+  p.bpw = v.bpw;
+  p.c = v.c;
+  p.lay = v.lay;
+  dim3 grid(v.nch, v.hkv, v.B);
+  return hip_status(launch_select(p, v.d, v.G, grid, st));
+}
+
+cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
+                         const int32_t* seq_lens, const int32_t* sel, float* out, float* lse,
+                         uint8_t* ws, hipStream_t st) {
+  DecodeParams p;
+  p.q = q;
+  p.kv = make_view(kv, v);
+  p.seq_lens = seq_lens;
+  p.sel = sel;
+  p.out = out;
+  p.lse = lse;
+  p.part = reinterpret_cast<float*>(ws + v.dec_part);
+  p.cnt = reinterpret_cast<unsigned*>(ws + v.dec_cnt);
+  p.hkv = v.hkv;
+  p.hq = v.hq;
+  p.tmax = v.tmax;
+  p.s = v.s;
+  p.w = v.w;
+  p.nwg = v.nwg;
+  p.spw = v.spw;
+  p.c = v.c;
+  dim3 grid(v.nwg, v.hkv, v.B);
+  return hip_status(launch_decode(p, v.d, v.G, v.kv_f32 != 0, grid, st));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t cobs_record_bytes(const cobs_config_t* cfg) {
+  if (check_config(cfg) != COBS_OK) return 0;
+  return (size_t)derive(cfg).lay.total;
+}
+
+size_t cobs_workspace_bytes(const cobs_config_t* cfg, cobs_op_t op) {
+  if (check_config(cfg) != COBS_OK) return 0;
+  const Derived v = derive(cfg);
+  switch (op) {
+    case COBS_OP_BUILD: return 0;
+    case COBS_OP_SELECT: return v.sel_bytes;
+    case COBS_OP_DECODE: return v.dec_bytes;
+    case COBS_OP_STEP: return v.step_bytes;
+    default: return 0;
+  }
+}
+
+cobs_status_t cobs_build_block_stats(const cobs_config_t* cfg, const cobs_kv_t* kv,
+                                     const int32_t* seq_lens, int32_t first_block,
+                                     int32_t num_blocks, void* summaries, void* ws,
+                                     size_t ws_bytes, void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  cobs_status_t s = check_config(cfg);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if ((s = check_kv(kv, v)) != COBS_OK) return s;
+  if (!seq_lens || !summaries || !aligned(summaries, 16)) return COBS_ERR_INVALID_ARG;
+  if (first_block < 0 || num_blocks < 0 || (int64_t)first_block + num_blocks > v.nbmax)
+    return COBS_ERR_INVALID_ARG;
+  return run_build(v, kv, seq_lens, first_block, num_blocks, false, summaries,
+                   static_cast<hipStream_t>(stream));
+}
+
+cobs_status_t cobs_select(const cobs_config_t* cfg, const float* q, const void* summaries,
+                          const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
+                          size_t ws_bytes, void* stream) {
+  cobs_status_t s = check_config(cfg);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if (!q || !summaries || !seq_lens || !sel || !aligned(summaries, 16)) return COBS_ERR_INVALID_ARG;
+  if ((s = check_ws(ws, ws_bytes, v.sel_bytes)) != COBS_OK) return s;
+  return run_select(v, q, summaries, seq_lens, sel, scores, static_cast<uint8_t*>(ws),
+                    static_cast<hipStream_t>(stream));
+}
+
+cobs_status_t cobs_sparse_decode(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                 const int32_t* seq_lens, const int32_t* sel, float* out,
+                                 float* lse, void* ws, size_t ws_bytes, void* stream) {
+  cobs_status_t s = check_config(cfg);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if ((s = check_kv(kv, v)) != COBS_OK) return s;
+  if (!q || !seq_lens || !out || (!sel && v.s > 0)) return COBS_ERR_INVALID_ARG;
+  if ((s = check_ws(ws, ws_bytes, v.dec_bytes)) != COBS_OK) return s;
+  return run_decode(v, q, kv, seq_lens, sel, out, lse, static_cast<uint8_t*>(ws),
+                    static_cast<hipStream_t>(stream));
+}
+
+cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                               const int32_t* seq_lens, void* summaries, int32_t* sel, float* out,
+                               float* lse, void* ws, size_t ws_bytes, void* stream) {
+  cobs_status_t s = check_config(cfg);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if ((s = check_kv(kv, v)) != COBS_OK) return s;
+  if (!q || !seq_lens || !summaries || !out || !aligned(summaries, 16)) return COBS_ERR_INVALID_ARG;
+  if ((s = check_ws(ws, ws_bytes, v.step_bytes)) != COBS_OK) return s;
+  uint8_t* wsb = static_cast<uint8_t*>(ws);
+  // the selection goes to the caller's buffer if given, else to the workspace
+  int32_t* selp = sel ? sel : reinterpret_cast<int32_t*>(wsb + v.step_sel);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if ((s = run_build(v, kv, seq_lens, 0, 0, true, summaries, st)) != COBS_OK) return s;
+  if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st)) != COBS_OK) return s;
+  return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
+}
+
+cobs_status_t cobs_pack_e2m1(const float* x, int64_t num_vectors, int32_t dim, uint8_t* codes,
+                             float* scales, void* stream) {
+  if (!x || !codes || !scales || num_vectors < 0 || dim < 2 || dim > 4096 || dim % 2)
+    return COBS_ERR_INVALID_ARG;
+  if (num_vectors > 0x7fffffff) return COBS_ERR_UNSUPPORTED;
+  return hip_status(launch_pack_e2m1(x, num_vectors, dim, codes, scales, static_cast<hipStream_t>(stream)));
+}
+
+const char* cobs_status_string(cobs_status_t status) {
+  switch (status) {
+    case COBS_OK: return "COBS_OK";
+    case COBS_ERR_INVALID_ARG: return "COBS_ERR_INVALID_ARG: invalid argument";
+    case COBS_ERR_UNSUPPORTED: return "COBS_ERR_UNSUPPORTED: configuration not implemented";
+    case COBS_ERR_WORKSPACE: return "COBS_ERR_WORKSPACE: workspace missing, too small or misaligned";
+    case COBS_ERR_HIP: return "COBS_ERR_HIP: HIP launch or runtime error";
+    default: return "unknown cobs_status_t";
+  }
+}
+
+}  // extern "C"

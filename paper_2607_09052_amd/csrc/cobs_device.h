@@ -1,0 +1,145 @@
+// Device-side helpers shared by the COBS kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cobs {
+
+constexpr int kL = 64;          // tokens per block (one token per lane of a wave)
+constexpr int kMaxG = 16;       // query heads per KV head
+constexpr int kMaxRank = 16;
+constexpr int kMaxBlocksPerSeq = 8192;   // T_max / L bound for the in-LDS top-s
+
+enum Dtype : int { DT_F32 = 0, DT_BF16 = 1, DT_E2M1 = 2 };
+
+// ---------------------------------------------------------------- record --
+// Byte layout of one block descriptor (see include/cobs.h).
+struct RecLayout {
+  int mean_off;    // offset of the mean vector
+  int mean_bytes;
+  int fac_off;     // offset of factor 0
+  int vec_bytes;   // bytes of one factor vector
+  int total;       // record size, multiple of 16
+};
+
+__host__ __device__ inline int vec_bytes(int d, int dt) {
+  return dt == DT_F32 ? 4 * d : (dt == DT_BF16 ? 2 * d : d / 2);
+}
+
+__host__ __device__ inline RecLayout rec_layout(int d, int r, int mdt, int fdt) {
+  RecLayout l;
+  int fscale = (fdt == DT_E2M1) ? ((4 * r + 15) / 16) * 16 : 0;
+  l.mean_off = 16 + fscale;
+  l.mean_bytes = vec_bytes(d, mdt);
+  l.fac_off = l.mean_off + l.mean_bytes;
+  l.vec_bytes = vec_bytes(d, fdt);
+  l.total = ((l.fac_off + r * l.vec_bytes + 15) / 16) * 16;
+  return l;
+}
+
+// ------------------------------------------------------------ conversions --
+__device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
+
+// Round-to-nearest-even fp32 -> bf16 bits (finite inputs).
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// E2M1 code (4 bits) -> value without scale: 1 sign bit, 2 exponent bits (bias 1),
+// 1 mantissa bit; exponent 0 is subnormal (0 or 0.5).
+__device__ __forceinline__ float e2m1_value(uint32_t c) {
+  uint32_t m = c & 7u;
+  uint32_t bits = (((m >> 1) + 126u) << 23) | ((m & 1u) << 22);
+  float v = (m >= 2u) ? __uint_as_float(bits) : (m ? 0.5f : 0.0f);
+  return (c & 8u) ? -v : v;
+}
+
+// Magnitude code of a = |x/scale| clamped to [0, 6]: nearest point of
+// {0, .5, 1, 1.5, 2, 3, 4, 6}, a tie going to the even code.  Each midpoint
+// comparison is strict when the lower neighbour has the even code.
+__device__ __forceinline__ uint32_t e2m1_mag_code(float a) {
+  return (uint32_t)(a > 0.25f) + (uint32_t)(a >= 0.75f) + (uint32_t)(a > 1.25f) +
+         (uint32_t)(a >= 1.75f) + (uint32_t)(a > 2.5f) + (uint32_t)(a >= 3.5f) +
+         (uint32_t)(a > 5.0f);
+}
+
+// Code of one element given the vector's scale (> 0).  fp32 division, correctly
+// rounded (the library is built without fast-math).
+__device__ __forceinline__ uint32_t e2m1_code(float x, float scale) {
+  float y = x / scale;
+  float a = fminf(fabsf(y), 6.0f);
+  uint32_t c = e2m1_mag_code(a);
+  return (y < 0.0f && c != 0u) ? (c | 8u) : c;
+}
+
+// Order-preserving map float -> uint32 (larger float, larger key).
+__device__ __forceinline__ uint32_t order_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// -------------------------------------------------------------- KV access --
+struct KvView {
+  const void* k;
+  const void* v;
+  int64_t sb, sh, st;            // element strides (contiguous mode)
+  const int32_t* table;          // [B, nbmax] page ids or nullptr
+  int64_t num_pages;
+  int nbmax;                     // T_max / L
+  int hkv;
+  int d;
+};
+
+// Element offset of token t of (b, h); -1 when its page id is out of range.
+__device__ __forceinline__ int64_t kv_offset(const KvView& kv, int b, int h, int t) {
+  if (kv.table == nullptr) return (int64_t)b * kv.sb + (int64_t)h * kv.sh + (int64_t)t * kv.st;
+  int page = kv.table[(int64_t)b * kv.nbmax + t / kL];
+  if (page < 0 || (int64_t)page >= kv.num_pages) return -1;
+  return (((int64_t)page * kv.hkv + h) * kL + (t % kL)) * (int64_t)kv.d;
+}
+
+__device__ __forceinline__ int clamp_len(int T, int tmax) { return T < 0 ? 0 : (T > tmax ? tmax : T); }
+
+// -------------------------------------------------------- wave reductions --
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+// Merge two (max, sum of exp(x - max)) pairs.
+__device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
+  float mn = fmaxf(m, m2);
+  if (mn == -INFINITY) { m = mn; s = 0.0f; return; }
+  s = s * __expf(m - mn) + s2 * __expf(m2 - mn);
+  m = mn;
+}
+
+// Release this workgroup's global writes and count its arrival on `counter`;
+// returns true (in every thread) for the last of `expected` arrivals, which
+// then sees every other workgroup's writes.  The last arrival resets the counter.
+__device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected, int* sflag) {
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned prev = atomicAdd(counter, 1u);
+    int last = (prev == expected - 1u) ? 1 : 0;
+    if (last) atomicExch(counter, 0u);     // every other arrival has happened
+    *sflag = last;
+  }
+  __syncthreads();
+  bool last = *sflag != 0;
+  if (last) __threadfence();
+  return last;
+}
+
+}  // namespace cobs

@@ -57,7 +57,8 @@ def config(name, **over):
     cfg = dict(CONFIGS[name])
     cfg.update(over)
     cfg.setdefault("steps", 0)
-    cfg.setdefault("T_max", cfg["T"] + cfg["steps"])
+    # cache capacity: the tokens of the workload rounded up to whole blocks
+    cfg.setdefault("T_max", -(-(cfg["T"] + cfg["steps"]) // cfg["L"]) * cfg["L"])
     return cfg
 
 
@@ -279,6 +280,10 @@ def make_keys_block(n, d, law, seed, rank=None):
     law "gauss": i.i.d. N(0,1); "lowrank": rank-`rank` plus tiny noise;
     "const": every token equal; "spiked": the c3 law.
     """
+    return np.ascontiguousarray(_keys_block(n, d, law, seed, rank))
+
+
+def _keys_block(n, d, law, seed, rank):
     rng = np.random.default_rng(seed)
     if law == "gauss":
         return rng.standard_normal((n, d)).astype(np.float32)

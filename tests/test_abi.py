@@ -1,0 +1,103 @@
+"""The C-ABI library loads, exports every declared symbol, sizes records and
+workspaces consistently with the documented layout, and rejects invalid
+arguments on the host before touching the GPU.  CPU only: no kernel launches.
+"""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from oracle import records as R
+from paper_2607_09052_amd import cobs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "cobs.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^\s*(?:size_t|cobs_status_t|const char\*)\s+(cobs_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    declared = _declared_functions()
+    assert len(declared) == 8, declared
+    lib = cobs.lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert sorted(cobs.EXPORTS) == declared
+    nm = subprocess.run(["nm", "-D", "--defined-only", cobs.LIB_PATH], capture_output=True, text=True)
+    exported = set(re.findall(r" T (cobs_\w+)", nm.stdout))
+    assert set(declared) <= exported
+
+
+def _cfg(**over):
+    base = dict(batch=2, num_q_heads=8, num_kv_heads=2, head_dim=128, max_seq_len=4096, rank=4,
+                budget=8, window=128, kv_dtype="bf16", mean_dtype="f32", factor_dtype="f32")
+    base.update(over)
+    return cobs.Config(**base)
+
+
+@pytest.mark.parametrize("md", ["f32", "bf16", "e2m1"])
+@pytest.mark.parametrize("fd", ["f32", "bf16", "e2m1"])
+@pytest.mark.parametrize("d,r", [(64, 2), (128, 4), (128, 16), (64, 0)])
+def test_record_bytes_match_oracle_layout(md, fd, d, r):
+    assert cobs.record_bytes(_cfg(head_dim=d, rank=r, mean_dtype=md, factor_dtype=fd)) == \
+        R.layout(d, r, md, fd)["total"]
+
+
+def test_workspace_sizes_are_aligned_and_ordered():
+    cfg = _cfg()
+    sel, dec, step = (cobs.workspace_bytes(cfg, op) for op in (1, 2, 3))
+    assert cobs.workspace_bytes(cfg, 0) == 0
+    assert sel % 256 == 0 and dec % 256 == 0 and step % 256 == 0
+    assert step >= sel + dec
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(num_q_heads=7), 1),          # Hq not a multiple of Hkv
+    (dict(num_q_heads=6, num_kv_heads=2), 2),   # G = 3
+    (dict(head_dim=96), 2),
+    (dict(block_size=32), 2),
+    (dict(rank=17), 2),
+    (dict(rank=-1), 1),
+    (dict(max_seq_len=4000), 1),       # not a multiple of L
+    (dict(budget=-1), 1),
+    (dict(softmax_scale=-1.0), 1),
+    (dict(max_seq_len=64 * 8193), 2),
+])
+def test_invalid_configs_are_rejected(over, code):
+    cfg = _cfg(**over).c_struct()
+    lib = cobs.lib()
+    assert lib.cobs_record_bytes(ctypes.byref(cfg)) == 0
+    st = lib.cobs_select(ctypes.byref(cfg), ctypes.c_void_p(16), ctypes.c_void_p(16), ctypes.c_void_p(16),
+                         ctypes.c_void_p(16), None, ctypes.c_void_p(256), 1 << 30, None)
+    assert st == code
+
+
+def test_null_and_workspace_errors_on_host():
+    lib = cobs.lib()
+    cfg = _cfg().c_struct()
+    fake = ctypes.c_void_p(1 << 20)
+    # null q
+    assert lib.cobs_select(ctypes.byref(cfg), None, fake, fake, fake, None, fake, 1 << 30, None) == 1
+    # workspace too small / misaligned
+    assert lib.cobs_select(ctypes.byref(cfg), fake, fake, fake, fake, None, fake, 16, None) == 3
+    assert lib.cobs_select(ctypes.byref(cfg), fake, fake, fake, fake, None, ctypes.c_void_p((1 << 20) + 8),
+                           1 << 30, None) == 3
+    # misaligned KV / bad strides
+    kv = cobs._KV(fake.value + 2, fake.value, 0, 0, 128, None, 0)
+    assert lib.cobs_sparse_decode(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, fake, fake, None, fake,
+                                  1 << 30, None) == 1
+    kv = cobs._KV(fake.value, fake.value, 0, 0, 100, None, 0)       # stride_t < d
+    assert lib.cobs_sparse_decode(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, fake, fake, None, fake,
+                                  1 << 30, None) == 1
+    # block range outside the cache
+    kv = cobs._KV(fake.value, fake.value, 0, 0, 128, None, 0)
+    assert lib.cobs_build_block_stats(ctypes.byref(cfg), ctypes.byref(kv), fake, 60, 10, fake, None, 0,
+                                      None) == 1
+    assert lib.cobs_pack_e2m1(fake, 4, 3, fake, fake, None) == 1
+    assert lib.cobs_status_string(3).startswith(b"COBS_ERR_WORKSPACE")
