@@ -124,22 +124,55 @@ __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2
   m = mn;
 }
 
-// Release this workgroup's global writes and count its arrival on `counter`;
-// returns true (in every thread) for the last of `expected` arrivals, which
-// then sees every other workgroup's writes.  The last arrival resets the counter.
+// Cross-workgroup data (per-workgroup partials, per-block scores) is written
+// with agent-scope write-through stores and read back with agent-scope loads,
+// so it is coherent across the XCDs' L2 caches without an L2 write-back or
+// invalidate (which a device-scope fence would cost every workgroup).
+__device__ __forceinline__ void st_agent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_agent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Count this workgroup's arrival on `counter` once its write-through stores
+// have been acknowledged; returns true (in every thread) for the last of
+// `expected` arrivals, which may then read every other workgroup's data with
+// ld_agent.  The last arrival resets the counter for the next launch.
 __device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected, int* sflag) {
-  __threadfence();
-  __syncthreads();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);          // this wave's stores are complete
+  __syncthreads();                        // ... and every other wave's
   if (threadIdx.x == 0) {
-    unsigned prev = atomicAdd(counter, 1u);
-    int last = (prev == expected - 1u) ? 1 : 0;
-    if (last) atomicExch(counter, 0u);     // every other arrival has happened
+    const unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = (prev == expected - 1u) ? 1 : 0;
+    if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     *sflag = last;
   }
   __syncthreads();
-  bool last = *sflag != 0;
-  if (last) __threadfence();
-  return last;
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  return *sflag != 0;
+}
+
+}  // namespace cobs
+
+namespace cobs {
+
+// Order LDS accesses of one wavefront: every lane's earlier LDS writes are
+// visible to the wave's later LDS reads.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Sum over each row of 16 lanes, result in every lane of the row (DPP only).
+__device__ __forceinline__ float row16_sum(float x) {
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));  // xor 1
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // xor 2
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false)); // half mirror
+  x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false)); // mirror
+  return x;
 }
 
 }  // namespace cobs

@@ -5,8 +5,9 @@
 // Grid (chunks, Hkv, B), 256 threads.  Each workgroup scores `bpw` consecutive
 // blocks of one (batch row, KV head): 16 lanes share one block, each lane
 // owning d/16 contiguous elements of every stored vector, so a vector is read
-// as one contiguous segment.  The lanes' partial dot products for the G query
-// heads are combined by a 16-lane butterfly.  Every workgroup writes its
+// as one contiguous segment; all of a block's loads are issued before its
+// arithmetic.  The lanes' partial dot products for the G query heads are
+// combined by a 16-lane DPP reduction.  Every workgroup writes its
 // l_b^g values and a per-head (max, sum exp) partial to the workspace; the
 // last workgroup of the unit to arrive merges the partials in chunk order into
 // ln Z^g, forms sigma_b = ln sum_g exp(l_b^g - ln Z^g) for the candidates and
@@ -19,34 +20,46 @@ namespace cobs {
 constexpr int kSelThreads = 256;
 
 
-// Load the EPL elements [ln*EPL, ln*EPL + EPL) of a stored vector as floats
-// (E2M1 without its scale).
+// Raw bytes of one lane's slice of a stored vector: elements
+// [ln*EPL, ln*EPL + EPL), up to 32 bytes (fp32 at d = 128).
 template <int EPL>
-__device__ __forceinline__ void load_lane_vec(const uint8_t* v, int dt, int ln, float* x) {
+__device__ __forceinline__ void load_slice(const uint8_t* v, int dt, int ln, uint4* raw) {
   if (dt == DT_F32) {
-    const float4* s = reinterpret_cast<const float4*>(v) + ln * (EPL / 4);
+    const uint4* s = reinterpret_cast<const uint4*>(v) + ln * (EPL / 4);
+#pragma unroll
+    for (int k = 0; k < EPL / 4; ++k) raw[k] = s[k];
+  } else if (dt == DT_BF16) {
+    if constexpr (EPL == 8) raw[0] = reinterpret_cast<const uint4*>(v)[ln];
+    else { const uint2 a = reinterpret_cast<const uint2*>(v)[ln]; raw[0].x = a.x; raw[0].y = a.y; }
+  } else {
+    if constexpr (EPL == 8) raw[0].x = reinterpret_cast<const uint32_t*>(v)[ln];
+    else raw[0].x = reinterpret_cast<const uint16_t*>(v)[ln];
+  }
+}
+
+// Slice bytes -> EPL floats (E2M1 without its scale; hardware FP4 convert).
+template <int EPL>
+__device__ __forceinline__ void unpack_slice(const uint4* raw, int dt, float* x) {
+  if (dt == DT_F32) {
 #pragma unroll
     for (int k = 0; k < EPL / 4; ++k) {
-      const float4 a = s[k];
-      x[4 * k] = a.x; x[4 * k + 1] = a.y; x[4 * k + 2] = a.z; x[4 * k + 3] = a.w;
+      x[4 * k] = __uint_as_float(raw[k].x); x[4 * k + 1] = __uint_as_float(raw[k].y);
+      x[4 * k + 2] = __uint_as_float(raw[k].z); x[4 * k + 3] = __uint_as_float(raw[k].w);
     }
   } else if (dt == DT_BF16) {
-    const uint32_t* s = reinterpret_cast<const uint32_t*>(v) + ln * (EPL / 2);
-    if constexpr (EPL == 8) {
-      const uint4 a = *reinterpret_cast<const uint4*>(s);
-      const uint32_t u[4] = {a.x, a.y, a.z, a.w};
+    const uint32_t u[4] = {raw[0].x, raw[0].y, raw[0].z, raw[0].w};
 #pragma unroll
-      for (int k = 0; k < 4; ++k) { x[2 * k] = bf16_lo(u[k]); x[2 * k + 1] = bf16_hi(u[k]); }
-    } else {
-      const uint2 a = *reinterpret_cast<const uint2*>(s);
-      x[0] = bf16_lo(a.x); x[1] = bf16_hi(a.x); x[2] = bf16_lo(a.y); x[3] = bf16_hi(a.y);
-    }
+    for (int k = 0; k < EPL / 2; ++k) { x[2 * k] = bf16_lo(u[k]); x[2 * k + 1] = bf16_hi(u[k]); }
   } else {
-    uint32_t u;
-    if constexpr (EPL == 8) u = reinterpret_cast<const uint32_t*>(v)[ln];
-    else u = reinterpret_cast<const uint16_t*>(v)[ln];
-#pragma unroll
-    for (int k = 0; k < EPL; ++k) x[k] = e2m1_value((u >> (4 * k)) & 15u);
+    const uint32_t u = raw[0].x;
+    const auto f0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(u, 1.0f, 0);
+    const auto f1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(u, 1.0f, 1);
+    x[0] = f0[0]; x[1] = f0[1]; x[2] = f1[0]; x[3] = f1[1];
+    if constexpr (EPL == 8) {
+      const auto f2 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(u, 1.0f, 2);
+      const auto f3 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(u, 1.0f, 3);
+      x[4] = f2[0]; x[5] = f2[1]; x[6] = f3[0]; x[7] = f3[1];
+    }
   }
 }
 
@@ -67,7 +80,7 @@ __device__ int block_excl_scan(int v, int* sh, int* total) {
   return incl - v;
 }
 
-template <int D, int G>
+template <int D, int G, int RMAX>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
   constexpr int EPL = D / 16;
   __shared__ float gm[16][G], gs[16][G];
@@ -98,42 +111,55 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
   for (int g = 0; g < G; ++g) { run_m[g] = -INFINITY; run_s[g] = 0.0f; }
 
   const int blk_end = min(nb, (chunk + 1) * p.bpw);
+  const int r = p.r;
   for (int blk = chunk * p.bpw + grp; blk < blk_end; blk += 16) {
     const uint8_t* R = p.rec + ((int64_t)unit * p.nbmax + blk) * p.lay.total;
+    // every load of the block's record slice is issued before any arithmetic
     const int n = *reinterpret_cast<const int32_t*>(R);
-    float x[EPL];
-    float lin[G], quad[G];
-    load_lane_vec<EPL>(R + p.lay.mean_off, p.mdt, ln, x);
     const float mscale = (p.mdt == DT_E2M1) ? *reinterpret_cast<const float*>(R + 4) : 1.0f;
+    float fsc[RMAX];
+    uint4 raw[RMAX + 1][2];
+    load_slice<EPL>(R + p.lay.mean_off, p.mdt, ln, raw[0]);
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float a = 0.0f;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) a += x[e] * qv[g][e];
-#pragma unroll
-      for (int o = 8; o >= 1; o >>= 1) a += __shfl_xor(a, o, 16);
-      lin[g] = a * mscale;
-      quad[g] = 0.0f;
+    for (int i = 0; i < RMAX; ++i) {
+      if (i < r) {
+        load_slice<EPL>(R + p.lay.fac_off + i * p.lay.vec_bytes, p.fdt, ln, raw[i + 1]);
+        fsc[i] = (p.fdt == DT_E2M1) ? reinterpret_cast<const float*>(R + 16)[i] : 1.0f;
+      }
     }
-    for (int i = 0; i < p.r; ++i) {
-      load_lane_vec<EPL>(R + p.lay.fac_off + i * p.lay.vec_bytes, p.fdt, ln, x);
-      const float fs = (p.fdt == DT_E2M1) ? reinterpret_cast<const float*>(R + 16)[i] : 1.0f;
+    float lin[G], quad[G];
+    {
+      float x[EPL];
+      unpack_slice<EPL>(raw[0], p.mdt, x);
 #pragma unroll
       for (int g = 0; g < G; ++g) {
         float a = 0.0f;
 #pragma unroll
         for (int e = 0; e < EPL; ++e) a += x[e] * qv[g][e];
+        lin[g] = row16_sum(a) * mscale;
+        quad[g] = 0.0f;
+      }
+    }
 #pragma unroll
-        for (int o = 8; o >= 1; o >>= 1) a += __shfl_xor(a, o, 16);
-        a *= fs;
-        quad[g] += a * a;
+    for (int i = 0; i < RMAX; ++i) {
+      if (i < r) {
+        float x[EPL];
+        unpack_slice<EPL>(raw[i + 1], p.fdt, x);
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          float a = 0.0f;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) a += x[e] * qv[g][e];
+          a = row16_sum(a) * fsc[i];
+          quad[g] += a * a;
+        }
       }
     }
     const float lnn = logf((float)n);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const float l = lnn + lin[g] + 0.5f * quad[g];
-      if (ln == 0) p.ell[((int64_t)unit * G + g) * p.nbmax + blk] = l;
+      if (ln == 0) st_agent(&p.ell[((int64_t)unit * G + g) * p.nbmax + blk], l);
       lse_merge(run_m[g], run_s[g], l, 1.0f);
     }
   }
@@ -146,8 +172,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
     float m = -INFINITY, s = 0.0f;
     for (int k = 0; k < 16; ++k) lse_merge(m, s, gm[k][tid], gs[k][tid]);
     float* pp = p.part + (((int64_t)unit * p.nch + chunk) * G + tid) * 2;
-    pp[0] = m;
-    pp[1] = s;
+    st_agent(&pp[0], m);
+    st_agent(&pp[1], s);
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
 
@@ -158,7 +184,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
     float m = -INFINITY, s = 0.0f;
     for (int ch = slot; ch < p.nch; ch += SLOTS) {
       const float* pp = p.part + (((int64_t)unit * p.nch + ch) * G + g) * 2;
-      lse_merge(m, s, pp[0], pp[1]);
+      lse_merge(m, s, ld_agent(&pp[0]), ld_agent(&pp[1]));
     }
     redm[tid] = m;
     reds[tid] = s;
@@ -186,7 +212,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
       float mx = -INFINITY;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        v[g] = p.ell[((int64_t)unit * G + g) * p.nbmax + blk] - lse_s[g];
+        v[g] = ld_agent(&p.ell[((int64_t)unit * G + g) * p.nbmax + blk]) - lse_s[g];
         mx = fmaxf(mx, v[g]);
       }
       float acc = 0.0f;
@@ -278,7 +304,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
 // ------------------------------------------------------------- launchers --
 template <int D, int G>
 static hipError_t launch_select_dg(const SelectParams& p, dim3 grid, hipStream_t st) {
-  hipLaunchKernelGGL((select_kernel<D, G>), grid, dim3(kSelThreads), 0, st, p);
+  if (p.r <= 4) hipLaunchKernelGGL((select_kernel<D, G, 4>), grid, dim3(kSelThreads), 0, st, p);
+  else hipLaunchKernelGGL((select_kernel<D, G, kMaxRank>), grid, dim3(kSelThreads), 0, st, p);
   return hipGetLastError();
 }
 
