@@ -1,18 +1,27 @@
 """Decode-step benchmark of the COBS path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload c2] [--copies M] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload c2] [--copies M]
+                    [--no-cpu-baseline] [--traffic FILE]
 
 One step = one cobs_decode_step call on one layer: refresh of the record of the
 block holding the newest token, block scoring + top-s selection, and sparse
 attention over the selected blocks plus the window, for every batch row and
 KV head.  Inputs are seeded synthetic tensors resident in HBM before timing.
-To measure HBM rather than the 256 MB last-level cache, the timed steps rotate
-over M independent copies of the layer (K/V cache, descriptors, queries) whose
-combined footprint read per step exceeds 2 GB.
 
-Prints one JSON line: the metric (us per decode step per layer), achieved
-GB/s on the step's algorithmic bytes, the roofline of the dominant kernel
-(timed on its own with HIP events on the launch stream) and the fp64 oracle's
+The timed loop is a decode loop: every step appends one token, so the context
+of each layer copy advances by one per step through T_hi-63 .. T_hi (one full
+fill of the newest block, T_hi the workload's context) and wraps; the copies
+start at staggered phases, so over any window of steps one in 64 is the step
+that fills a block and recomputes its covariance factors (the other steps
+refresh the partial block's mean).  To measure HBM rather than the 256 MB
+last-level cache the steps rotate over M independent copies of the layer (K/V
+cache, descriptors, queries) that together read >= 2 GB per sweep.  A sweep
+(one step per copy plus the context advance) is captured once as a HIP graph
+and replayed, so host launch overhead is not in the measurement.
+
+Prints one JSON line: the metric (us per decode step per layer), achieved GB/s
+on the step's algorithmic bytes, the roofline of the dominant kernel (timed on
+its own the same way, HIP events on the launch stream) and the fp64 oracle's
 time on the host cores as a baseline.
 """
 
@@ -35,6 +44,7 @@ from paper_2607_09052_amd import cobs  # noqa: E402
 HBM_PEAK_GBPS = 8000.0
 METRIC = "µs per decode step per layer and achieved HBM GB/s (fraction of peak) at 32k ctx"
 ESZ = {"f32": 4, "bf16": 2}
+CYCLE = 64
 
 
 def vec_bytes(d, dt):
@@ -49,6 +59,7 @@ def descriptor_bytes(cfg):
 
 
 def union_tokens(T, w, sel_row, L=64):
+    """Tokens attended: the window plus the selected blocks' tokens before it."""
     ws = max(0, T - w)
     nc = -(-ws // L)
     n = T - ws
@@ -62,19 +73,21 @@ def union_tokens(T, w, sel_row, L=64):
 
 
 def algorithmic_bytes(cfg, seq_lens, sel):
-    """Per-kernel algorithmic bytes of one decode step, from the actual selection."""
+    """Per-kernel algorithmic bytes of one decode step, from the actual selection.
+
+    select: every block's descriptor (unpadded), q, sel written.
+    decode: K and V of every attended token, q, sel, out and lse written.
+    tail:   the keys of the block holding the newest token, its record written.
+    """
     B, Hkv, Hq, d = cfg.batch, cfg.num_kv_heads, cfg.num_q_heads, cfg.head_dim
     kv = ESZ[cfg.kv_dtype]
     q_bytes = B * Hq * d * 4
     sel_bytes = B * Hkv * cfg.budget * 4
     out_bytes = B * Hq * (d + 1) * 4
-    score = 0
-    dec = 0
-    tail = 0
+    score = dec = tail = 0
     for b in range(B):
         T = int(seq_lens[b])
-        nb = -(-T // 64)
-        score += Hkv * nb * descriptor_bytes(cfg)
+        score += Hkv * (-(-T // 64)) * descriptor_bytes(cfg)
         n_tail = T - (T - 1) // 64 * 64
         tail += Hkv * (n_tail * d * kv + cobs.record_bytes(cfg))
         for h in range(Hkv):
@@ -83,75 +96,85 @@ def algorithmic_bytes(cfg, seq_lens, sel):
                 tail=tail, step=score + dec + tail + q_bytes + sel_bytes + out_bytes)
 
 
-def time_launches(fn, n, stream):
-    """Average duration per call of `fn(i)`, HIP events on the launch stream."""
+def replay_time(graph, reps, stream):
+    """Microseconds per replay of `graph`, HIP events on `stream`."""
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
-    for i in range(n):
-        fn(i)
+    for _ in range(reps):
+        graph.replay()
     end.record(stream)
     torch.cuda.synchronize()
-    return start.elapsed_time(end) * 1e3 / n          # microseconds
+    return start.elapsed_time(end) * 1e3 / reps
 
 
-def cpu_baseline(prob, cfg, budget_s=12.0):
+def capture(fn, stream):
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        fn()
+    return g
+
+
+def cpu_baseline(prob, cfg, t_lo, budget_s=12.0):
     """The fp64 oracle's decode step on the host cores, on a bounded sample.
 
-    Untimed: the oracle builds its own descriptors for the sampled units.
-    Timed per unit: refresh of the tail block's statistics, scoring, top-s
-    and sparse attention.  Scaled to one full step (all units of the layer).
+    Untimed: the oracle builds its own descriptors for two (batch row, KV head)
+    units.  Timed per unit-step, cycling the context through the same block-fill
+    cycle as the GPU loop: refresh of the tail block's statistics (factors
+    when it is full), scoring, top-s and sparse attention.  Scaled to one step
+    of the whole layer (all units).
     """
     from oracle import method as M
     c = prob["cfg"]
     G = c["Hq"] // c["Hkv"]
     units = [(b, h) for b in range(c["B"]) for h in range(c["Hkv"])]
-    T = c["T"]
-    r, L = cfg.rank, 64
+    r, L, T_hi = cfg.rank, 64, c["T"]
     prepared = []
     t_prep = time.time()
     for (b, h) in units[:2]:
-        K = prob["k"][b, h, :T].to("cpu", torch.float64).numpy()
-        V = prob["v"][b, h, :T].to("cpu", torch.float64).numpy()
+        K = prob["k"][b, h, :T_hi].to("cpu", torch.float64).numpy()
+        V = prob["v"][b, h, :T_hi].to("cpu", torch.float64).numpy()
         q = prob["q"][b, h * G:(h + 1) * G].to("cpu", torch.float64).numpy()
-        stats = M.stored_statistics(*M.block_statistics(K, T, L, r), cfg.mean_dtype, cfg.factor_dtype)
+        stats = M.stored_statistics(*M.block_statistics(K, T_hi, L, r), cfg.mean_dtype, cfg.factor_dtype)
         prepared.append((q, K, V, [np.array(x) for x in stats]))
     prep_s = time.time() - t_prep
     n = 0
     t0 = time.time()
     while time.time() - t0 < budget_s:
         q, K, V, stats = prepared[n % len(prepared)]
+        T = t_lo + (n // len(prepared)) % CYCLE
         j = (T - 1) // L
         tail = M.stored_statistics(*M.block_statistics(K[j * L:T], T - j * L, L, r),
                                    cfg.mean_dtype, cfg.factor_dtype)
         for arr, x in zip(stats, tail):
             arr[j] = x[0]
+        nb = -(-T // L)
         M.decode_unit(q, K, V, T, L, r, cfg.budget, cfg.window, cfg.scale, cfg.mean_dtype,
-                      cfg.factor_dtype, stats=tuple(stats))
+                      cfg.factor_dtype, stats=tuple(a[:nb] for a in stats))
         n += 1
     per_unit = (time.time() - t0) / n
     cores = len(os.sched_getaffinity(0))
-    return {"value": per_unit * len(units) * 1e6, "unit": "us/step/layer", "cores": cores,
+    return {"value": round(per_unit * len(units) * 1e6, 1), "unit": "us/step/layer", "cores": cores,
             "kind": "oracle",
-            "sample": f"{n} unit-steps of 2 (batch row, KV head) units at T={T} in {per_unit * n:.1f} s, "
-                      f"scaled x{len(units)} units; descriptor prefill ({prep_s:.1f} s) untimed; "
-                      f"numpy BLAS threads = {cores} host cores"}
+            "sample": f"{n} unit-steps of 2 of the {len(units)} (batch row, KV head) units, T cycling "
+                      f"{t_lo}..{t_lo + CYCLE - 1}, in {per_unit * n:.1f} s, scaled x{len(units)}; "
+                      f"descriptor prefill ({prep_s:.1f} s) untimed; numpy/BLAS on {cores} host cores"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="c2", choices=sorted(synth.CONFIGS))
-    ap.add_argument("--copies", type=int, default=0, help="layer copies to rotate (0: >= 2 GB read)")
+    ap.add_argument("--copies", type=int, default=0, help="layer copies to rotate (0: >= 2 GB per sweep)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--traffic", default="", help="JSON file with rocprofv3 FETCH/WRITE bytes per launch")
+    ap.add_argument("--traffic", default="", help="JSON {kernel: {fetch_bytes, write_bytes}} from rocprofv3")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the decode step shards "
-              "by KV head or batch row with no communication; see the design notes)", file=sys.stderr)
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported here (the decode step "
+              "shards by KV head or batch row with no communication)", file=sys.stderr)
         sys.exit(2)
 
     dev = "cuda:0"
@@ -162,83 +185,106 @@ def main():
     cfg = cobs.Config(batch=c["B"], num_q_heads=c["Hq"], num_kv_heads=c["Hkv"], head_dim=c["d"],
                       max_seq_len=c["T_max"], rank=c["r"], budget=c["s"], window=c["w"],
                       kv_dtype=c["kv_dtype"], mean_dtype=c["mean_dtype"], factor_dtype=c["factor_dtype"])
-    seq = prob["seq_lens"]
+    B, T_hi = c["B"], c["T"]
+    t_lo = T_hi - CYCLE + 1
+    seq_hi = torch.full((B,), T_hi, dtype=torch.int32, device=dev)
     rec = cobs.new_summaries(cfg, dev)
-    cobs.cobs_build_block_stats(cfg, prob["k"], prob["v"], seq, rec)
-    torch.cuda.synchronize()
-
-    # bytes one step reads, then the number of independent copies to rotate
-    sel0 = torch.empty((c["B"], c["Hkv"], c["s"]), dtype=torch.int32, device=dev)
-    out = torch.empty((c["B"], c["Hq"], c["d"]), dtype=torch.float32, device=dev)
-    lse = torch.empty((c["B"], c["Hq"]), dtype=torch.float32, device=dev)
+    cobs.cobs_build_block_stats(cfg, prob["k"], prob["v"], seq_hi, rec)
+    out = torch.empty((B, c["Hq"], c["d"]), dtype=torch.float32, device=dev)
+    lse = torch.empty((B, c["Hq"]), dtype=torch.float32, device=dev)
+    sel = torch.empty((B, c["Hkv"], c["s"]), dtype=torch.int32, device=dev)
     ws = cobs.new_workspace(cfg, cobs.OP_STEP, dev)
-    cobs.cobs_decode_step(cfg, prob["q"], prob["k"], prob["v"], seq, rec, out, ws, sel=sel0, lse=lse)
-    torch.cuda.synchronize()
-    ab = algorithmic_bytes(cfg, seq.tolist(), sel0.cpu())
+
+    # one eager fill cycle: algorithmic bytes of every phase of the loop
+    per_phase = []
+    r_tmp = rec.clone()
+    for ph in range(CYCLE):
+        s_ = torch.full((B,), t_lo + ph, dtype=torch.int32, device=dev)
+        cobs.cobs_decode_step(cfg, prob["q"], prob["k"], prob["v"], s_, r_tmp, out, ws, sel=sel, lse=lse)
+        per_phase.append(algorithmic_bytes(cfg, s_.tolist(), sel.cpu()))
+    del r_tmp
+    ab = {k_: float(np.mean([x[k_] for x in per_phase])) for k_ in per_phase[0]}
+    ab_fill = per_phase[-1]
+
     copies = args.copies or max(2, math.ceil(2e9 / ab["step"]))
     layers = [(prob["q"], prob["k"], prob["v"], rec)]
     for _ in range(copies - 1):
         layers.append(tuple(x.clone() for x in layers[0]))
-    sels = [torch.empty_like(sel0) for _ in layers]
+    seqs = torch.tensor([[t_lo + (i % CYCLE)] * B for i in range(copies)], dtype=torch.int32, device=dev)
+    sels = [torch.empty_like(sel) for _ in layers]
     wss = [cobs.new_workspace(cfg, cobs.OP_STEP, dev) for _ in layers]
-    stream = torch.cuda.current_stream()
-
-    def step(i):
-        q, k, v, r_ = layers[i % copies]
-        cobs.cobs_decode_step(cfg, q, k, v, seq, r_, out, wss[i % copies], sel=sels[i % copies], lse=lse)
-
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for i in range(args.steps):
-        step(i)
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms_step = start.elapsed_time(end) / args.steps
-    us_step = ms_step * 1e3
-
-    # per-kernel durations: each entry point alone, rotating copies the same way
     sel_ws = [cobs.new_workspace(cfg, cobs.OP_SELECT, dev) for _ in layers]
     dec_ws = [cobs.new_workspace(cfg, cobs.OP_DECODE, dev) for _ in layers]
-    n_k = max(args.steps, 50)
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
 
-    def k_select(i):
-        q, k, v, r_ = layers[i % copies]
-        cobs.cobs_select(cfg, q, r_, seq, sels[i % copies], sel_ws[i % copies])
+    def advance():
+        seqs.sub_(t_lo - 1).remainder_(CYCLE).add_(t_lo)
 
-    def k_decode(i):
-        q, k, v, r_ = layers[i % copies]
-        cobs.cobs_sparse_decode(cfg, q, k, v, seq, sels[i % copies], out, dec_ws[i % copies], lse=lse)
+    def sweep_step():
+        for i, (q, k, v, r_) in enumerate(layers):
+            cobs.cobs_decode_step(cfg, q, k, v, seqs[i], r_, out, wss[i], sel=sels[i], lse=lse, stream=stream)
+        advance()
 
-    def k_tail(i):
-        q, k, v, r_ = layers[i % copies]
-        cobs.cobs_build_block_stats(cfg, k, v, seq, r_, first_block=cfg.num_blocks - 1, num_blocks=1)
+    def sweep_select():
+        for i, (q, k, v, r_) in enumerate(layers):
+            cobs.cobs_select(cfg, q, r_, seqs[i], sels[i], sel_ws[i], stream=stream)
 
-    for fn in (k_select, k_decode, k_tail):
-        for i in range(5):
-            fn(i)
-    kern = {"select_kernel": (time_launches(k_select, n_k, stream), ab["select"]),
-            "decode_kernel": (time_launches(k_decode, n_k, stream), ab["decode"]),
-            "build_stats_kernel (tail)": (time_launches(k_tail, n_k, stream), ab["tail"])}
-    dom = max(kern, key=lambda k_: kern[k_][0])
-    dom_us, dom_bytes = kern[dom]
+    def sweep_decode():
+        for i, (q, k, v, r_) in enumerate(layers):
+            cobs.cobs_sparse_decode(cfg, q, k, v, seqs[i], sels[i], out, dec_ws[i], lse=lse, stream=stream)
+
+    def sweep_tail():
+        for i, (q, k, v, r_) in enumerate(layers):
+            cobs.cobs_build_block_stats(cfg, k, v, seqs[i], r_, first_block=cfg.num_blocks - 1, num_blocks=1,
+                                        stream=stream)
+
+    def sweep_fill():
+        for i, (q, k, v, r_) in enumerate(layers):
+            cobs.cobs_decode_step(cfg, q, k, v, seq_hi, r_, out, wss[i], sel=sels[i], lse=lse, stream=stream)
+
+    for fn in (sweep_step, sweep_select, sweep_decode, sweep_tail, sweep_fill):   # eager warm-up
+        fn()
+    torch.cuda.synchronize()
+    g_step = capture(sweep_step, stream)
+    reps_w = max(1, math.ceil(args.warmup / copies))
+    reps = max(1, math.ceil(args.steps / copies))
+    for _ in range(reps_w):
+        g_step.replay()
+    us_sweep = replay_time(g_step, reps, stream)
+    steps = reps * copies
+    us_step = us_sweep / copies
+    # per-kernel averages and the fixed-context fill step, same protocol
+    kern_us = {}
+    for key, fn in (("select_kernel", sweep_select), ("decode_kernel", sweep_decode),
+                    ("build_stats_kernel", sweep_tail)):
+        g = capture(fn, stream)
+        g.replay()
+        kern_us[key] = replay_time(g, max(2, reps // 2), stream) / copies
+    g_fill = capture(sweep_fill, stream)
+    g_fill.replay()
+    fill_us = replay_time(g_fill, max(2, reps // 4), stream) / copies
+    torch.cuda.set_stream(torch.cuda.default_stream())
+
+    kbytes = {"select_kernel": ab["select"], "decode_kernel": ab["decode"], "build_stats_kernel": ab["tail"]}
+    dom = max(kern_us, key=kern_us.get)
+    dom_gbps = kbytes[dom] / (kern_us[dom] * 1e-6) / 1e9
     traffic = None
     if args.traffic and os.path.exists(args.traffic):
         with open(args.traffic) as f:
-            traffic = json.load(f).get(dom.split()[0])
-
+            t = json.load(f).get(dom)
+        if t:
+            traffic = round(t["fetch_bytes"] + t["write_bytes"])
     gbps = ab["step"] / (us_step * 1e-6) / 1e9
     res = {
         "metric": METRIC,
         "value": round(us_step, 3),
         "unit": "us/step/layer",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 6),
+        "steps": steps,
+        "warmup": reps_w * copies,
+        "ms_per_step": round(us_step / 1e3, 6),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -247,21 +293,23 @@ def main():
         "achieved_gbps": round(gbps, 1),
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
         "config": {
-            "workload": f"{name}: B={c['B']} Hq={c['Hq']} Hkv={c['Hkv']} d={c['d']} T={c['T']} L=64 "
-                        f"r={c['r']} s={c['s']} w={c['w']} K/V {c['kv_dtype']}, descriptors "
-                        f"{c['mean_dtype']} mean / {c['factor_dtype']} factors",
-            "bytes_per_step": ab["step"],
+            "workload": f"{name}: B={B} Hq={c['Hq']} Hkv={c['Hkv']} d={c['d']} T={t_lo}..{T_hi} "
+                        f"(decode loop, one block fill per {CYCLE} steps) L=64 r={c['r']} s={c['s']} "
+                        f"w={c['w']}, K/V {c['kv_dtype']}, descriptors {c['mean_dtype']} mean / "
+                        f"{c['factor_dtype']} factors",
+            "bytes_per_step": round(ab["step"]),
             "layer_copies_rotated": copies,
-            "kernels_us": {k_: round(v_[0], 3) for k_, v_ in kern.items()},
+            "kernels_us": {k_: round(v_, 3) for k_, v_ in kern_us.items()},
+            "fill_step_us": round(fill_us, 3),
+            "fill_step_bytes": ab_fill["step"],
         },
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(dom_bytes / (dom_us * 1e-6) / 1e9, 1),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(dom_bytes / (dom_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "algorithmic_bytes": round(kbytes[dom])},
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(prob, cfg)
+        res["cpu_baseline"] = cpu_baseline(prob, cfg, t_lo)
     print(json.dumps(res), flush=True)
 
 

@@ -95,49 +95,74 @@ __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams 
   const int n = min(kL, T - j * kL);
   const int r = p.r;
 
-  // ---- stage keys transposed: KT[e][i] = k_{jL+i}[e]
-  for (int idx = tid; idx < kL * (D / 8); idx += kBuildThreads) {
-    const int i = idx / (D / 8), e0 = (idx % (D / 8)) * 8;
-    float v[8];
+  // ---- load the block's keys into registers: RPP rows per pass, 8 elements per thread
+  constexpr int TPR = D / 8;                       // threads per row
+  constexpr int RPP = kBuildThreads / TPR;         // rows per pass
+  constexpr int NPASS = kL / RPP;
+  const int e0 = (tid % TPR) * 8, r0 = tid / TPR;
+  float v[NPASS][8];
+  double cs[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) v[q] = 0.0f;
-    if (i < n) {
-      const int64_t off = kv_offset(p.kv, b, h, j * kL + i);
-      if (off >= 0) {
-        if (p.kv_f32) {
-          const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(p.kv.k) + off + e0);
-          float4 a = src[0], c = src[1];
-          v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = c.x; v[5] = c.y; v[6] = c.z; v[7] = c.w;
-        } else {
-          uint4 a = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.kv.k) + off + e0);
-          v[0] = bf16_lo(a.x); v[1] = bf16_hi(a.x); v[2] = bf16_lo(a.y); v[3] = bf16_hi(a.y);
-          v[4] = bf16_lo(a.z); v[5] = bf16_hi(a.z); v[6] = bf16_lo(a.w); v[7] = bf16_hi(a.w);
-        }
+  for (int q = 0; q < 8; ++q) cs[q] = 0.0;
+#pragma unroll
+  for (int ps = 0; ps < NPASS; ++ps) {
+    const int i = r0 + ps * RPP;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[ps][q] = 0.0f;
+    const int64_t off = (i < n) ? kv_offset(p.kv, b, h, j * kL + i) : -1;
+    if (off >= 0) {
+      if (p.kv_f32) {
+        const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(p.kv.k) + off + e0);
+        const float4 a = src[0], c = src[1];
+        v[ps][0] = a.x; v[ps][1] = a.y; v[ps][2] = a.z; v[ps][3] = a.w;
+        v[ps][4] = c.x; v[ps][5] = c.y; v[ps][6] = c.z; v[ps][7] = c.w;
+      } else {
+        const uint4 a = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.kv.k) + off + e0);
+        v[ps][0] = bf16_lo(a.x); v[ps][1] = bf16_hi(a.x); v[ps][2] = bf16_lo(a.y); v[ps][3] = bf16_hi(a.y);
+        v[ps][4] = bf16_lo(a.z); v[ps][5] = bf16_hi(a.z); v[ps][6] = bf16_lo(a.w); v[ps][7] = bf16_hi(a.w);
       }
     }
+  }
+  // ---- block mean (first cumulant): fp64 column sums in a fixed order (exact for
+  // the block's fp32 keys unless their magnitudes span > 2^29), one rounding to
+  // fp32, so a block of identical keys centres to exact zeros
 #pragma unroll
-    for (int q = 0; q < 8; ++q) KT[(e0 + q) * KS + i] = v[q];
-  }
+  for (int ps = 0; ps < NPASS; ++ps)
+#pragma unroll
+    for (int q = 0; q < 8; ++q) cs[q] += (double)v[ps][q];
+  double* red64 = reinterpret_cast<double*>(Gm);   // RPP x D doubles, free until the Gram
+#pragma unroll
+  for (int q = 0; q < 8; ++q) red64[r0 * D + e0 + q] = cs[q];
   __syncthreads();
-
-  // ---- block mean (first cumulant): fp64 sum in a fixed order (exact for the
-  // block's fp32 keys unless their magnitudes span > 2^29), one rounding to fp32,
-  // so a block of identical keys centres to exact zeros
   if (tid < D) {
-    double s = 0.0;
-    for (int i = 0; i < n; ++i) s += (double)KT[tid * KS + i];
-    mean[tid] = (float)(s / (double)n);
+    double sum = 0.0;
+    for (int g = 0; g < RPP; ++g) sum += red64[g * D + tid];
+    mean[tid] = (float)(sum / (double)n);
   }
   __syncthreads();
-  for (int idx = tid; idx < D * kL; idx += kBuildThreads) {
-    const int e = idx / kL, i = idx % kL;
-    KT[e * KS + i] = (i < n) ? KT[e * KS + i] - mean[e] : 0.0f;
+  const bool factors = (n == kL) && (r > 0);
+  uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
+  const RecLayout lay = p.lay;
+  if (!factors) {
+    // partial block (or r = 0): count, mean, zero factors
+    for (int idx = tid; idx < lay.mean_off / 4; idx += kBuildThreads)
+      reinterpret_cast<uint32_t*>(R)[idx] = (idx == 0) ? (uint32_t)n : 0u;
+    __syncthreads();
+    store_vector(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), tid, kBuildThreads, red);
+    for (int idx = lay.fac_off / 4 + tid; idx < lay.total / 4; idx += kBuildThreads)
+      reinterpret_cast<uint32_t*>(R)[idx] = 0u;
+    return;
+  }
+  // stage the centred keys transposed: KT[e][i] = k_{jL+i}[e] - kbar[e]
+#pragma unroll
+  for (int ps = 0; ps < NPASS; ++ps) {
+    const int i = r0 + ps * RPP;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) KT[(e0 + q) * KS + i] = v[ps][q] - mean[e0 + q];
   }
   for (int idx = tid; idx < kMaxRank * D; idx += kBuildThreads) Xi[idx] = 0.0f;
   __syncthreads();
-
-  const bool factors = (n == kL) && (r > 0);
-  if (factors) {
+  {
     // ---- Gram matrix Gamma = Kc Kc^T / n, 4x4 tile per thread
     {
       const int i0 = 4 * (tid / 16), j0 = 4 * (tid % 16);
@@ -281,20 +306,15 @@ __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams 
         cur ^= 1;
       }
     }
-    // ---- top-r Ritz values, descending, ties to the lower index
-    if (tid == 0) {
-      float th[P];
-      bool used[P];
-#pragma unroll
-      for (int a = 0; a < P; ++a) { th[a] = Hm[cur][a * (P + 1) + a]; used[a] = false; }
-      for (int i = 0; i < r; ++i) {
-        int best = -1;
-        for (int a = 0; a < P; ++a)
-          if (!used[a] && (best < 0 || th[a] > th[best])) best = a;
-        used[best] = true;
-        order[i] = best;
-        ritzval[i] = th[best];
+    // ---- top-r Ritz values, descending, ties to the lower index (rank by counting)
+    if (tid < P) {
+      const float ta = Hm[cur][tid * (P + 1) + tid];
+      int rank = 0;
+      for (int c = 0; c < P; ++c) {
+        const float tc = Hm[cur][c * (P + 1) + c];
+        rank += (tc > ta) || (tc == ta && c < tid);
       }
+      if (rank < r) { order[rank] = tid; ritzval[rank] = ta; }
     }
     __syncthreads();
     // Ritz vectors w_i = W V[:, order_i] (into Ym), xi_i = Kc^T w_i / sqrt(n)
@@ -345,8 +365,6 @@ __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams 
   }
 
   // ---- write the record
-  uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
-  const RecLayout lay = p.lay;
   for (int idx = tid; idx < lay.mean_off / 4; idx += kBuildThreads) {
     uint32_t v = 0;
     if (idx == 0) v = (uint32_t)n;

@@ -63,21 +63,24 @@ __device__ __forceinline__ void unpack_slice(const uint4* raw, int dt, float* x)
   }
 }
 
-// Exclusive prefix sum over the 256 threads of the workgroup; *total gets the sum.
-__device__ int block_excl_scan(int v, int* sh, int* total) {
-  const int tid = threadIdx.x;
-  sh[tid] = v;
-  __syncthreads();
-  for (int off = 1; off < kSelThreads; off <<= 1) {
-    const int t = (tid >= off) ? sh[tid - off] : 0;
-    __syncthreads();
-    sh[tid] += t;
-    __syncthreads();
+// Exclusive prefix sum over the 256 threads of the workgroup (wave-level
+// shuffle scans, then the four wave totals); *total gets the sum.
+__device__ int block_excl_scan(int v, int* wsum, int* total) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
   }
-  const int incl = sh[tid];
-  *total = sh[kSelThreads - 1];
+  if (lane == 63) wsum[wave] = x;
   __syncthreads();
-  return incl - v;
+  int pre = 0;
+#pragma unroll
+  for (int w = 0; w < kSelThreads / 64; ++w) pre += (w < wave) ? wsum[w] : 0;
+  *total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+  __syncthreads();
+  return pre + x - v;
 }
 
 template <int D, int G, int RMAX>
@@ -88,7 +91,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
   __shared__ float redm[kSelThreads], reds[kSelThreads];
   __shared__ uint32_t keys[kMaxBlocksPerSeq];
   __shared__ int hist[256];
-  __shared__ int scan_buf[kSelThreads];
+  __shared__ int scan_buf[kSelThreads / 64];
   __shared__ int s_digit, s_rem, s_last;
 
   const int tid = threadIdx.x;

@@ -386,3 +386,36 @@ def test_decode_step_is_build_select_decode():
     cobs.cobs_decode_step(cfg, q, k, v, seq, rec1, out3, ws)
     sync()
     assert torch.equal(out1, out3)
+
+
+def test_decode_step_in_a_graph_matches_eager_on_every_replay():
+    """The step enqueues kernels only (no memsets, no allocation): a captured graph
+    replays it exactly, also with eager work and synchronisations in between."""
+    prob = synth.make_problem("c2", seed=41, B=2, Hq=8, Hkv=2, T=4096)
+    cfg = cobs.Config(batch=2, num_q_heads=8, num_kv_heads=2, head_dim=128, max_seq_len=4096, rank=4,
+                      budget=16, window=512)
+    q, k, v = prob["q"].to(DEV), prob["k"].to(DEV), prob["v"].to(DEV)
+    seq = torch.tensor([4096, 3001], dtype=torch.int32, device=DEV)
+    rec = cobs.new_summaries(cfg, DEV)
+    cobs.cobs_build_block_stats(cfg, k, v, seq, rec)
+    ws = cobs.new_workspace(cfg, cobs.OP_STEP, DEV)
+    out_e = torch.empty((2, 8, 128), dtype=torch.float32, device=DEV)
+    sel_e = torch.empty((2, 2, 16), dtype=torch.int32, device=DEV)
+    cobs.cobs_decode_step(cfg, q, k, v, seq, rec, out_e, ws, sel=sel_e)
+    sync()
+    out_g = torch.empty_like(out_e)
+    sel_g = torch.empty_like(sel_e)
+    stream = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        cobs.cobs_decode_step(cfg, q, k, v, seq, rec, out_g, ws, sel=sel_g, stream=stream)
+    for rep in range(4):
+        out_g.zero_()
+        sel_g.fill_(-5)
+        graph.replay()
+        sync()
+        say(f"graph replay {rep}")
+        assert torch.equal(out_g, out_e) and torch.equal(sel_g, sel_e)
+        # eager work between replays, on the same workspace
+        cobs.cobs_decode_step(cfg, q, k, v, seq, rec, out_e, ws, sel=sel_e)
+        sync()
