@@ -78,9 +78,13 @@ Derived derive(const cobs_config_t* c) {
   v.nch = (v.nbmax + v.bpw - 1) / v.bpw;
   // decode: segments = selected blocks + blocks touched by the window
   const int nwin_max = v.w == 0 ? 0 : std::min(v.nbmax, (v.w + kL - 1) / kL + 1);
-  const int nseg = v.s + nwin_max;
+  // work items: segments of <= 64 tokens (fp32 K/V) or pieces of <= 32 (bf16 K/V)
+  const int nseg = (v.kv_f32 ? 1 : 2) * (v.s + nwin_max);
+  // about two workgroups per CU resident at a time, at most kMaxDecodeWg per unit
   v.spw = 4;
-  while (v.spw < 64 && (int64_t)v.units * ((nseg + v.spw - 1) / v.spw) > 4096) v.spw *= 2;
+  while (v.spw < nseg && ((int64_t)v.units * ((nseg + v.spw - 1) / v.spw) > 1024 ||
+                          (nseg + v.spw - 1) / v.spw > kMaxDecodeWg))
+    v.spw *= 2;
   v.nwg = std::max(1, (nseg + v.spw - 1) / v.spw);
 
   size_t off = 0;

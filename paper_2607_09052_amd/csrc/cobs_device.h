@@ -10,6 +10,7 @@ constexpr int kL = 64;          // tokens per block (one token per lane of a wav
 constexpr int kMaxG = 16;       // query heads per KV head
 constexpr int kMaxRank = 16;
 constexpr int kMaxBlocksPerSeq = 8192;   // T_max / L bound for the in-LDS top-s
+constexpr int kMaxDecodeWg = 64;         // decode workgroups (partials) per (batch row, KV head)
 
 enum Dtype : int { DT_F32 = 0, DT_BF16 = 1, DT_E2M1 = 2 };
 

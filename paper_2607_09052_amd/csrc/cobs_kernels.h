@@ -36,7 +36,7 @@ struct DecodeParams {
   float* lse;
   float* part;      // [B*Hkv][nwg][G][D + 2]
   unsigned* cnt;    // [B*Hkv]
-  int hkv, hq, tmax, s, w, nwg, spw;
+  int hkv, hq, tmax, s, w, nwg, spw;   // spw: work items (segments or pieces) per workgroup
   float c;
 };
 

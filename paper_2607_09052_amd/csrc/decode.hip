@@ -36,6 +36,49 @@ __device__ __forceinline__ void unpack16(const uint4& u, float* x) {
   }
 }
 
+// Last workgroup of a unit: merge the unit's nwg (<= kMaxDecodeWg) partials
+// (max, sum, unnormalised output per head) and write out and lse.  Every
+// partial's statistics are loaded at once; the output sums run over the
+// partials in workgroup order with their loads issued ahead.
+template <int D, int G>
+__device__ void merge_partials(const DecodeParams& p, int unit, int b, int h) {
+  __shared__ float fk[kMaxDecodeWg][G];
+  __shared__ float mk[kMaxDecodeWg][G], lk[kMaxDecodeWg][G];
+  __shared__ float Mg[G], Lg[G];
+  const int tid = threadIdx.x;
+  const int nwg = p.nwg;
+  const float* up = p.part + (int64_t)unit * nwg * G * (D + 2);
+  for (int idx = tid; idx < nwg * G; idx += kDecThreads) {
+    const int k = idx / G, g = idx % G;
+    mk[k][g] = ld_agent(&up[(k * G + g) * (D + 2)]);
+    lk[k][g] = ld_agent(&up[(k * G + g) * (D + 2) + 1]);
+  }
+  __syncthreads();
+  if (tid < G) {
+    float M = -INFINITY;
+    for (int k = 0; k < nwg; ++k) M = fmaxf(M, mk[k][tid]);
+    float L = 0.0f;
+    for (int k = 0; k < nwg; ++k) {
+      const float f = (M == -INFINITY || mk[k][tid] == -INFINITY) ? 0.0f : __expf(mk[k][tid] - M);
+      fk[k][tid] = f;
+      L += f * lk[k][tid];
+    }
+    Mg[tid] = M;
+    Lg[tid] = L;
+  }
+  __syncthreads();
+  for (int idx = tid; idx < G * D; idx += kDecThreads) {
+    const int g = idx / D, dd = idx % D;
+    float acc = 0.0f;
+#pragma unroll 8
+    for (int k = 0; k < nwg; ++k) acc += fk[k][g] * ld_agent(&up[(k * G + g) * (D + 2) + 2 + dd]);
+    const float L = Lg[g];
+    const int64_t oq = (int64_t)b * p.hq + h * G + g;
+    p.out[oq * D + dd] = (L > 0.0f) ? acc / L : 0.0f;
+    if (dd == 0 && p.lse) p.lse[oq] = (L > 0.0f) ? Mg[g] + logf(L) : -INFINITY;
+  }
+}
+
 template <int D, int G, bool F32>
 __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
   constexpr int ES = F32 ? 4 : 2;            // element bytes
@@ -228,34 +271,251 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
 
-  // ---- last workgroup: merge all partials of the unit in workgroup order
-  const float* up = p.part + (int64_t)unit * p.nwg * G * (D + 2);
+  merge_partials<D, G>(p, unit, b, h);
+}
+
+// ---------------------------------------------------------------------------
+// bf16 K/V: scores on the matrix cores.
+//
+// Work unit: a piece of at most 32 tokens (half of a segment); piece 2*i + hf is
+// half hf of segment i.  For a piece the wave issues its K loads directly in the
+// operand layout of v_mfma_f32_16x16x32_bf16 (A[m][k]: lane l holds row
+// 16*mt + l%16, columns 32*kk + 8*(l/16) .. +7) and its V loads as
+// row-contiguous 16-byte chunks.  The query block (G heads, scaled by c, padded
+// to 16 columns) is the B operand, split into bf16 high and low parts so the two
+// products sum to the fp32 query within 2^-16 relative.  The 16 x 16 score tile
+// lands with lane l holding tokens 16*mt + 4*(l/16) + i of head l % 16, so the
+// softmax statistics of head h live in the lanes with l % 16 == h.
+// Probabilities go through LDS to the V layout, where each lane accumulates its
+// 8 output columns for every head.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
+
+template <int D, int G>
+__global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p) {
+  static_assert(G <= 16, "at most 16 query heads per KV head");
+  constexpr int KST = D / 32;                 // k-steps of the score product
+  constexpr int CPR = D / 8;                  // 16-byte chunks per row (bf16)
+  constexpr int RPI = 64 / CPR;               // V rows per load instruction
+  constexpr int PT = 32;                      // tokens per piece
+  constexpr int VC = PT / RPI;                // V chunks per lane per piece
+  constexpr int GP = (G + 3) / 4 * 4;
+
+  __shared__ __align__(16) float qs[G][D];
+  __shared__ __align__(16) float ps[4][PT][GP];
+  __shared__ float wm[4][G], wl[4][G];
+  __shared__ __align__(16) float wo[4][G][D];
+  __shared__ int s_last, s_kvalid;
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int b = blockIdx.z, h = blockIdx.y, wg = blockIdx.x;
+  const int unit = b * p.hkv + h;
+  const int T = clamp_len(p.seq_lens[b], p.tmax);
+  const int ws = max(0, T - p.w);
+  const int nc = (ws + kL - 1) / kL;
+  const int nwin = (T > ws) ? ((T - 1) / kL - ws / kL + 1) : 0;
+  const int npiece = 2 * (p.s + nwin);
+
+  for (int idx = tid; idx < G * D; idx += kDecThreads)
+    qs[idx / D][idx % D] = p.q[((int64_t)b * p.hq + h * G) * D + idx] * p.c;
+  const int32_t* sl = p.sel + (int64_t)unit * p.s;
+  if (tid == 0) s_kvalid = p.s;
+  __syncthreads();
+  for (int i = tid; i < p.s; i += kDecThreads) {
+    const int bi = sl[i];
+    if (bi < 0 || bi >= nc || (i > 0 && bi <= sl[i - 1])) atomicMin(&s_kvalid, i);
+  }
+  __syncthreads();
+  const int kvalid = s_kvalid;
+
+  // B operands: query head l % 16 (zero beyond G), columns 32*kk + 8*(l/16) + j
+  const int hcol = lane & 15, lgrp = lane >> 4;
+  bf16x8_t qhi[KST], qlo[KST];
+#pragma unroll
+  for (int kk = 0; kk < KST; ++kk) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float x = (hcol < G) ? qs[hcol < G ? hcol : 0][32 * kk + 8 * lgrp + j] : 0.0f;
+      const uint32_t hb = f32_to_bf16_rne(x);
+      const uint32_t lb = f32_to_bf16_rne(x - __uint_as_float(hb << 16));
+      qhi[kk][j] = __builtin_bit_cast(__bf16, (uint16_t)hb);
+      qlo[kk][j] = __builtin_bit_cast(__bf16, (uint16_t)lb);
+    }
+  }
+
+  const char* kbase = static_cast<const char*>(p.kv.k);
+  const char* vbase = static_cast<const char*>(p.kv.v);
+  const int vchunk = lane % CPR, vrow0 = lane / CPR;
+
+  float m_run = -INFINITY, l_run = 0.0f;      // statistics of head hcol
+  float o[G][8];
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[g][e] = 0.0f;
+
+  const int pc_end = min(npiece, (wg + 1) * p.spw);
+  for (int pc = wg * p.spw + wave; pc < pc_end; pc += 4) {
+    const int seg = pc >> 1, half = pc & 1;
+    int t0 = 0, t1 = 0;
+    if (seg < p.s) {
+      if (seg < kvalid) {
+        t0 = sl[seg] * kL;
+        t1 = min(t0 + kL, ws);
+      }
+    } else {
+      const int jb = ws / kL + (seg - p.s);
+      t0 = max(ws, jb * kL);
+      t1 = min(T, jb * kL + kL);
+    }
+    const int a0 = t0 + PT * half;
+    const int n = min(t1 - a0, PT);
+    if (n <= 0) continue;
+
+    // ---- loads: K in the MFMA A layout, V as row chunks
+    uint4 kr[2][KST];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      const int row = 16 * mt + hcol;
+      const int64_t off = (row < n) ? kv_offset(p.kv, b, h, a0 + row) : -1;
+#pragma unroll
+      for (int kk = 0; kk < KST; ++kk)
+        kr[mt][kk] = (off >= 0) ? *reinterpret_cast<const uint4*>(kbase + off * 2 + 64 * kk + 16 * lgrp)
+                                : make_uint4(0, 0, 0, 0);
+    }
+    uint4 vr[VC];
+#pragma unroll
+    for (int i = 0; i < VC; ++i) {
+      const int row = vrow0 + RPI * i;
+      const int64_t off = (row < n) ? kv_offset(p.kv, b, h, a0 + row) : -1;
+      vr[i] = (off >= 0) ? reinterpret_cast<const uint4*>(vbase + off * 2)[vchunk] : make_uint4(0, 0, 0, 0);
+    }
+
+    // ---- scores S[token][head] on the matrix cores
+    f32x4_t sc[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int kk = 0; kk < KST; ++kk) {
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[mt][kk]), qhi[kk], acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[mt][kk]), qlo[kk], acc, 0, 0, 0);
+      }
+      sc[mt] = acc;
+    }
+    // ---- streaming softmax (head hcol; replicated over the four lane groups)
+    float mx = -INFINITY;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (16 * mt + 4 * lgrp + i >= n) sc[mt][i] = -INFINITY;
+        mx = fmaxf(mx, sc[mt][i]);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m_run, mx);
+    const float alpha = (m_run == -INFINITY) ? 0.0f : __expf(m_run - mn);
+    float ls = 0.0f;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float pr = (sc[mt][i] == -INFINITY) ? 0.0f : __expf(sc[mt][i] - mn);
+        sc[mt][i] = pr;
+        ls += pr;
+      }
+    ls += __shfl_xor(ls, 16, 64);
+    ls += __shfl_xor(ls, 32, 64);
+    l_run = l_run * alpha + ls;
+    m_run = mn;
+    if (hcol < G) {
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ps[wave][16 * mt + 4 * lgrp + i][hcol] = sc[mt][i];
+    }
+    // every head's accumulator is rescaled by its own alpha (held by lane g)
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const float ag = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), g));
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[g][e] *= ag;
+    }
+    wave_lds_sync();
+    // ---- values
+#pragma unroll
+    for (int i = 0; i < VC; ++i) {
+      const int row = vrow0 + RPI * i;
+      float vf[8];
+      unpack16<false>(vr[i], vf);
+      float pg[GP];
+#pragma unroll
+      for (int g = 0; g < GP; g += 4) {
+        const float4 pp = *reinterpret_cast<const float4*>(&ps[wave][row][g]);
+        pg[g] = pp.x; pg[g + 1] = pp.y; pg[g + 2] = pp.z; pg[g + 3] = pp.w;
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] += pg[g] * vf[e];
+    }
+    wave_lds_sync();
+  }
+
+  // ---- combine the lanes sharing a column chunk, then the four waves
+#pragma unroll
+  for (int mask = CPR; mask < 64; mask <<= 1)
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[g][e] += __shfl_xor(o[g][e], mask, 64);
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const float mg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m_run), g));
+    const float lg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(l_run), g));
+    if (lane == 0) { wm[wave][g] = mg; wl[wave][g] = lg; }
+  }
+  if (lane < CPR) {
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) wo[wave][g][lane * 8 + e] = o[g][e];
+  }
+  __syncthreads();
+  float* wpart = p.part + ((int64_t)unit * p.nwg + wg) * G * (D + 2);
   for (int idx = tid; idx < G * D; idx += kDecThreads) {
     const int g = idx / D, dd = idx % D;
     float M = -INFINITY;
-    for (int k = 0; k < p.nwg; ++k) M = fmaxf(M, ld_agent(&up[(k * G + g) * (D + 2)]));
+#pragma unroll
+    for (int k = 0; k < 4; ++k) M = fmaxf(M, wm[k][g]);
     float acc = 0.0f, lsum = 0.0f;
     if (M != -INFINITY) {
-      for (int k = 0; k < p.nwg; ++k) {
-        const float* pk = up + (k * G + g) * (D + 2);
-        const float mk = ld_agent(&pk[0]);
-        if (mk == -INFINITY) continue;
-        const float f = __expf(mk - M);
-        lsum += f * ld_agent(&pk[1]);
-        acc += f * ld_agent(&pk[2 + dd]);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float f = (wm[k][g] == -INFINITY) ? 0.0f : __expf(wm[k][g] - M);
+        acc += f * wo[k][g][dd];
+        lsum += f * wl[k][g];
       }
     }
-    const int64_t oq = (int64_t)b * p.hq + h * G + g;
-    p.out[oq * D + dd] = (lsum > 0.0f) ? acc / lsum : 0.0f;
-    if (dd == 0 && p.lse) p.lse[oq] = (lsum > 0.0f) ? M + logf(lsum) : -INFINITY;
+    st_agent(&wpart[g * (D + 2) + 2 + dd], acc);
+    if (dd == 0) {
+      st_agent(&wpart[g * (D + 2)], M);
+      st_agent(&wpart[g * (D + 2) + 1], lsum);
+    }
   }
+  if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
+  merge_partials<D, G>(p, unit, b, h);
 }
 
 // ------------------------------------------------------------- launchers --
 template <int D, int G>
 static hipError_t launch_decode_dg(const DecodeParams& p, bool f32, dim3 grid, hipStream_t st) {
   if (f32) hipLaunchKernelGGL((decode_kernel<D, G, true>), grid, dim3(kDecThreads), 0, st, p);
-  else hipLaunchKernelGGL((decode_kernel<D, G, false>), grid, dim3(kDecThreads), 0, st, p);
+  else hipLaunchKernelGGL((decode_mfma_kernel<D, G>), grid, dim3(kDecThreads), 0, st, p);
   return hipGetLastError();
 }
 
