@@ -73,8 +73,11 @@ Derived derive(const cobs_config_t* c) {
   v.lay = rec_layout(v.d, v.r, v.mdt, v.fdt);
 
   // selector: enough workgroups to cover the chip, at least 16 blocks each
-  v.bpw = 16;
-  while (v.bpw < 256 && (int64_t)v.units * ((v.nbmax + v.bpw - 1) / v.bpw) > 2048) v.bpw *= 2;
+  // (the matrix-core scorer for bf16 / E2M1 descriptors takes 16 blocks per wave)
+  const bool mfma_sel = v.mdt != DT_F32 && v.fdt != DT_F32;
+  v.bpw = mfma_sel ? 64 : 16;
+  while (v.bpw < 256 && (int64_t)v.units * ((v.nbmax + v.bpw - 1) / v.bpw) > (mfma_sel ? 1024 : 2048))
+    v.bpw *= 2;
   v.nch = (v.nbmax + v.bpw - 1) / v.bpw;
   // decode: segments = selected blocks + blocks touched by the window
   const int nwin_max = v.w == 0 ? 0 : std::min(v.nbmax, (v.w + kL - 1) / kL + 1);

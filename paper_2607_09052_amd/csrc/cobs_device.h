@@ -138,8 +138,9 @@ __device__ __forceinline__ float ld_agent(const float* p) {
 
 // Count this workgroup's arrival on `counter` once its write-through stores
 // have been acknowledged; returns true (in every thread) for the last of
-// `expected` arrivals, which may then read every other workgroup's data with
-// ld_agent.  The last arrival resets the counter for the next launch.
+// `expected` arrivals.  The last arrival resets the counter for the next launch
+// and performs one agent-scope acquire (this XCD's caches drop stale lines), so
+// it may read every other workgroup's write-through data with ordinary loads.
 __device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected, int* sflag) {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __builtin_amdgcn_s_waitcnt(0);          // this wave's stores are complete
@@ -151,8 +152,10 @@ __device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected
     *sflag = last;
   }
   __syncthreads();
+  const bool last = *sflag != 0;
+  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  return *sflag != 0;
+  return last;
 }
 
 }  // namespace cobs

@@ -50,8 +50,8 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h) {
   const float* up = p.part + (int64_t)unit * nwg * G * (D + 2);
   for (int idx = tid; idx < nwg * G; idx += kDecThreads) {
     const int k = idx / G, g = idx % G;
-    mk[k][g] = ld_agent(&up[(k * G + g) * (D + 2)]);
-    lk[k][g] = ld_agent(&up[(k * G + g) * (D + 2) + 1]);
+    mk[k][g] = up[(k * G + g) * (D + 2)];
+    lk[k][g] = up[(k * G + g) * (D + 2) + 1];
   }
   __syncthreads();
   if (tid < G) {
@@ -71,7 +71,7 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h) {
     const int g = idx / D, dd = idx % D;
     float acc = 0.0f;
 #pragma unroll 8
-    for (int k = 0; k < nwg; ++k) acc += fk[k][g] * ld_agent(&up[(k * G + g) * (D + 2) + 2 + dd]);
+    for (int k = 0; k < nwg; ++k) acc += fk[k][g] * up[(k * G + g) * (D + 2) + 2 + dd];
     const float L = Lg[g];
     const int64_t oq = (int64_t)b * p.hq + h * G + g;
     p.out[oq * D + dd] = (L > 0.0f) ? acc / L : 0.0f;
