@@ -74,7 +74,7 @@ Derived derive(const cobs_config_t* c) {
 
   // selector: enough workgroups to cover the chip, at least 16 blocks each
   // (the matrix-core scorer for bf16 / E2M1 descriptors takes 16 blocks per wave)
-  const bool mfma_sel = v.mdt != DT_F32 && v.fdt != DT_F32;
+  const bool mfma_sel = select_on_matrix_cores(v.mdt, v.fdt);
   v.bpw = mfma_sel ? 64 : 16;
   while (v.bpw < 256 && (int64_t)v.units * ((v.nbmax + v.bpw - 1) / v.bpw) > (mfma_sel ? 1024 : 2048))
     v.bpw *= 2;

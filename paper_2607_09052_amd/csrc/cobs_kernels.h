@@ -19,7 +19,7 @@ struct SelectParams {
   const int32_t* seq_lens;
   int32_t* sel;
   float* scores;
-  float* ell;       // [B*Hkv][G][nbmax]
+  float* ell;       // [B*Hkv][nbmax][G]
   float* part;      // [B*Hkv][nch][G][2]
   unsigned* cnt;    // [B*Hkv]
   int hkv, hq, nbmax, tmax, r, s, w, mdt, fdt, nch, bpw;
@@ -44,6 +44,7 @@ hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st);
 hipError_t launch_pack_e2m1(const float* x, int64_t nvec, int dim, uint8_t* codes, float* scales,
                             hipStream_t st);
 hipError_t launch_select(const SelectParams& p, int d, int g, dim3 grid, hipStream_t st);
+bool select_on_matrix_cores(int mdt, int fdt);
 hipError_t launch_decode(const DecodeParams& p, int d, int g, bool f32, dim3 grid, hipStream_t st);
 
 }  // namespace cobs

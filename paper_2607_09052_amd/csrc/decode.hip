@@ -36,46 +36,140 @@ __device__ __forceinline__ void unpack16(const uint4& u, float* x) {
   }
 }
 
+// Token range of work item `it` (PT tokens per item, kL / PT items per segment):
+// n tokens from the element offset `base` of its first token, consecutive tokens
+// `rs` elements apart.  Segment i < s is selected block sel[i] (only while i is
+// inside the valid selection prefix), cut at the window start; segment s + j is
+// the part of the j-th window block inside the window.  n = 0 for an empty item
+// and for one on an out-of-range page (never dereferenced).
+template <int PT>
+__device__ __forceinline__ void item_range(const DecodeParams& p, int selv, int kvalid, int b, int h,
+                                           int T, int ws, int it, int& n, int64_t& base) {
+  constexpr int IPS = kL / PT;
+  const int seg = it / IPS, part = it % IPS;
+  int t0 = 0, t1 = 0;
+  if (seg < p.s) {
+    if (seg < kvalid) {
+      t0 = selv * kL;
+      t1 = min(t0 + kL, ws);
+    }
+  } else {
+    const int jb = ws / kL + (seg - p.s);
+    t0 = max(ws, jb * kL);
+    t1 = min(T, jb * kL + kL);
+  }
+  const int a0 = t0 + PT * part;
+  n = max(0, min(t1 - a0, PT));
+  base = (n > 0) ? kv_offset(p.kv, b, h, a0) : 0;
+  if (base < 0) { n = 0; base = 0; }
+}
+
+// Prologue shared by the decode kernels: the queries (scaled by c) into LDS
+// when `load_q`, the valid selection prefix (its longest strictly ascending run
+// of candidate ids) and the table of the `cnt` <= kDecThreads work items from
+// `first` on.  The selection, query and validity loads are issued together
+// before the first barrier; the table is complete at the second.
+template <int D, int G, int PT>
+__device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, int h, int T, int ws, int nc,
+                                                int first, int cnt, bool load_q, float (*qs)[D], int* red,
+                                                int* pn_s, int64_t* pbase_s) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int unit = b * p.hkv + h;
+  const int32_t* sl = p.sel + (int64_t)unit * p.s;
+  const int it = first + tid;
+  const int seg = it / (kL / PT);
+  const int selv = (p.s > 0) ? sl[(tid < cnt && seg < p.s) ? seg : 0] : 0;
+  int kv = p.s;                 // first entry breaking the ascending run of candidates
+  for (int i = tid; i < p.s; i += kDecThreads) {
+    const int bi = sl[i], prev = sl[i > 0 ? i - 1 : 0];
+    if (bi < 0 || bi >= nc || (i > 0 && bi <= prev)) kv = min(kv, i);
+  }
+  if (load_q)
+    for (int idx = tid; idx < G * D; idx += kDecThreads)
+      qs[idx / D][idx % D] = p.q[((int64_t)b * p.hq + h * G) * D + idx] * p.c;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) kv = min(kv, __shfl_xor(kv, o, 64));
+  if (lane == 0) red[wave] = kv;
+  __syncthreads();
+  const int kvalid = min(min(red[0], red[1]), min(red[2], red[3]));
+  if (tid < cnt) {
+    int n;
+    int64_t base;
+    item_range<PT>(p, selv, kvalid, b, h, T, ws, it, n, base);
+    pn_s[tid] = n;
+    pbase_s[tid] = base;
+  }
+  __syncthreads();
+}
+
 // Last workgroup of a unit: merge the unit's nwg (<= kMaxDecodeWg) partials
-// (max, sum, unnormalised output per head) and write out and lse.  Every
-// partial's statistics are loaded at once; the output sums run over the
-// partials in workgroup order with their loads issued ahead.
+// (max, sum, unnormalised output per head) in workgroup order and write out and
+// lse.  Thread t owns outputs t + 256 j; the partials' statistics go to LDS
+// while the first KB partials' outputs load into registers in the same round
+// trip, and each thread forms the merge weights of its own heads.
 template <int D, int G>
 __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h) {
-  __shared__ float fk[kMaxDecodeWg][G];
+  constexpr int OPT = (G * D + kDecThreads - 1) / kDecThreads;   // outputs per thread
+  constexpr int KB = (OPT <= 4) ? 16 : 8;                        // partials per load batch
   __shared__ float mk[kMaxDecodeWg][G], lk[kMaxDecodeWg][G];
-  __shared__ float Mg[G], Lg[G];
   const int tid = threadIdx.x;
   const int nwg = p.nwg;
   const float* up = p.part + (int64_t)unit * nwg * G * (D + 2);
+  float ov[KB][OPT];
+  auto load_batch = [&](int k0) {
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      const int kc = min(k0 + k, nwg - 1);
+#pragma unroll
+      for (int j = 0; j < OPT; ++j) {
+        const int idx = min(tid + kDecThreads * j, G * D - 1);
+        ov[k][j] = up[(kc * G + idx / D) * (D + 2) + 2 + idx % D];
+      }
+    }
+  };
+  load_batch(0);
   for (int idx = tid; idx < nwg * G; idx += kDecThreads) {
     const int k = idx / G, g = idx % G;
-    mk[k][g] = up[(k * G + g) * (D + 2)];
-    lk[k][g] = up[(k * G + g) * (D + 2) + 1];
+    const float2 ml = *reinterpret_cast<const float2*>(&up[(k * G + g) * (D + 2)]);
+    mk[k][g] = ml.x;
+    lk[k][g] = ml.y;
   }
   __syncthreads();
-  if (tid < G) {
-    float M = -INFINITY;
-    for (int k = 0; k < nwg; ++k) M = fmaxf(M, mk[k][tid]);
-    float L = 0.0f;
-    for (int k = 0; k < nwg; ++k) {
-      const float f = (M == -INFINITY || mk[k][tid] == -INFINITY) ? 0.0f : __expf(mk[k][tid] - M);
-      fk[k][tid] = f;
-      L += f * lk[k][tid];
+  float M[OPT], L[OPT], acc[OPT];
+#pragma unroll
+  for (int j = 0; j < OPT; ++j) {
+    const int g = min(tid + kDecThreads * j, G * D - 1) / D;
+    float mx = -INFINITY;
+    for (int k = 0; k < nwg; ++k) mx = fmaxf(mx, mk[k][g]);
+    M[j] = mx;
+    L[j] = 0.0f;
+    acc[j] = 0.0f;
+  }
+  for (int k0 = 0; k0 < nwg; k0 += KB) {
+    if (k0 > 0) load_batch(k0);
+#pragma unroll
+    for (int k = 0; k < KB; ++k) {
+      if (k0 + k < nwg) {
+#pragma unroll
+        for (int j = 0; j < OPT; ++j) {
+          const int g = min(tid + kDecThreads * j, G * D - 1) / D;
+          const float mkg = mk[k0 + k][g];
+          const float f = (M[j] == -INFINITY || mkg == -INFINITY) ? 0.0f : __expf(mkg - M[j]);
+          L[j] += f * lk[k0 + k][g];
+          acc[j] += f * ov[k][j];
+        }
+      }
     }
-    Mg[tid] = M;
-    Lg[tid] = L;
   }
-  __syncthreads();
-  for (int idx = tid; idx < G * D; idx += kDecThreads) {
-    const int g = idx / D, dd = idx % D;
-    float acc = 0.0f;
-#pragma unroll 8
-    for (int k = 0; k < nwg; ++k) acc += fk[k][g] * up[(k * G + g) * (D + 2) + 2 + dd];
-    const float L = Lg[g];
-    const int64_t oq = (int64_t)b * p.hq + h * G + g;
-    p.out[oq * D + dd] = (L > 0.0f) ? acc / L : 0.0f;
-    if (dd == 0 && p.lse) p.lse[oq] = (L > 0.0f) ? Mg[g] + logf(L) : -INFINITY;
+#pragma unroll
+  for (int j = 0; j < OPT; ++j) {
+    const int idx = tid + kDecThreads * j;
+    if (idx < G * D) {
+      const int g = idx / D, dd = idx % D;
+      const int64_t oq = (int64_t)b * p.hq + h * G + g;
+      p.out[oq * D + dd] = (L[j] > 0.0f) ? acc[j] / L[j] : 0.0f;
+      if (dd == 0 && p.lse) p.lse[oq] = (L[j] > 0.0f) ? M[j] + logf(L[j]) : -INFINITY;
+    }
   }
 }
 
@@ -95,7 +189,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
   __shared__ __align__(16) float ps[4][64][GP];
   __shared__ float wm[4][G], wl[4][G];
   __shared__ __align__(16) float wo[4][G][D];
-  __shared__ int s_last, s_kvalid;
+  __shared__ int s_last, s_red[4];
+  __shared__ int pn_s[kDecThreads];
+  __shared__ int64_t pbase_s[kDecThreads];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int b = blockIdx.z, h = blockIdx.y, wg = blockIdx.x;
@@ -105,19 +201,8 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
   const int nc = (ws + kL - 1) / kL;
   const int nwin = (T > ws) ? ((T - 1) / kL - ws / kL + 1) : 0;
   const int nseg = p.s + nwin;
-
-  for (int idx = tid; idx < G * D; idx += kDecThreads)
-    qs[idx / D][idx % D] = p.q[((int64_t)b * p.hq + h * G) * D + idx] * p.c;
-  // the selection used is its longest strictly ascending prefix of candidate ids
-  const int32_t* sl = p.sel + (int64_t)unit * p.s;
-  if (tid == 0) s_kvalid = p.s;
-  __syncthreads();
-  for (int i = tid; i < p.s; i += kDecThreads) {
-    const int bi = sl[i];
-    if (bi < 0 || bi >= nc || (i > 0 && bi <= sl[i - 1])) atomicMin(&s_kvalid, i);
-  }
-  __syncthreads();
-  const int kvalid = s_kvalid;
+  const int seg_lo = wg * p.spw, seg_end = min(nseg, seg_lo + p.spw);
+  const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;        // elements between consecutive tokens
 
   const char* kbase = static_cast<const char*>(p.kv.k);
   const char* vbase = static_cast<const char*>(p.kv.v);
@@ -132,35 +217,26 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
     for (int e = 0; e < EPC; ++e) o[g][e] = 0.0f;
   }
 
-  const int seg_end = min(nseg, (wg + 1) * p.spw);
-  for (int seg = wg * p.spw + wave; seg < seg_end; seg += 4) {
-    int t0 = 0, t1 = 0;
-    if (seg < p.s) {
-      if (seg < kvalid) {
-        t0 = sl[seg] * kL;
-        t1 = min(t0 + kL, ws);
-      }
-    } else {
-      const int jb = ws / kL + (seg - p.s);
-      t0 = max(ws, jb * kL);
-      t1 = min(T, jb * kL + kL);
-    }
-    const int n = t1 - t0;
-    if (n <= 0) continue;
+  for (int sb = seg_lo; sb < seg_end; sb += kDecThreads) {
+   const int cnt = min(kDecThreads, seg_end - sb);
+   decode_prologue<D, G, kL>(p, b, h, T, ws, nc, sb, cnt, sb == seg_lo, qs, s_red, pn_s, pbase_s);
+   for (int it = wave; it < cnt; it += 4) {
+    const int n = pn_s[it];
+    if (n == 0) continue;
+    const int64_t t0off = pbase_s[it];
 
-    // ---- issue the loads: K rows (lane <-> token), V sub-tile 0 (lane <-> chunk)
-    const int64_t koff = (lane < n) ? kv_offset(p.kv, b, h, t0 + lane) : -1;
+    // ---- issue the loads: K rows (lane <-> token), V sub-tile 0 (lane <-> chunk);
+    // rows past n re-read row n - 1 and are masked
+    const int64_t koff = t0off + min(lane, n - 1) * rs;
     uint4 kr[KC];
 #pragma unroll
-    for (int c = 0; c < KC; ++c)
-      kr[c] = (koff >= 0) ? reinterpret_cast<const uint4*>(kbase + koff * ES)[c] : make_uint4(0, 0, 0, 0);
+    for (int c = 0; c < KC; ++c) kr[c] = reinterpret_cast<const uint4*>(kbase + koff * ES)[c];
     uint4 vr[VC];
     auto load_v = [&](int half) {
 #pragma unroll
       for (int i = 0; i < VC; ++i) {
-        const int row = half * VR + vrow0 + RPI * i;
-        const int64_t off = (row < n) ? kv_offset(p.kv, b, h, t0 + row) : -1;
-        vr[i] = (off >= 0) ? reinterpret_cast<const uint4*>(vbase + off * ES)[vchunk] : make_uint4(0, 0, 0, 0);
+        const int row = min(half * VR + vrow0 + RPI * i, n - 1);
+        vr[i] = reinterpret_cast<const uint4*>(vbase + (t0off + row * rs) * ES)[vchunk];
       }
     };
     load_v(0);
@@ -173,8 +249,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
     for (int hf = 0; hf < HALVES; ++hf) {
       if (hf == 1) {
 #pragma unroll
-        for (int c = 0; c < KC; ++c)
-          kr[c] = (koff >= 0) ? reinterpret_cast<const uint4*>(kbase + koff * ES)[KC + c] : make_uint4(0, 0, 0, 0);
+        for (int c = 0; c < KC; ++c) kr[c] = reinterpret_cast<const uint4*>(kbase + koff * ES)[KC + c];
       }
 #pragma unroll
       for (int c = 0; c < KC; ++c) {
@@ -192,7 +267,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
       }
     }
     // ---- streaming softmax update
-    const bool active = koff >= 0;
+    const bool active = lane < n;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const float sg = active ? sc[g] : -INFINITY;
@@ -228,6 +303,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
       }
     }
     wave_lds_sync();      // ps is rewritten by the next segment
+   }
   }
 
   // ---- combine the lanes sharing a column chunk, then the four waves
@@ -308,7 +384,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p
   __shared__ __align__(16) float ps[4][PT][GP];
   __shared__ float wm[4][G], wl[4][G];
   __shared__ __align__(16) float wo[4][G][D];
-  __shared__ int s_last, s_kvalid;
+  __shared__ int s_last, s_red[4];
+  __shared__ int pn_s[kDecThreads];
+  __shared__ int64_t pbase_s[kDecThreads];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int b = blockIdx.z, h = blockIdx.y, wg = blockIdx.x;
@@ -318,18 +396,11 @@ __global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p
   const int nc = (ws + kL - 1) / kL;
   const int nwin = (T > ws) ? ((T - 1) / kL - ws / kL + 1) : 0;
   const int npiece = 2 * (p.s + nwin);
+  const int pc_lo = wg * p.spw, pc_end = min(npiece, pc_lo + p.spw);
+  const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;        // elements between consecutive tokens
 
-  for (int idx = tid; idx < G * D; idx += kDecThreads)
-    qs[idx / D][idx % D] = p.q[((int64_t)b * p.hq + h * G) * D + idx] * p.c;
-  const int32_t* sl = p.sel + (int64_t)unit * p.s;
-  if (tid == 0) s_kvalid = p.s;
-  __syncthreads();
-  for (int i = tid; i < p.s; i += kDecThreads) {
-    const int bi = sl[i];
-    if (bi < 0 || bi >= nc || (i > 0 && bi <= sl[i - 1])) atomicMin(&s_kvalid, i);
-  }
-  __syncthreads();
-  const int kvalid = s_kvalid;
+  decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pc_lo, max(0, min(kDecThreads, pc_end - pc_lo)), true,
+                            qs, s_red, pn_s, pbase_s);
 
   // B operands: query head l % 16 (zero beyond G), columns 32*kk + 8*(l/16) + j
   const int hcol = lane & 15, lgrp = lane >> 4;
@@ -357,42 +428,31 @@ __global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.0f;
 
-  const int pc_end = min(npiece, (wg + 1) * p.spw);
-  for (int pc = wg * p.spw + wave; pc < pc_end; pc += 4) {
-    const int seg = pc >> 1, half = pc & 1;
-    int t0 = 0, t1 = 0;
-    if (seg < p.s) {
-      if (seg < kvalid) {
-        t0 = sl[seg] * kL;
-        t1 = min(t0 + kL, ws);
-      }
-    } else {
-      const int jb = ws / kL + (seg - p.s);
-      t0 = max(ws, jb * kL);
-      t1 = min(T, jb * kL + kL);
-    }
-    const int a0 = t0 + PT * half;
-    const int n = min(t1 - a0, PT);
-    if (n <= 0) continue;
+  for (int pb = pc_lo; pb < pc_end; pb += kDecThreads) {
+   const int cnt = min(kDecThreads, pc_end - pb);
+   if (pb != pc_lo) decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pb, cnt, false, qs, s_red, pn_s, pbase_s);
+   for (int it = wave; it < cnt; it += 4) {
+    const int n = pn_s[it];
+    if (n == 0) continue;
+    const int64_t t0off = pbase_s[it];
 
-    // ---- loads: K in the MFMA A layout, V as row chunks
+    // ---- loads: K in the MFMA A layout, V as row chunks; rows past n re-read
+    // row n - 1 and are masked
     uint4 kr[2][KST];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      const int row = 16 * mt + hcol;
-      const int64_t off = (row < n) ? kv_offset(p.kv, b, h, a0 + row) : -1;
+      const int64_t off = t0off + min(16 * mt + hcol, n - 1) * rs;
 #pragma unroll
       for (int kk = 0; kk < KST; ++kk)
-        kr[mt][kk] = (off >= 0) ? *reinterpret_cast<const uint4*>(kbase + off * 2 + 64 * kk + 16 * lgrp)
-                                : make_uint4(0, 0, 0, 0);
+        kr[mt][kk] = *reinterpret_cast<const uint4*>(kbase + off * 2 + 64 * kk + 16 * lgrp);
     }
     uint4 vr[VC];
 #pragma unroll
     for (int i = 0; i < VC; ++i) {
-      const int row = vrow0 + RPI * i;
-      const int64_t off = (row < n) ? kv_offset(p.kv, b, h, a0 + row) : -1;
-      vr[i] = (off >= 0) ? reinterpret_cast<const uint4*>(vbase + off * 2)[vchunk] : make_uint4(0, 0, 0, 0);
+      const int64_t off = t0off + min(vrow0 + RPI * i, n - 1) * rs;
+      vr[i] = reinterpret_cast<const uint4*>(vbase + off * 2)[vchunk];
     }
+    __builtin_amdgcn_sched_barrier(0);   // every load of the piece ahead of its arithmetic
 
     // ---- scores S[token][head] on the matrix cores
     f32x4_t sc[2];
@@ -464,6 +524,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p
         for (int e = 0; e < 8; ++e) o[g][e] += pg[g] * vf[e];
     }
     wave_lds_sync();
+   }
   }
 
   // ---- combine the lanes sharing a column chunk, then the four waves
