@@ -1,7 +1,7 @@
 """Decode-step benchmark of the COBS path on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload c2] [--copies M]
-                    [--no-cpu-baseline] [--traffic FILE]
+                    [--no-cpu-baseline] [--traffic FILE] [--calibrate-copy MIB]
 
 One step = one cobs_decode_step call on one layer: refresh of the record of the
 block holding the newest token, block scoring + top-s selection, and sparse
@@ -96,6 +96,32 @@ def algorithmic_bytes(cfg, seq_lens, sel):
                 tail=tail, step=score + dec + tail + q_bytes + sel_bytes + out_bytes)
 
 
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2607_09052_amd", "csrc"))):
+        with open(os.path.join(ROOT, "paper_2607_09052_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(path, workload, kernel):
+    """HBM bytes (read + written) per launch of `kernel` from the rocprofv3 counter
+    summary, or None when there is none for this workload or the kernel sources
+    have changed since the counters were taken."""
+    if not path or not os.path.exists(path):
+        return None
+    src, hit = None, None
+    with open(path) as f:
+        for line in f:
+            w = line.split()
+            if len(w) == 2 and w[0] == "source_sha256":
+                src = w[1]
+            elif len(w) == 5 and w[0] == "traffic" and w[1] == workload and w[2] == kernel:
+                hit = int(w[3]) + int(w[4])
+    return hit if (hit is not None and src == kernel_source_hash()) else None
+
+
 def replay_time(graph, reps, stream):
     """Microseconds per replay of `graph`, HIP events on `stream`."""
     start = torch.cuda.Event(enable_timing=True)
@@ -170,8 +196,21 @@ def main():
     ap.add_argument("--workload", default="c2", choices=sorted(synth.CONFIGS))
     ap.add_argument("--copies", type=int, default=0, help="layer copies to rotate (0: >= 2 GB per sweep)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--traffic", default="", help="JSON {kernel: {fetch_bytes, write_bytes}} from rocprofv3")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic.txt"),
+                    help="rocprofv3 HBM traffic summary ('traffic <workload> <kernel> <read> <written>' lines)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB ten times (HBM counter calibration)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.randn(n, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "copies": 10}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported here (the decode step "
               "shards by KV head or batch row with no communication)", file=sys.stderr)
@@ -270,12 +309,7 @@ def main():
     kbytes = {"select_kernel": ab["select"], "decode_kernel": ab["decode"], "build_stats_kernel": ab["tail"]}
     dom = max(kern_us, key=kern_us.get)
     dom_gbps = kbytes[dom] / (kern_us[dom] * 1e-6) / 1e9
-    traffic = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            t = json.load(f).get(dom)
-        if t:
-            traffic = round(t["fetch_bytes"] + t["write_bytes"])
+    traffic = measured_traffic(args.traffic, name, dom)
     gbps = ab["step"] / (us_step * 1e-6) / 1e9
     res = {
         "metric": METRIC,
