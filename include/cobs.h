@@ -93,12 +93,17 @@ typedef struct {
 /* KV cache of one layer.
  * Contiguous mode (block_table == NULL): element (b, h, t, i) of K lives at
  *   k + b*stride_b + h*stride_h + t*stride_t + i   (strides in elements, i < d
- *   contiguous), likewise V with the same strides.  stride_t >= d.
+ *   contiguous), likewise V with the same strides.  d <= stride_t <= 2^22, and
+ *   every stride a multiple of 16 bytes' worth of elements (COBS_ERR_INVALID_ARG
+ *   otherwise; a larger stride_t gives COBS_ERR_UNSUPPORTED).
  * Paged mode (block_table != NULL): block_table is a device int32 array
  *   [B, T_max/L] of page ids; page p of the K pool holds [Hkv, L, d] contiguous
  *   elements, so (b, h, t, i) lives at
  *   k + ((block_table[b*(T_max/L) + t/L]*Hkv + h)*L + t%L)*d + i.
- *   Strides are ignored; page ids must lie in [0, num_pages).                    */
+ *   Strides are ignored; page ids must lie in [0, num_pages) (an id outside it is
+ *   never dereferenced: the decode leaves that page's tokens out and the
+ *   statistics build reads them as zero keys).
+ * k, v: 16-byte aligned.                                                          */
 typedef struct {
   const void* k;
   const void* v;

@@ -4,6 +4,8 @@
 #include <math.h>
 
 #include <algorithm>
+#include <map>
+#include <mutex>
 
 #include "cobs.h"
 #include "cobs_kernels.h"
@@ -46,8 +48,8 @@ struct Derived {
   int mdt, fdt, kv_f32;
   float c;
   RecLayout lay;
-  int bpw, nch;         // selector: blocks per workgroup, workgroups per unit
-  int spw, nwg;         // decode: segments per workgroup, workgroups per unit
+  int nch_max;          // selector: workgroups (chunks) per unit, upper bound
+  int nwg_max;          // decode: workgroups (partials) per unit, upper bound
   size_t sel_ell, sel_part, sel_cnt, sel_bytes;
   size_t dec_part, dec_cnt, dec_bytes;
   size_t step_sel, step_bytes;   // decode step: select region, decode region, selection
@@ -72,31 +74,17 @@ Derived derive(const cobs_config_t* c) {
   v.c = c->softmax_scale > 0.0f ? c->softmax_scale : 1.0f / sqrtf((float)v.d);
   v.lay = rec_layout(v.d, v.r, v.mdt, v.fdt);
 
-  // selector: enough workgroups to cover the chip, at least 16 blocks each
-  // (the matrix-core scorer for bf16 / E2M1 descriptors takes 16 blocks per wave)
-  const bool mfma_sel = select_on_matrix_cores(v.mdt, v.fdt);
-  v.bpw = mfma_sel ? 64 : 16;
-  while (v.bpw < 256 && (int64_t)v.units * ((v.nbmax + v.bpw - 1) / v.bpw) > (mfma_sel ? 1024 : 2048))
-    v.bpw *= 2;
-  v.nch = (v.nbmax + v.bpw - 1) / v.bpw;
-  // decode: segments = selected blocks + blocks touched by the window
-  const int nwin_max = v.w == 0 ? 0 : std::min(v.nbmax, (v.w + kL - 1) / kL + 1);
-  // work items: segments of <= 64 tokens (fp32 K/V) or pieces of <= 32 (bf16 K/V)
-  const int nseg = (v.kv_f32 ? 1 : 2) * (v.s + nwin_max);
-  // about two workgroups per CU resident at a time, at most kMaxDecodeWg per unit
-  v.spw = 4;
-  while (v.spw < nseg && ((int64_t)v.units * ((nseg + v.spw - 1) / v.spw) > 1024 ||
-                          (nseg + v.spw - 1) / v.spw > kMaxDecodeWg))
-    v.spw *= 2;
-  v.nwg = std::max(1, (nseg + v.spw - 1) / v.spw);
+  // grid bounds for the workspace; the launchers pick the actual grids within them
+  v.nch_max = (v.nbmax + select_min_bpw(v.mdt, v.fdt) - 1) / select_min_bpw(v.mdt, v.fdt);
+  v.nwg_max = decode_max_wg(v.s, v.w, v.nbmax, v.kv_f32 != 0);
 
   size_t off = 0;
   v.sel_ell = off;  off = round_up(off + sizeof(float) * (size_t)v.units * v.G * v.nbmax, kAlign);
-  v.sel_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nch * v.G * 2, kAlign);
+  v.sel_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nch_max * v.G * 2, kAlign);
   v.sel_cnt = off;  off = round_up(off + sizeof(unsigned) * (size_t)v.units, kAlign);
   v.sel_bytes = off;
   off = 0;
-  v.dec_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nwg * v.G * (v.d + 2), kAlign);
+  v.dec_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nwg_max * v.G * (v.d + 2), kAlign);
   v.dec_cnt = off;  off = round_up(off + sizeof(unsigned) * (size_t)v.units, kAlign);
   v.dec_bytes = off;
   v.step_sel = v.sel_bytes + v.dec_bytes;
@@ -114,6 +102,7 @@ cobs_status_t check_kv(const cobs_kv_t* kv, const Derived& v) {
   const int64_t vec = v.kv_f32 ? 4 : 8;          // elements per 16-byte load
   if (kv->stride_t < v.d || kv->stride_h < 0 || kv->stride_b < 0) return COBS_ERR_INVALID_ARG;
   if (kv->stride_t % vec || kv->stride_h % vec || kv->stride_b % vec) return COBS_ERR_INVALID_ARG;
+  if (kv->stride_t > (int64_t)1 << 22) return COBS_ERR_UNSUPPORTED;   // 32-bit row offsets within a block
   return COBS_OK;
 }
 
@@ -182,12 +171,11 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
   p.w = v.w;
   p.mdt = v.mdt;
   p.fdt = v.fdt;
-  p.nch = v.nch;
-  p.bpw = v.bpw;
+  p.nch = v.nch_max;
+  p.bpw = 0;
   p.c = v.c;
   p.lay = v.lay;
-  dim3 grid(v.nch, v.hkv, v.B);
-  return hip_status(launch_select(p, v.d, v.G, grid, st));
+  return hip_status(launch_select(p, v.d, v.G, v.B, st));
 }
 
 cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
@@ -207,14 +195,45 @@ cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
   p.tmax = v.tmax;
   p.s = v.s;
   p.w = v.w;
-  p.nwg = v.nwg;
-  p.spw = v.spw;
+  p.nwg = v.nwg_max;
+  p.spw = 0;
   p.c = v.c;
-  dim3 grid(v.nwg, v.hkv, v.B);
-  return hip_status(launch_decode(p, v.d, v.G, v.kv_f32 != 0, grid, st));
+  return hip_status(launch_decode(p, v.d, v.G, v.kv_f32 != 0, v.B, v.nbmax, st));
 }
 
 }  // namespace
+
+namespace cobs {
+
+int device_cus() {
+  static std::mutex mu;
+  static std::map<int, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find(dev);
+  if (it != cache.end()) return it->second;
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) n = 256;
+  cache[dev] = n;
+  return n;
+}
+
+int resident_workgroups(const void* kernel, int threads) {
+  static std::mutex mu;
+  static std::map<std::pair<int, const void*>, int> cache;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 1;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = cache.find({dev, kernel});
+  if (it != cache.end()) return it->second;
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kernel, threads, 0) != hipSuccess || n < 1) n = 1;
+  cache[{dev, kernel}] = n;
+  return n;
+}
+
+}  // namespace cobs
 
 extern "C" {
 

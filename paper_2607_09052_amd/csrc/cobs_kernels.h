@@ -1,6 +1,8 @@
 // Launch interface between the C ABI host layer and the HIP kernels.
 #pragma once
 
+#include <algorithm>
+
 #include "cobs_device.h"
 
 namespace cobs {
@@ -21,7 +23,7 @@ struct SelectParams {
   float* scores;
   float* ell;       // [B*Hkv][nbmax][G]
   float* part;      // [B*Hkv][nch][G][2]
-  unsigned* cnt;    // [B*Hkv]
+  unsigned* cnt;    // [B*Hkv] arrival counters
   int hkv, hq, nbmax, tmax, r, s, w, mdt, fdt, nch, bpw;
   float c;
   RecLayout lay;
@@ -35,7 +37,7 @@ struct DecodeParams {
   float* out;
   float* lse;
   float* part;      // [B*Hkv][nwg][G][D + 2]
-  unsigned* cnt;    // [B*Hkv]
+  unsigned* cnt;    // [B*Hkv] arrival counters
   int hkv, hq, tmax, s, w, nwg, spw;   // spw: work items (segments or pieces) per workgroup
   float c;
 };
@@ -43,8 +45,18 @@ struct DecodeParams {
 hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st);
 hipError_t launch_pack_e2m1(const float* x, int64_t nvec, int dim, uint8_t* codes, float* scales,
                             hipStream_t st);
-hipError_t launch_select(const SelectParams& p, int d, int g, dim3 grid, hipStream_t st);
+// Launchers choose the grid (chunks / work items per workgroup) from the
+// device's resident-workgroup count; workspace bounds come from the *_max
+// helpers, which depend on the problem description only.
+hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st);
 bool select_on_matrix_cores(int mdt, int fdt);
-hipError_t launch_decode(const DecodeParams& p, int d, int g, bool f32, dim3 grid, hipStream_t st);
+int select_min_bpw(int mdt, int fdt);
+hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int nbmax, hipStream_t st);
+int decode_max_wg(int s, int w, int nbmax, bool f32);
+
+// Resident workgroups of `threads` threads per CU for a kernel, and the CU
+// count, of the current device (cached per device and kernel).
+int resident_workgroups(const void* kernel, int threads);
+int device_cus();
 
 }  // namespace cobs

@@ -36,6 +36,15 @@ __device__ __forceinline__ void unpack16(const uint4& u, float* x) {
   }
 }
 
+// A value every lane of the wave holds (read from LDS at a wave-uniform index),
+// moved to scalar registers.
+__device__ __forceinline__ int wave_uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ int64_t wave_uniform(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
 // Token range of work item `it` (PT tokens per item, kL / PT items per segment):
 // n tokens from the element offset `base` of its first token, consecutive tokens
 // `rs` elements apart.  Segment i < s is selected block sel[i] (only while i is
@@ -174,7 +183,7 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h) {
 }
 
 template <int D, int G, bool F32>
-__global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
+__device__ __forceinline__ void decode_task(const DecodeParams& p, int b, int h, int wg) {
   constexpr int ES = F32 ? 4 : 2;            // element bytes
   constexpr int CPR = D * ES / 16;           // 16-byte chunks per row: 8, 16 or 32
   constexpr int EPC = 16 / ES;               // elements per chunk
@@ -194,7 +203,6 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
   __shared__ int64_t pbase_s[kDecThreads];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int b = blockIdx.z, h = blockIdx.y, wg = blockIdx.x;
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   const int ws = max(0, T - p.w);
@@ -221,22 +229,26 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
    const int cnt = min(kDecThreads, seg_end - sb);
    decode_prologue<D, G, kL>(p, b, h, T, ws, nc, sb, cnt, sb == seg_lo, qs, s_red, pn_s, pbase_s);
    for (int it = wave; it < cnt; it += 4) {
-    const int n = pn_s[it];
+    const int n = wave_uniform(pn_s[it]);
     if (n == 0) continue;
-    const int64_t t0off = pbase_s[it];
+    // the item's first token (scalar base), rows by 32-bit byte offsets
+    const int64_t t0off = wave_uniform(pbase_s[it]);
+    const char* kp = kbase + t0off * ES;
+    const char* vp = vbase + t0off * ES;
+    const int rsb = (int)rs * ES;
 
     // ---- issue the loads: K rows (lane <-> token), V sub-tile 0 (lane <-> chunk);
     // rows past n re-read row n - 1 and are masked
-    const int64_t koff = t0off + min(lane, n - 1) * rs;
+    const int koff = min(lane, n - 1) * rsb;
     uint4 kr[KC];
 #pragma unroll
-    for (int c = 0; c < KC; ++c) kr[c] = reinterpret_cast<const uint4*>(kbase + koff * ES)[c];
+    for (int c = 0; c < KC; ++c) kr[c] = reinterpret_cast<const uint4*>(kp + koff)[c];
     uint4 vr[VC];
     auto load_v = [&](int half) {
 #pragma unroll
       for (int i = 0; i < VC; ++i) {
         const int row = min(half * VR + vrow0 + RPI * i, n - 1);
-        vr[i] = reinterpret_cast<const uint4*>(vbase + (t0off + row * rs) * ES)[vchunk];
+        vr[i] = reinterpret_cast<const uint4*>(vp + row * rsb)[vchunk];
       }
     };
     load_v(0);
@@ -249,7 +261,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
     for (int hf = 0; hf < HALVES; ++hf) {
       if (hf == 1) {
 #pragma unroll
-        for (int c = 0; c < KC; ++c) kr[c] = reinterpret_cast<const uint4*>(kbase + koff * ES)[KC + c];
+        for (int c = 0; c < KC; ++c) kr[c] = reinterpret_cast<const uint4*>(kp + koff)[KC + c];
       }
 #pragma unroll
       for (int c = 0; c < KC; ++c) {
@@ -371,7 +383,7 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
 
 template <int D, int G>
-__global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p) {
+__device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, int h, int wg) {
   static_assert(G <= 16, "at most 16 query heads per KV head");
   constexpr int KST = D / 32;                 // k-steps of the score product
   constexpr int CPR = D / 8;                  // 16-byte chunks per row (bf16)
@@ -389,7 +401,6 @@ __global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p
   __shared__ int64_t pbase_s[kDecThreads];
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int b = blockIdx.z, h = blockIdx.y, wg = blockIdx.x;
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   const int ws = max(0, T - p.w);
@@ -432,25 +443,27 @@ __global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p
    const int cnt = min(kDecThreads, pc_end - pb);
    if (pb != pc_lo) decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pb, cnt, false, qs, s_red, pn_s, pbase_s);
    for (int it = wave; it < cnt; it += 4) {
-    const int n = pn_s[it];
+    const int n = wave_uniform(pn_s[it]);
     if (n == 0) continue;
-    const int64_t t0off = pbase_s[it];
+    // the piece's first token (scalar base), rows by 32-bit byte offsets
+    const int64_t t0off = wave_uniform(pbase_s[it]);
+    const char* kp = kbase + t0off * 2;
+    const char* vp = vbase + t0off * 2;
+    const int rsb = (int)rs * 2;
 
     // ---- loads: K in the MFMA A layout, V as row chunks; rows past n re-read
     // row n - 1 and are masked
     uint4 kr[2][KST];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      const int64_t off = t0off + min(16 * mt + hcol, n - 1) * rs;
+      const int off = min(16 * mt + hcol, n - 1) * rsb + 16 * lgrp;
 #pragma unroll
-      for (int kk = 0; kk < KST; ++kk)
-        kr[mt][kk] = *reinterpret_cast<const uint4*>(kbase + off * 2 + 64 * kk + 16 * lgrp);
+      for (int kk = 0; kk < KST; ++kk) kr[mt][kk] = *reinterpret_cast<const uint4*>(kp + off + 64 * kk);
     }
     uint4 vr[VC];
 #pragma unroll
     for (int i = 0; i < VC; ++i) {
-      const int64_t off = t0off + min(vrow0 + RPI * i, n - 1) * rs;
-      vr[i] = reinterpret_cast<const uint4*>(vbase + off * 2)[vchunk];
+      vr[i] = reinterpret_cast<const uint4*>(vp + min(vrow0 + RPI * i, n - 1) * rsb)[vchunk];
     }
     __builtin_amdgcn_sched_barrier(0);   // every load of the piece ahead of its arithmetic
 
@@ -572,27 +585,60 @@ __global__ __launch_bounds__(kDecThreads) void decode_mfma_kernel(DecodeParams p
   merge_partials<D, G>(p, unit, b, h);
 }
 
-// ------------------------------------------------------------- launchers --
-template <int D, int G>
-static hipError_t launch_decode_dg(const DecodeParams& p, bool f32, dim3 grid, hipStream_t st) {
-  if (f32) hipLaunchKernelGGL((decode_kernel<D, G, true>), grid, dim3(kDecThreads), 0, st, p);
-  else hipLaunchKernelGGL((decode_mfma_kernel<D, G>), grid, dim3(kDecThreads), 0, st, p);
-  return hipGetLastError();
+// Grid (workgroups per unit, Hkv, B).
+template <int D, int G, bool F32>
+__global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
+  decode_task<D, G, F32>(p, blockIdx.z, blockIdx.y, blockIdx.x);
 }
 
+template <int D, int G>
+__global__ __launch_bounds__(kDecThreads, (G <= 4) ? 3 : (G <= 8 ? 2 : 1)) void decode_mfma_kernel(DecodeParams p) {
+  decode_mfma_task<D, G>(p, blockIdx.z, blockIdx.y, blockIdx.x);
+}
+
+// ------------------------------------------------------------- launchers --
+typedef void (*DecodeKernel)(DecodeParams);
+
 template <int D>
-static hipError_t launch_decode_d(const DecodeParams& p, int g, bool f32, dim3 grid, hipStream_t st) {
+static DecodeKernel decode_kernel_d(int g, bool f32) {
   switch (g) {
-    case 1: return launch_decode_dg<D, 1>(p, f32, grid, st);
-    case 2: return launch_decode_dg<D, 2>(p, f32, grid, st);
-    case 4: return launch_decode_dg<D, 4>(p, f32, grid, st);
-    case 8: return launch_decode_dg<D, 8>(p, f32, grid, st);
-    default: return launch_decode_dg<D, 16>(p, f32, grid, st);
+    case 1: return f32 ? decode_kernel<D, 1, true> : decode_mfma_kernel<D, 1>;
+    case 2: return f32 ? decode_kernel<D, 2, true> : decode_mfma_kernel<D, 2>;
+    case 4: return f32 ? decode_kernel<D, 4, true> : decode_mfma_kernel<D, 4>;
+    case 8: return f32 ? decode_kernel<D, 8, true> : decode_mfma_kernel<D, 8>;
+    default: return f32 ? decode_kernel<D, 16, true> : decode_mfma_kernel<D, 16>;
   }
 }
 
-hipError_t launch_decode(const DecodeParams& p, int d, int g, bool f32, dim3 grid, hipStream_t st) {
-  return d == 128 ? launch_decode_d<128>(p, g, f32, grid, st) : launch_decode_d<64>(p, g, f32, grid, st);
+// Work items per (batch row, KV head): segments of <= 64 tokens (fp32 K/V) or
+// pieces of <= 32 (bf16 K/V) of the selected blocks and the window's blocks.
+int decode_items(int s, int w, int nbmax, bool f32) {
+  const int nwin_max = (w == 0) ? 0 : std::min(nbmax, (w + kL - 1) / kL + 1);
+  return (f32 ? 1 : 2) * (s + nwin_max);
+}
+
+int decode_max_wg(int s, int w, int nbmax, bool f32) {
+  return std::max(1, std::min(kMaxDecodeWg, (decode_items(s, w, nbmax, f32) + 3) / 4));
+}
+
+// A unit's work items split over nwg <= kMaxDecodeWg workgroups (one partial
+// each), sized so that the grid fills the chip's resident workgroup slots in
+// one round (an underfilled last round streams at a fraction of the bandwidth).
+hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int nbmax, hipStream_t st) {
+  const DecodeKernel k = (d == 128) ? decode_kernel_d<128>(g, f32) : decode_kernel_d<64>(g, f32);
+  const int items = decode_items(p.s, p.w, nbmax, f32);
+  const int64_t units = (int64_t)batch * p.hkv;
+  const int64_t slots = (int64_t)resident_workgroups(reinterpret_cast<const void*>(k), kDecThreads) * device_cus();
+  // one round of the chip's resident workgroup slots, the items spread evenly
+  // over a unit's workgroups
+  int64_t spw = (units * items + slots - 1) / slots;
+  spw = std::max<int64_t>(spw, (items + kMaxDecodeWg - 1) / kMaxDecodeWg);
+  spw = std::max<int64_t>(spw, 4);
+  const int nwg = std::max(1, (int)((items + spw - 1) / spw));
+  p.nwg = nwg;
+  p.spw = std::max(1, (items + nwg - 1) / nwg);
+  hipLaunchKernelGGL(k, dim3(nwg, p.hkv, batch), dim3(kDecThreads), 0, st, p);
+  return hipGetLastError();
 }
 
 }  // namespace cobs

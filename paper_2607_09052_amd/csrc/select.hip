@@ -1,17 +1,35 @@
-// Block selector dispatch: fp32 descriptors (or an fp32 half of the pair) are
-// scored on the vector ALUs, bf16 / E2M1 descriptors on the matrix cores.
+// Block selector dispatch and grid sizing.  fp32 descriptors (or an fp32 half
+// of the pair) are scored on the vector ALUs, bf16 / E2M1 descriptors on the
+// matrix cores.  The chunk size is chosen so that the grid fills the chip's
+// resident workgroup slots in one round: an underfilled last round streams at
+// a fraction of the bandwidth.
 #include "cobs_kernels.h"
 
 namespace cobs {
 
-hipError_t launch_select_valu(const SelectParams& p, int d, int g, dim3 grid, hipStream_t st);
-hipError_t launch_select_mfma(const SelectParams& p, int d, int g, dim3 grid, hipStream_t st);
+typedef void (*SelectKernel)(SelectParams);
+SelectKernel select_valu_kernel_for(const SelectParams& p, int d, int g);
+SelectKernel select_mfma_kernel_for(const SelectParams& p, int d, int g);
 
 bool select_on_matrix_cores(int mdt, int fdt) { return mdt != DT_F32 && fdt != DT_F32; }
 
-hipError_t launch_select(const SelectParams& p, int d, int g, dim3 grid, hipStream_t st) {
-  return select_on_matrix_cores(p.mdt, p.fdt) ? launch_select_mfma(p, d, g, grid, st)
-                                              : launch_select_valu(p, d, g, grid, st);
+int select_min_bpw(int mdt, int fdt) { return select_on_matrix_cores(mdt, fdt) ? 64 : 16; }
+
+hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st) {
+  const bool mfma = select_on_matrix_cores(p.mdt, p.fdt);
+  const SelectKernel k = mfma ? select_mfma_kernel_for(p, d, g) : select_valu_kernel_for(p, d, g);
+  if (!k) return hipErrorInvalidValue;
+  const int base = select_min_bpw(p.mdt, p.fdt);
+  const int64_t units = (int64_t)batch * p.hkv;
+  const int64_t slots = (int64_t)resident_workgroups(reinterpret_cast<const void*>(k), 256) * device_cus();
+  // blocks per workgroup: a multiple of `base`, enough that units * chunks fits the slots
+  // blocks per workgroup: a multiple of `base`, one round of the resident slots
+  int64_t bpw = (units * p.nbmax + slots - 1) / slots;
+  bpw = std::max<int64_t>(base, (bpw + base - 1) / base * base);
+  p.bpw = (int)std::min<int64_t>(bpw, ((int64_t)p.nbmax + base - 1) / base * base);
+  p.nch = (p.nbmax + p.bpw - 1) / p.bpw;
+  hipLaunchKernelGGL(k, dim3(p.nch, p.hkv, batch), dim3(256), 0, st, p);
+  return hipGetLastError();
 }
 
 }  // namespace cobs

@@ -116,27 +116,40 @@ __device__ __forceinline__ void load_g(const float* src, float* v) {
 }
 
 // Last workgroup of a unit.  Candidate block j (j < nc) is held by thread
-// j % 256 as key slot j / 256; every per-slot loop stops at the U live slots
+// j % 256 as key slot j / 256 < KPT, the caller's bound on the slot count: the
+// per-slot loops are fully unrolled to KPT with guards for the U live slots
 // (a wave64 vector instruction costs four cycles and this phase runs on one
-// workgroup).  ln Z^g comes from the chunk partials (wave 0, overlapped with
+// workgroup, so the bound follows the candidate count).  ln Z^g comes from the chunk partials (wave 0, overlapped with
 // every thread's first score loads); sigma and its order-preserving key per
 // candidate; the s-th largest key by radix select over the bytes below the
 // keys' common prefix; the selection as two bitmaps built from wave ballots
 // (keys above the threshold; keys equal to it, of which the lowest-index
 // `need` are taken) and written in ascending order by a scan over the
 // 32-block words.
-template <int G>
-__device__ void finish_select(const SelectParams& p, int unit, int T, int nb) {
-  constexpr int KPT = kMaxBlocksPerSeq / kSelThreads;   // key slots per thread
+// LDS of the finishing phase (one instance per kernel, whatever slot bound runs).
+struct FinishLds {
+  float lse[kMaxG];
+  uint32_t red[2][kSelThreads / 64];
+  __align__(16) int hist[2][256];
+  int scan[kSelThreads / 64];
+  int digit, rem, cnt;
+  uint32_t gtw[kMaxBlocksPerSeq / 32], eqw[kMaxBlocksPerSeq / 32];
+};
+
+template <int G, int KPT>
+__device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds& F) {
+  static_assert(KPT * kSelThreads <= kMaxBlocksPerSeq, "key slots");
   constexpr int UB = (64 / G) < KPT ? (64 / G) : KPT;    // slots whose scores load together
-  constexpr int NWORD = kMaxBlocksPerSeq / 32;
-  static_assert(NWORD == kSelThreads, "one bitmap word per thread");
-  __shared__ float lse_s[G];
-  __shared__ uint32_t red_s[2][kSelThreads / 64];
-  __shared__ __align__(16) int hist[2][256];
-  __shared__ int scan_buf[kSelThreads / 64];
-  __shared__ int s_digit, s_rem, s_cnt;
-  __shared__ uint32_t gtw[NWORD], eqw[NWORD];
+  static_assert(kMaxBlocksPerSeq / 32 == kSelThreads, "one bitmap word per thread");
+  float* lse_s = F.lse;
+  auto& red_s = F.red;
+  auto& hist = F.hist;
+  int* scan_buf = F.scan;
+  int& s_digit = F.digit;
+  int& s_rem = F.rem;
+  int& s_cnt = F.cnt;
+  uint32_t* gtw = F.gtw;
+  uint32_t* eqw = F.eqw;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
   const int ws = max(0, T - p.w);
@@ -150,10 +163,8 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, int nb) {
   // first batch of scores, issued before the partial merge
   float v[UB][G];
 #pragma unroll
-  for (int u = 0; u < UB; ++u) {
-    if (u >= U) break;
-    load_g<G>(ellu + (int64_t)min(u * kSelThreads + tid, last) * G, v[u]);
-  }
+  for (int u = 0; u < UB; ++u)
+    if (u < U) load_g<G>(ellu + (int64_t)min(u * kSelThreads + tid, last) * G, v[u]);
   if (wave == 0) {
     // lane l merges chunks l / G, l / G + 64 / G, ... of head l % G; the lanes of
     // one head then combine by butterfly shuffles over the chunk bits
@@ -186,17 +197,14 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, int nb) {
   uint32_t key[KPT];
 #pragma unroll
   for (int u0 = 0; u0 < KPT; u0 += UB) {
-    if (u0 >= U) break;
     if (u0 > 0) {
 #pragma unroll
-      for (int u = 0; u < UB; ++u) {
-        if (u0 + u >= U) break;
-        load_g<G>(ellu + (int64_t)min((u0 + u) * kSelThreads + tid, last) * G, v[u]);
-      }
+      for (int u = 0; u < UB; ++u)
+        if (u0 + u < U) load_g<G>(ellu + (int64_t)min((u0 + u) * kSelThreads + tid, last) * G, v[u]);
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
-      if (u0 + u >= U) break;
+      if (u0 + u >= U) continue;
       const int blk = (u0 + u) * kSelThreads + tid;
       float mx = -INFINITY;
 #pragma unroll
@@ -222,10 +230,8 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, int nb) {
   if (k > 0 && k < nc) {
     uint32_t kmax = 0u, kmin = 0xffffffffu;
 #pragma unroll
-    for (int u = 0; u < KPT; ++u) {
-      if (u >= U) break;
-      if (live(u)) { kmax = max(kmax, key[u]); kmin = min(kmin, key[u]); }
-    }
+    for (int u = 0; u < KPT; ++u)
+      if (u < U && live(u)) { kmax = max(kmax, key[u]); kmin = min(kmin, key[u]); }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
       kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
@@ -247,10 +253,8 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, int nb) {
         // histogram of this byte over the keys matching the prefix; the other
         // buffer is cleared for the next pass
 #pragma unroll
-        for (int u = 0; u < KPT; ++u) {
-          if (u >= U) break;
-          if (live(u) && (key[u] & mask) == prefix) atomicAdd(&hist[cur][(key[u] >> shift) & 255u], 1);
-        }
+        for (int u = 0; u < KPT; ++u)
+          if (u < U && live(u) && (key[u] & mask) == prefix) atomicAdd(&hist[cur][(key[u] >> shift) & 255u], 1);
         hist[cur ^ 1][tid] = 0;
         __syncthreads();
         if (wave == 0) {
@@ -290,14 +294,15 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, int nb) {
   // lanes covers words 8 u + 2 w and 8 u + 2 w + 1
 #pragma unroll
   for (int u = 0; u < KPT; ++u) {
-    if (u >= U) break;
-    const bool lv = live(u);
-    const uint64_t gt = __ballot(lv && (all || key[u] > kth));
-    const uint64_t eq = __ballot(lv && !all && key[u] == kth);
-    if (lane == 0) {
-      const int w0 = 8 * u + 2 * wave;
-      gtw[w0] = (uint32_t)gt; gtw[w0 + 1] = (uint32_t)(gt >> 32);
-      eqw[w0] = (uint32_t)eq; eqw[w0 + 1] = (uint32_t)(eq >> 32);
+    if (u < U) {
+      const bool lv = live(u);
+      const uint64_t gt = __ballot(lv && (all || key[u] > kth));
+      const uint64_t eq = __ballot(lv && !all && key[u] == kth);
+      if (lane == 0) {
+        const int w0 = 8 * u + 2 * wave;
+        gtw[w0] = (uint32_t)gt; gtw[w0 + 1] = (uint32_t)(gt >> 32);
+        eqw[w0] = (uint32_t)eq; eqw[w0 + 1] = (uint32_t)(eq >> 32);
+      }
     }
   }
   __syncthreads();
@@ -331,7 +336,7 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, int nb) {
 // combined by a 16-lane DPP reduction.
 // ---------------------------------------------------------------------------
 template <int D, int G, int RMAX, int MDT, int FDT>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
+__device__ __forceinline__ void select_task(const SelectParams& p, int b, int h, int chunk) {
   constexpr int EPL = D / 16;
   constexpr int MW = slice_words<MDT, EPL>(), FW = slice_words<FDT, EPL>();
   constexpr int SW = (FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0;    // 16-byte words of factor scales
@@ -339,7 +344,6 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
   __shared__ int s_last;
 
   const int tid = threadIdx.x;
-  const int b = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   const int nb = (T + kL - 1) / kL;
@@ -454,7 +458,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
     st_agent(&pp[1], s);
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
-  finish_select<G>(p, unit, T, nb);
+  __shared__ FinishLds fin;
+  const int nc = (max(0, T - p.w) + kL - 1) / kL;
+  if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
+  else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
+  else finish_select<G, kMaxBlocksPerSeq / kSelThreads>(p, unit, T, fin);
 }
 
 // ---------------------------------------------------------------------------
@@ -495,7 +503,7 @@ __device__ __forceinline__ sbf16x8_t tile_operand(const uint32_t* w, int kk) {
 }
 
 template <int D, int G, int RMAX, int MDT, int FDT>
-__global__ __launch_bounds__(kSelThreads) void select_mfma_kernel(SelectParams p) {
+__device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, int h, int chunk) {
   static_assert(MDT != DT_F32 && FDT != DT_F32, "matrix-core scorer takes bf16 / E2M1 descriptors");
   constexpr int KST = D / 32;                                  // k-steps per lane group
   constexpr int MW = elem_bytes<MDT>(D / 4) / 4, FW = elem_bytes<FDT>(D / 4) / 4;
@@ -505,7 +513,6 @@ __global__ __launch_bounds__(kSelThreads) void select_mfma_kernel(SelectParams p
   __shared__ int s_last;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int b = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   const int nb = (T + kL - 1) / kL;
@@ -636,7 +643,22 @@ __global__ __launch_bounds__(kSelThreads) void select_mfma_kernel(SelectParams p
     st_agent(&pp[1], s);
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
-  finish_select<G>(p, unit, T, nb);
+  __shared__ FinishLds fin;
+  const int nc = (max(0, T - p.w) + kL - 1) / kL;
+  if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
+  else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
+  else finish_select<G, kMaxBlocksPerSeq / kSelThreads>(p, unit, T, fin);
+}
+
+// Grid (chunks, Hkv, B).
+template <int D, int G, int RMAX, int MDT, int FDT>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
+  select_task<D, G, RMAX, MDT, FDT>(p, blockIdx.z, blockIdx.y, blockIdx.x);
+}
+
+template <int D, int G, int RMAX, int MDT, int FDT>
+__global__ __launch_bounds__(kSelThreads) void select_mfma_kernel(SelectParams p) {
+  select_mfma_task<D, G, RMAX, MDT, FDT>(p, blockIdx.z, blockIdx.y, blockIdx.x);
 }
 
 }  // namespace cobs
