@@ -126,21 +126,33 @@ __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2
 }
 
 // Cross-workgroup data (per-workgroup partials, per-block scores) is written
-// with agent-scope write-through stores and read back with agent-scope loads,
-// so it is coherent across the XCDs' L2 caches without an L2 write-back or
-// invalidate (which a device-scope fence would cost every workgroup).
+// with agent-scope write-through stores and read back with agent-coherent
+// buffer loads (cache policy SC1), which miss in the reading XCD's L2 instead
+// of returning lines an earlier launch left there.  This needs neither an L2
+// write-back nor an L2 invalidate (a device-scope fence would cost both, per
+// workgroup).  A view covers `bytes` bytes from `base`; reads past it return 0.
 __device__ __forceinline__ void st_agent(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float ld_agent(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+constexpr int kCachePolicySc1 = 16;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_view(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float4 ld_coherent4(__amdgpu_buffer_rsrc_t v, uint32_t off) {
+  const auto x = __builtin_amdgcn_raw_buffer_load_b128(v, (int)off, 0, kCachePolicySc1);
+  return make_float4(__uint_as_float(x[0]), __uint_as_float(x[1]), __uint_as_float(x[2]), __uint_as_float(x[3]));
+}
+__device__ __forceinline__ float2 ld_coherent2(__amdgpu_buffer_rsrc_t v, uint32_t off) {
+  const auto x = __builtin_amdgcn_raw_buffer_load_b64(v, (int)off, 0, kCachePolicySc1);
+  return make_float2(__uint_as_float(x[0]), __uint_as_float(x[1]));
+}
+__device__ __forceinline__ float ld_coherent1(__amdgpu_buffer_rsrc_t v, uint32_t off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(v, (int)off, 0, kCachePolicySc1));
 }
 
 // Count this workgroup's arrival on `counter` once its write-through stores
 // have been acknowledged; returns true (in every thread) for the last of
-// `expected` arrivals.  The last arrival resets the counter for the next launch
-// and performs one agent-scope acquire (this XCD's caches drop stale lines), so
-// it may read every other workgroup's write-through data with ordinary loads.
+// `expected` arrivals, which resets the counter for the next launch.
 __device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected, int* sflag) {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __builtin_amdgcn_s_waitcnt(0);          // this wave's stores are complete
@@ -153,7 +165,6 @@ __device__ __forceinline__ bool arrive_last(unsigned* counter, unsigned expected
   }
   __syncthreads();
   const bool last = *sflag != 0;
-  if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
   return last;
 }

@@ -123,7 +123,7 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h) {
   __shared__ float mk[kMaxDecodeWg][G], lk[kMaxDecodeWg][G];
   const int tid = threadIdx.x;
   const int nwg = p.nwg;
-  const float* up = p.part + (int64_t)unit * nwg * G * (D + 2);
+  const __amdgpu_buffer_rsrc_t up = coherent_view(p.part + (int64_t)unit * nwg * G * (D + 2), 4u * nwg * G * (D + 2));
   float ov[KB][OPT];
   auto load_batch = [&](int k0) {
 #pragma unroll
@@ -132,14 +132,14 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h) {
 #pragma unroll
       for (int j = 0; j < OPT; ++j) {
         const int idx = min(tid + kDecThreads * j, G * D - 1);
-        ov[k][j] = up[(kc * G + idx / D) * (D + 2) + 2 + idx % D];
+        ov[k][j] = ld_coherent1(up, 4u * ((kc * G + idx / D) * (D + 2) + 2 + idx % D));
       }
     }
   };
   load_batch(0);
   for (int idx = tid; idx < nwg * G; idx += kDecThreads) {
     const int k = idx / G, g = idx % G;
-    const float2 ml = *reinterpret_cast<const float2*>(&up[(k * G + g) * (D + 2)]);
+    const float2 ml = ld_coherent2(up, 4u * ((k * G + g) * (D + 2)));
     mk[k][g] = ml.x;
     lk[k][g] = ml.y;
   }

@@ -98,34 +98,24 @@ __device__ inline int block_excl_scan(int v, int* wsum, int* total) {
 }
 
 // ------------------------------------------------------------- finishing --
-// The G scores of one block (stored [block][head]) in as few loads as possible.
+// The G scores of one block (stored [block][head], byte offset `off` in the
+// unit's score view) in as few loads as possible.
 template <int G>
-__device__ __forceinline__ void load_g(const float* src, float* v) {
+__device__ __forceinline__ void load_g(__amdgpu_buffer_rsrc_t view, uint32_t off, float* v) {
   if constexpr (G >= 4) {
 #pragma unroll
     for (int g = 0; g < G; g += 4) {
-      const float4 x = *reinterpret_cast<const float4*>(src + g);
+      const float4 x = ld_coherent4(view, off + 4 * g);
       v[g] = x.x; v[g + 1] = x.y; v[g + 2] = x.z; v[g + 3] = x.w;
     }
   } else if constexpr (G == 2) {
-    const float2 x = *reinterpret_cast<const float2*>(src);
+    const float2 x = ld_coherent2(view, off);
     v[0] = x.x; v[1] = x.y;
   } else {
-    v[0] = *src;
+    v[0] = ld_coherent1(view, off);
   }
 }
 
-// Last workgroup of a unit.  Candidate block j (j < nc) is held by thread
-// j % 256 as key slot j / 256 < KPT, the caller's bound on the slot count: the
-// per-slot loops are fully unrolled to KPT with guards for the U live slots
-// (a wave64 vector instruction costs four cycles and this phase runs on one
-// workgroup, so the bound follows the candidate count).  ln Z^g comes from the chunk partials (wave 0, overlapped with
-// every thread's first score loads); sigma and its order-preserving key per
-// candidate; the s-th largest key by radix select over the bytes below the
-// keys' common prefix; the selection as two bitmaps built from wave ballots
-// (keys above the threshold; keys equal to it, of which the lowest-index
-// `need` are taken) and written in ascending order by a scan over the
-// 32-block words.
 // LDS of the finishing phase (one instance per kernel, whatever slot bound runs).
 struct FinishLds {
   float lse[kMaxG];
@@ -156,7 +146,7 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
   const int nc = (ws + kL - 1) / kL;                 // candidates: b L < T - w
   const int k = min(p.s, nc);
   const int U = (nc + kSelThreads - 1) / kSelThreads;
-  const float* ellu = p.ell + (int64_t)unit * p.nbmax * G;
+  const __amdgpu_buffer_rsrc_t ellu = coherent_view(p.ell + (int64_t)unit * p.nbmax * G, 4u * p.nbmax * G);
   const int last = max(nc - 1, 0);
 
   hist[0][tid] = 0;
@@ -164,19 +154,20 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
   float v[UB][G];
 #pragma unroll
   for (int u = 0; u < UB; ++u)
-    if (u < U) load_g<G>(ellu + (int64_t)min(u * kSelThreads + tid, last) * G, v[u]);
+    if (u < U) load_g<G>(ellu, 4u * G * min(u * kSelThreads + tid, last), v[u]);
   if (wave == 0) {
     // lane l merges chunks l / G, l / G + 64 / G, ... of head l % G; the lanes of
     // one head then combine by butterfly shuffles over the chunk bits
     constexpr int SLOTS = 64 / G;
     const int g = lane % G;
+    const __amdgpu_buffer_rsrc_t parts = coherent_view(p.part + (int64_t)unit * p.nch * G * 2, 8u * p.nch * G);
     float m = -INFINITY, s = 0.0f;
     for (int ch0 = lane / G; ch0 < p.nch; ch0 += 4 * SLOTS) {
       float2 pv[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int ch = min(ch0 + j * SLOTS, p.nch - 1);
-        pv[j] = *reinterpret_cast<const float2*>(p.part + (((int64_t)unit * p.nch + ch) * G + g) * 2);
+        pv[j] = ld_coherent2(parts, 8u * (ch * G + g));
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j)
@@ -200,7 +191,7 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
     if (u0 > 0) {
 #pragma unroll
       for (int u = 0; u < UB; ++u)
-        if (u0 + u < U) load_g<G>(ellu + (int64_t)min((u0 + u) * kSelThreads + tid, last) * G, v[u]);
+        if (u0 + u < U) load_g<G>(ellu, 4u * G * min((u0 + u) * kSelThreads + tid, last), v[u]);
     }
 #pragma unroll
     for (int u = 0; u < UB; ++u) {
