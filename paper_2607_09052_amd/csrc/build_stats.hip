@@ -1,388 +1,29 @@
-// Block statistics builder (Sec. 5.3 eq. lowrank, Gram trick of Sec. 5.6,
-// storage of Sec. 5.5) and the E2M1 encoder.
-//
-// One 256-thread workgroup per (batch row, KV head, block).  The block's keys
-// are staged transposed in LDS as fp32, centred on the block mean, and the
-// 64 x 64 Gram matrix Gamma = Kc Kc^T / n is formed.  Its top-r eigenvectors
-// come from a fixed-count block power iteration on P = 16 (r <= 4) or 32
-// columns, re-orthonormalised by Cholesky-QR every step, followed by a
-// Rayleigh-Ritz step whose P x P eigenproblem is solved by parallel cyclic
-// Jacobi.  The scaled eigenvectors are xi_i = Kc^T w_i / sqrt(n) (their squared
-// norms are the Ritz values), with the sign that makes the largest-magnitude
-// entry positive.  A partial block (n < L) stores zero factors.
-#include "cobs_kernels.h"
+// Block statistics build kernel (prefill, explicit block ranges, and the
+// decode step's refresh of the newest block) and the E2M1 encoder.
+#include "block_stats.h"
 
 namespace cobs {
 
-constexpr int kBuildThreads = 256;
-constexpr int kPowerIters = 16;
-constexpr int kJacobiSweeps = 4;
-
-
-__device__ __forceinline__ float init_sign(int i, int p) {
-  uint32_t h = (uint32_t)i * 2654435761u ^ ((uint32_t)p * 0x9E3779B9u + 0x7f4a7c15u);
-  h ^= h >> 16;
-  h *= 0x85ebca6bu;
-  h ^= h >> 13;
-  return (h & 1u) ? 1.0f : -1.0f;
-}
-
-// Encode one vector of `dim` fp32 values held in LDS (`x`) into `dst` with the
-// given storage dtype.  For E2M1 the scale is written to *scale_dst.  Executed
-// by the `nthr` threads whose local index is `lt`; `red` is LDS scratch of nthr floats.
-__device__ void store_vector(const float* x, int dim, int dt, uint8_t* dst, float* scale_dst,
-                             int lt, int nthr, float* red) {
-  if (dt == DT_F32) {
-    for (int e = lt; e < dim; e += nthr) reinterpret_cast<float*>(dst)[e] = x[e];
-    return;
-  }
-  if (dt == DT_BF16) {
-    for (int e = lt; e < dim / 2; e += nthr) {
-      uint32_t lo = f32_to_bf16_rne(x[2 * e]), hi = f32_to_bf16_rne(x[2 * e + 1]);
-      reinterpret_cast<uint32_t*>(dst)[e] = lo | (hi << 16);
-    }
-    return;
-  }
-  float m = 0.0f;
-  for (int e = lt; e < dim; e += nthr) m = fmaxf(m, fabsf(x[e]));
-  red[lt] = m;
-  __syncthreads();
-  for (int o = nthr / 2; o > 0; o >>= 1) {
-    if (lt < o) red[lt] = fmaxf(red[lt], red[lt + o]);
-    __syncthreads();
-  }
-  float absmax = red[0];
-  __syncthreads();
-  float scale = absmax / 6.0f;
-  if (lt == 0) *scale_dst = scale;
-  for (int e = lt; e < dim / 8; e += nthr) {
-    uint32_t w = 0;
-    if (scale > 0.0f) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) w |= e2m1_code(x[8 * e + j], scale) << (4 * j);
-    }
-    reinterpret_cast<uint32_t*>(dst)[e] = w;
-  }
-}
-
-template <int D, int P>
+// One 256-thread workgroup per (batch row, KV head, block).
+template <int D, int P, bool KF32>
 __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams p) {
-  constexpr int KS = kL + 4;             // row stride of the transposed keys
-  __shared__ __align__(16) float KT[D * KS];       // centred keys, KT[e][i]
-  __shared__ __align__(16) float mean[D];
-  __shared__ __align__(16) float Gm[kL * kL];      // Gram matrix, symmetric
-  __shared__ __align__(16) float Wm[kL * P];
-  __shared__ __align__(16) float Ym[kL * P];
-  __shared__ float Sm[P * (P + 1)];
-  __shared__ float Lm[P * (P + 1)];
-  __shared__ float rdiag[P];
-  __shared__ float Hm[2][P * (P + 1)];
-  __shared__ float Vm[2][P * (P + 1)];
-  __shared__ int partner[P];
-  __shared__ float cself[P], cpart[P];
-  __shared__ int order[kMaxRank];
-  __shared__ float ritzval[kMaxRank];
-  __shared__ __align__(16) float Xi[kMaxRank * D];
-  __shared__ float red[kBuildThreads];
-
-  const int tid = threadIdx.x;
+  __shared__ __align__(16) char pool[stats_lds_bytes<D, P, KF32>()];
   const int b = blockIdx.z, h = blockIdx.y;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   if (T <= 0) return;
   const int nb = (T + kL - 1) / kL;
   const int j = p.tail_mode ? (T - 1) / kL : p.first_block + (int)blockIdx.x;
   if (j < 0 || j >= nb) return;
-  const int n = min(kL, T - j * kL);
-  const int r = p.r;
-
-  // ---- load the block's keys into registers: RPP rows per pass, 8 elements per thread
-  constexpr int TPR = D / 8;                       // threads per row
-  constexpr int RPP = kBuildThreads / TPR;         // rows per pass
-  constexpr int NPASS = kL / RPP;
-  const int e0 = (tid % TPR) * 8, r0 = tid / TPR;
-  float v[NPASS][8];
-  double cs[8];
-#pragma unroll
-  for (int q = 0; q < 8; ++q) cs[q] = 0.0;
-#pragma unroll
-  for (int ps = 0; ps < NPASS; ++ps) {
-    const int i = r0 + ps * RPP;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) v[ps][q] = 0.0f;
-    const int64_t off = (i < n) ? kv_offset(p.kv, b, h, j * kL + i) : -1;
-    if (off >= 0) {
-      if (p.kv_f32) {
-        const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(p.kv.k) + off + e0);
-        const float4 a = src[0], c = src[1];
-        v[ps][0] = a.x; v[ps][1] = a.y; v[ps][2] = a.z; v[ps][3] = a.w;
-        v[ps][4] = c.x; v[ps][5] = c.y; v[ps][6] = c.z; v[ps][7] = c.w;
-      } else {
-        const uint4 a = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.kv.k) + off + e0);
-        v[ps][0] = bf16_lo(a.x); v[ps][1] = bf16_hi(a.x); v[ps][2] = bf16_lo(a.y); v[ps][3] = bf16_hi(a.y);
-        v[ps][4] = bf16_lo(a.z); v[ps][5] = bf16_hi(a.z); v[ps][6] = bf16_lo(a.w); v[ps][7] = bf16_hi(a.w);
-      }
-    }
-  }
-  // ---- block mean (first cumulant): fp64 column sums in a fixed order (exact for
-  // the block's fp32 keys unless their magnitudes span > 2^29), one rounding to
-  // fp32, so a block of identical keys centres to exact zeros
-#pragma unroll
-  for (int ps = 0; ps < NPASS; ++ps)
-#pragma unroll
-    for (int q = 0; q < 8; ++q) cs[q] += (double)v[ps][q];
-  double* red64 = reinterpret_cast<double*>(Gm);   // RPP x D doubles, free until the Gram
-#pragma unroll
-  for (int q = 0; q < 8; ++q) red64[r0 * D + e0 + q] = cs[q];
-  __syncthreads();
-  if (tid < D) {
-    double sum = 0.0;
-    for (int g = 0; g < RPP; ++g) sum += red64[g * D + tid];
-    mean[tid] = (float)(sum / (double)n);
-  }
-  __syncthreads();
-  const bool factors = (n == kL) && (r > 0);
-  uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
-  const RecLayout lay = p.lay;
-  if (!factors) {
-    // partial block (or r = 0): count, mean, zero factors
-    for (int idx = tid; idx < lay.mean_off / 4; idx += kBuildThreads)
-      reinterpret_cast<uint32_t*>(R)[idx] = (idx == 0) ? (uint32_t)n : 0u;
-    __syncthreads();
-    store_vector(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), tid, kBuildThreads, red);
-    for (int idx = lay.fac_off / 4 + tid; idx < lay.total / 4; idx += kBuildThreads)
-      reinterpret_cast<uint32_t*>(R)[idx] = 0u;
-    return;
-  }
-  // stage the centred keys transposed: KT[e][i] = k_{jL+i}[e] - kbar[e]
-#pragma unroll
-  for (int ps = 0; ps < NPASS; ++ps) {
-    const int i = r0 + ps * RPP;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) KT[(e0 + q) * KS + i] = v[ps][q] - mean[e0 + q];
-  }
-  for (int idx = tid; idx < kMaxRank * D; idx += kBuildThreads) Xi[idx] = 0.0f;
-  __syncthreads();
-  {
-    // ---- Gram matrix Gamma = Kc Kc^T / n, 4x4 tile per thread
-    {
-      const int i0 = 4 * (tid / 16), j0 = 4 * (tid % 16);
-      float acc[4][4] = {};
-      for (int e = 0; e < D; ++e) {
-        const float4 a = *reinterpret_cast<const float4*>(&KT[e * KS + i0]);
-        const float4 c = *reinterpret_cast<const float4*>(&KT[e * KS + j0]);
-        const float av[4] = {a.x, a.y, a.z, a.w}, cv[4] = {c.x, c.y, c.z, c.w};
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-          for (int y = 0; y < 4; ++y) acc[x][y] += av[x] * cv[y];
-      }
-      const float inv_n = 1.0f / (float)n;
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y) Gm[(i0 + x) * kL + j0 + y] = acc[x][y] * inv_n;
-    }
-    for (int idx = tid; idx < kL * P; idx += kBuildThreads) Wm[idx] = init_sign(idx / P, idx % P);
-    __syncthreads();
-
-    for (int it = 0; it <= kPowerIters; ++it) {
-      // ---- Y = Gamma W (Gamma symmetric: read column-wise, conflict free)
-      {
-        constexpr int CPT = P / 4;
-        const int i = tid / 4, c0 = (tid % 4) * CPT;
-        float acc[CPT] = {};
-        for (int k = 0; k < kL; ++k) {
-          const float g = Gm[k * kL + i];
-#pragma unroll
-          for (int c = 0; c < CPT; ++c) acc[c] += g * Wm[k * P + c0 + c];
-        }
-#pragma unroll
-        for (int c = 0; c < CPT; ++c) Ym[i * P + c0 + c] = acc[c];
-      }
-      __syncthreads();
-      if (it == kPowerIters) break;      // last product feeds the Rayleigh-Ritz step
-
-      // ---- Cholesky-QR: S = Y^T Y = L L^T, W = Y L^-T
-      for (int idx = tid; idx < P * P; idx += kBuildThreads) {
-        const int a = idx / P, c = idx % P;
-        float s = 0.0f;
-        for (int i = 0; i < kL; ++i) s += Ym[i * P + a] * Ym[i * P + c];
-        Sm[a * (P + 1) + c] = s;
-      }
-      __syncthreads();
-      if (tid < 64) {
-        float row[P];
-        const int li = tid < P ? tid : 0;
-#pragma unroll
-        for (int c = 0; c < P; ++c) row[c] = Sm[li * (P + 1) + c];
-        float trace = 0.0f;
-#pragma unroll
-        for (int c = 0; c < P; ++c) trace += Sm[c * (P + 1) + c];
-        const float thr = 1e-6f * trace;
-#pragma unroll
-        for (int k = 0; k < P; ++k) {
-          const float piv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[k]), k));
-          const bool ok = piv > thr && piv > 0.0f;
-          const float dk = ok ? sqrtf(piv) : 0.0f;
-          const float rdk = ok ? 1.0f / dk : 0.0f;
-          if (tid > k) row[k] *= rdk;
-          if (tid == k) row[k] = dk;
-          if (tid == 0) rdiag[k] = rdk;
-#pragma unroll
-          for (int c = k + 1; c < P; ++c) {
-            const float lck = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[k]), c));
-            if (tid > k) row[c] -= row[k] * lck;
-          }
-        }
-        if (tid < P) {
-#pragma unroll
-          for (int c = 0; c < P; ++c) Lm[tid * (P + 1) + c] = row[c];
-        }
-      }
-      __syncthreads();
-      if (tid < kL) {
-        float w[P];
-#pragma unroll
-        for (int k = 0; k < P; ++k) {
-          float acc = Ym[tid * P + k];
-#pragma unroll
-          for (int m = 0; m < k; ++m) acc -= w[m] * Lm[k * (P + 1) + m];
-          w[k] = acc * rdiag[k];
-        }
-#pragma unroll
-        for (int k = 0; k < P; ++k) Wm[tid * P + k] = w[k];
-      }
-      __syncthreads();
-    }
-
-    // ---- Rayleigh-Ritz: H = W^T Gamma W (symmetrised), eigenpairs by Jacobi
-    for (int idx = tid; idx < P * P; idx += kBuildThreads) {
-      const int a = idx / P, c = idx % P;
-      float s1 = 0.0f, s2 = 0.0f;
-      for (int i = 0; i < kL; ++i) {
-        s1 += Wm[i * P + a] * Ym[i * P + c];
-        s2 += Wm[i * P + c] * Ym[i * P + a];
-      }
-      Hm[0][a * (P + 1) + c] = 0.5f * (s1 + s2);
-      Vm[0][a * (P + 1) + c] = (a == c) ? 1.0f : 0.0f;
-    }
-    __syncthreads();
-    int cur = 0;
-    for (int sweep = 0; sweep < kJacobiSweeps; ++sweep) {
-      for (int rnd = 0; rnd < P - 1; ++rnd) {
-        if (tid < P / 2) {
-          // round-robin pairing: index 0 fixed, the others rotate
-          const int m1 = tid, m2 = P - 1 - tid;
-          const int x = (m1 == 0) ? 0 : 1 + (m1 - 1 + rnd) % (P - 1);
-          const int y = 1 + (m2 - 1 + rnd) % (P - 1);
-          const int pp = min(x, y), qq = max(x, y);
-          const float* H = Hm[cur];
-          const float app = H[pp * (P + 1) + pp], aqq = H[qq * (P + 1) + qq], apq = H[pp * (P + 1) + qq];
-          float c = 1.0f, s = 0.0f;
-          if (apq != 0.0f) {
-            const float th = (aqq - app) / (2.0f * apq);
-            const float t = (th >= 0.0f ? 1.0f : -1.0f) / (fabsf(th) + sqrtf(th * th + 1.0f));
-            c = 1.0f / sqrtf(t * t + 1.0f);
-            s = t * c;
-          }
-          partner[pp] = qq; partner[qq] = pp;
-          cself[pp] = c; cpart[pp] = -s;
-          cself[qq] = c; cpart[qq] = s;
-        }
-        __syncthreads();
-        const float* H = Hm[cur];
-        const float* V = Vm[cur];
-        float* H2 = Hm[cur ^ 1];
-        float* V2 = Vm[cur ^ 1];
-        for (int idx = tid; idx < P * P; idx += kBuildThreads) {
-          const int a = idx / P, c = idx % P;
-          const int pa = partner[a], pc = partner[c];
-          const float sa = cself[a], ta = cpart[a], sc = cself[c], tc = cpart[c];
-          H2[a * (P + 1) + c] = sa * sc * H[a * (P + 1) + c] + sa * tc * H[a * (P + 1) + pc] +
-                                ta * sc * H[pa * (P + 1) + c] + ta * tc * H[pa * (P + 1) + pc];
-          V2[a * (P + 1) + c] = V[a * (P + 1) + c] * sc + V[a * (P + 1) + pc] * tc;
-        }
-        __syncthreads();
-        cur ^= 1;
-      }
-    }
-    // ---- top-r Ritz values, descending, ties to the lower index (rank by counting)
-    if (tid < P) {
-      const float ta = Hm[cur][tid * (P + 1) + tid];
-      int rank = 0;
-      for (int c = 0; c < P; ++c) {
-        const float tc = Hm[cur][c * (P + 1) + c];
-        rank += (tc > ta) || (tc == ta && c < tid);
-      }
-      if (rank < r) { order[rank] = tid; ritzval[rank] = ta; }
-    }
-    __syncthreads();
-    // Ritz vectors w_i = W V[:, order_i] (into Ym), xi_i = Kc^T w_i / sqrt(n)
-    for (int idx = tid; idx < r * kL; idx += kBuildThreads) {
-      const int i = idx / kL, row = idx % kL;
-      const int col = order[i];
-      float s = 0.0f;
-      for (int a = 0; a < P; ++a) s += Wm[row * P + a] * Vm[cur][a * (P + 1) + col];
-      Ym[i * kL + row] = s;
-    }
-    __syncthreads();
-    const float rs = 1.0f / sqrtf((float)n);
-    const float top = ritzval[0];
-    for (int idx = tid; idx < r * D; idx += kBuildThreads) {
-      const int i = idx / D, e = idx % D;
-      float s = 0.0f;
-      if (ritzval[i] > 1e-6f * top && top > 0.0f) {
-        for (int row = 0; row < kL; ++row) s += KT[e * KS + row] * Ym[i * kL + row];
-        s *= rs;
-      }
-      Xi[i * D + e] = s;
-    }
-    __syncthreads();
-    // ---- sign: largest-magnitude entry positive (lowest index on ties); 16 threads per vector
-    {
-      const int i = tid / 16, lt = tid % 16;
-      float best = -1.0f;
-      int bidx = 0;
-      if (i < r) {
-        for (int e = lt; e < D; e += 16) {
-          const float a = fabsf(Xi[i * D + e]);
-          if (a > best) { best = a; bidx = e; }
-        }
-      }
-#pragma unroll
-      for (int o = 8; o >= 1; o >>= 1) {
-        const float ob = __shfl_xor(best, o, 16);
-        const int oi = __shfl_xor(bidx, o, 16);
-        if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; }
-      }
-      const float pivot = (i < r) ? Xi[i * D + bidx] : 0.0f;
-      __syncthreads();                   // every thread has read its pivot before any flip
-      if (i < r && pivot < 0.0f) {
-        for (int e = lt; e < D; e += 16) Xi[i * D + e] = -Xi[i * D + e];
-      }
-    }
-    __syncthreads();
-  }
-
-  // ---- write the record
-  for (int idx = tid; idx < lay.mean_off / 4; idx += kBuildThreads) {
-    uint32_t v = 0;
-    if (idx == 0) v = (uint32_t)n;
-    reinterpret_cast<uint32_t*>(R)[idx] = v;       // header, factor scales default 0
-  }
-  __syncthreads();
-  store_vector(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), tid,
-               kBuildThreads, red);
-  __syncthreads();
-  for (int i = 0; i < r; ++i) {
-    store_vector(&Xi[i * D], D, p.fdt, R + lay.fac_off + i * lay.vec_bytes,
-                 reinterpret_cast<float*>(R + 16) + i, tid, kBuildThreads, red);
-    __syncthreads();
-  }
-  // zero the tail padding of the record
-  const int used = lay.fac_off + r * lay.vec_bytes;
-  for (int idx = used / 4 + tid; idx < lay.total / 4; idx += kBuildThreads)
-    reinterpret_cast<uint32_t*>(R)[idx] = 0u;
+  StatsArgs a;
+  a.kv = p.kv;
+  a.rec = p.rec;
+  a.hkv = p.hkv;
+  a.nbmax = p.nbmax;
+  a.r = p.r;
+  a.mdt = p.mdt;
+  a.fdt = p.fdt;
+  a.lay = p.lay;
+  block_stats<D, P, KF32>(a, b, h, j, min(kL, T - j * kL), pool);
 }
 
 // E2M1 encoding of independent vectors, one workgroup per vector.
@@ -411,7 +52,8 @@ __global__ __launch_bounds__(256) void pack_e2m1_kernel(const float* x, int dim,
 // ------------------------------------------------------------- launchers --
 template <int D, int P>
 static hipError_t launch_build_dp(const BuildParams& p, dim3 grid, hipStream_t st) {
-  hipLaunchKernelGGL((build_stats_kernel<D, P>), grid, dim3(kBuildThreads), 0, st, p);
+  if (p.kv_f32) hipLaunchKernelGGL((build_stats_kernel<D, P, true>), grid, dim3(kBuildThreads), 0, st, p);
+  else hipLaunchKernelGGL((build_stats_kernel<D, P, false>), grid, dim3(kBuildThreads), 0, st, p);
   return hipGetLastError();
 }
 

@@ -126,6 +126,11 @@ struct FinishLds {
   uint32_t gtw[kMaxBlocksPerSeq / 32], eqw[kMaxBlocksPerSeq / 32];
 };
 
+// One LDS pool per selector workgroup, shared by its sequential phases: the
+// scoring loop and the finishing phase.
+template <size_t MAIN>
+constexpr size_t select_pool_bytes() { return sizeof(FinishLds) > MAIN ? sizeof(FinishLds) : MAIN; }
+
 template <int G, int KPT>
 __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds& F) {
   static_assert(KPT * kSelThreads <= kMaxBlocksPerSeq, "key slots");
@@ -331,7 +336,9 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
   constexpr int EPL = D / 16;
   constexpr int MW = slice_words<MDT, EPL>(), FW = slice_words<FDT, EPL>();
   constexpr int SW = (FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0;    // 16-byte words of factor scales
-  __shared__ float gm[16][G], gs[16][G];
+  __shared__ __align__(16) char pool[select_pool_bytes<2 * 16 * G * 4>()];
+  float (*gm)[G] = reinterpret_cast<float (*)[G]>(pool);
+  float (*gs)[G] = reinterpret_cast<float (*)[G]>(pool + 16 * G * 4);
   __shared__ int s_last;
 
   const int tid = threadIdx.x;
@@ -449,7 +456,7 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
     st_agent(&pp[1], s);
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
-  __shared__ FinishLds fin;
+  FinishLds& fin = *reinterpret_cast<FinishLds*>(pool);
   const int nc = (max(0, T - p.w) + kL - 1) / kL;
   if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
   else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
@@ -499,8 +506,10 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
   constexpr int KST = D / 32;                                  // k-steps per lane group
   constexpr int MW = elem_bytes<MDT>(D / 4) / 4, FW = elem_bytes<FDT>(D / 4) / 4;
   constexpr int HU = 1 + ((FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0);   // 16-byte header words used
-  __shared__ float gm[4][G], gs[4][G];
-  __shared__ uint4 hdr_s[4][16][HU];
+  __shared__ __align__(16) char pool[select_pool_bytes<4 * 16 * HU * 16 + 2 * 4 * G * 4>()];
+  uint4 (*hdr_s)[16][HU] = reinterpret_cast<uint4 (*)[16][HU]>(pool);
+  float (*gm)[G] = reinterpret_cast<float (*)[G]>(pool + 4 * 16 * HU * 16);
+  float (*gs)[G] = reinterpret_cast<float (*)[G]>(pool + 4 * 16 * HU * 16 + 4 * G * 4);
   __shared__ int s_last;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -634,7 +643,7 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
     st_agent(&pp[1], s);
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
-  __shared__ FinishLds fin;
+  FinishLds& fin = *reinterpret_cast<FinishLds*>(pool);
   const int nc = (max(0, T - p.w) + kL - 1) / kL;
   if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
   else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
