@@ -374,13 +374,22 @@ __device__ __forceinline__ void decode_task(const DecodeParams& p, int b, int h,
 // products sum to the fp32 query within 2^-16 relative.  The 16 x 16 score tile
 // lands with lane l holding tokens 16*mt + 4*(l/16) + i of head l % 16, so the
 // softmax statistics of head h live in the lanes with l % 16 == h.
-// Probabilities go through LDS to the V layout, where each lane accumulates its
-// 8 output columns for every head.
+// From 8 query heads per KV head on, P.V runs on the matrix cores too: the
+// probabilities stay in the registers the score tile left them in (the B
+// operand, token order permuted to match) and V, loaded straight into LDS with
+// swizzled chunks, is read by column.  With fewer heads the probabilities go
+// through LDS to the V row layout and each lane accumulates its 8 output
+// columns for every head on the vector ALUs.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
+
+// Chunk swizzle of a V tile row in LDS: the four lane groups of a wave read
+// rows 4 g + j and 16 + 4 g + j, i.e. (row >> 2) & 3 = g, so XOR-ing the
+// 16-byte chunk index with 2 g puts their reads on disjoint banks.
+__device__ __forceinline__ int vswz(int row) { return 2 * ((row >> 2) & 3); }
 
 template <int D, int G>
 __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, int h, int wg) {
@@ -390,10 +399,15 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   constexpr int RPI = 64 / CPR;               // V rows per load instruction
   constexpr int PT = 32;                      // tokens per piece
   constexpr int VC = PT / RPI;                // V chunks per lane per piece
+  constexpr int NDT = D / 16;                 // 16-column tiles of the output
   constexpr int GP = (G + 3) / 4 * 4;
+  // P.V on the matrix cores pays from G = 8 query heads per KV head on (its
+  // 16 head columns are mostly padding below that); fewer heads use the VALU
+  constexpr bool kMatPV = G >= 8;
 
   __shared__ __align__(16) float qs[G][D];
-  __shared__ __align__(16) float ps[4][PT][GP];
+  __shared__ __align__(16) uint16_t vt[kMatPV ? 4 : 1][kMatPV ? PT * D : 1];   // V tiles, swizzled chunks
+  __shared__ __align__(16) float ps[kMatPV ? 1 : 4][kMatPV ? 1 : PT][GP];      // P to the V layout
   __shared__ float wm[4][G], wl[4][G];
   __shared__ __align__(16) float wo[4][G][D];
   __shared__ int s_last, s_red[4];
@@ -433,9 +447,15 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   const int vchunk = lane % CPR, vrow0 = lane / CPR;
 
   float m_run = -INFINITY, l_run = 0.0f;      // statistics of head hcol
-  float o[G][8];
+  // matrix-core P.V: output tile t in the C layout, lane l holds
+  // O[16 t + 4 (l/16) + v][head l % 16]; vector P.V: lane l holds the 8 output
+  // columns of its V chunk for every head
+  f32x4_t oacc[kMatPV ? NDT : 1];
+  float o[kMatPV ? 1 : G][8];
 #pragma unroll
-  for (int g = 0; g < G; ++g)
+  for (int t = 0; t < (kMatPV ? NDT : 1); ++t) oacc[t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int g = 0; g < (kMatPV ? 1 : G); ++g)
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.0f;
 
@@ -460,10 +480,23 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
 #pragma unroll
       for (int kk = 0; kk < KST; ++kk) kr[mt][kk] = *reinterpret_cast<const uint4*>(kp + off + 64 * kk);
     }
-    uint4 vr[VC];
+    uint4 vr[kMatPV ? 1 : VC];
+    if constexpr (kMatPV) {
+      // V straight into this wave's LDS tile (16 bytes per lane, slot = lane):
+      // row r keeps its 16-byte chunk c at position c ^ vswz(r), so the column
+      // reads below spread over all banks
 #pragma unroll
-    for (int i = 0; i < VC; ++i) {
-      vr[i] = reinterpret_cast<const uint4*>(vp + min(vrow0 + RPI * i, n - 1) * rsb)[vchunk];
+      for (int i = 0; i < VC; ++i) {
+        const int row = vrow0 + RPI * i;
+        const int chunk = vchunk ^ vswz(row);
+        __builtin_amdgcn_global_load_lds(vp + min(row, n - 1) * rsb + 16 * chunk,
+                                         (__attribute__((address_space(3))) void*)(&vt[wave][0] + i * 512),
+                                         16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < VC; ++i)
+        vr[i] = reinterpret_cast<const uint4*>(vp + min(vrow0 + RPI * i, n - 1) * rsb)[vchunk];
     }
     __builtin_amdgcn_sched_barrier(0);   // every load of the piece ahead of its arithmetic
 
@@ -505,59 +538,105 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
     ls += __shfl_xor(ls, 32, 64);
     l_run = l_run * alpha + ls;
     m_run = mn;
-    if (hcol < G) {
+    if constexpr (kMatPV) {
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
+      for (int t = 0; t < NDT; ++t) oacc[t] *= alpha;
+      // ---- values on the matrix cores: O^T[d][head] += V^T[d][token] P[token][head].
+      // The token order of the contraction is free: operand element j of lane l
+      // stands for token 4 (l/16) + j (j < 4) or 16 + 4 (l/16) + j - 4, which
+      // is where the score tile left that lane's probabilities, so P (split into
+      // bf16 high and low parts) is the B operand as it is; V is read from LDS
+      // by column.
+      bf16x8_t phi, plo;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) ps[wave][16 * mt + 4 * lgrp + i][hcol] = sc[mt][i];
-    }
-    // every head's accumulator is rescaled by its own alpha (held by lane g)
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float ag = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), g));
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[g][e] *= ag;
-    }
-    wave_lds_sync();
-    // ---- values
-#pragma unroll
-    for (int i = 0; i < VC; ++i) {
-      const int row = vrow0 + RPI * i;
-      float vf[8];
-      unpack16<false>(vr[i], vf);
-      float pg[GP];
-#pragma unroll
-      for (int g = 0; g < GP; g += 4) {
-        const float4 pp = *reinterpret_cast<const float4*>(&ps[wave][row][g]);
-        pg[g] = pp.x; pg[g + 1] = pp.y; pg[g + 2] = pp.z; pg[g + 3] = pp.w;
+      for (int j = 0; j < 8; ++j) {
+        const float x = (j < 4) ? sc[0][j] : sc[1][j - 4];
+        const uint32_t hb = f32_to_bf16_rne(x);
+        const uint32_t lb = f32_to_bf16_rne(x - __uint_as_float(hb << 16));
+        phi[j] = __builtin_bit_cast(__bf16, (uint16_t)hb);
+        plo[j] = __builtin_bit_cast(__bf16, (uint16_t)lb);
       }
+      __builtin_amdgcn_s_waitcnt(0);       // the V tile has landed in LDS
+      wave_lds_sync();
 #pragma unroll
-      for (int g = 0; g < G; ++g)
+      for (int t = 0; t < NDT; ++t) {
+        bf16x8_t va;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) o[g][e] += pg[g] * vf[e];
+        for (int j = 0; j < 8; ++j) {
+          const int row = (j < 4) ? 4 * lgrp + j : 16 + 4 * lgrp + (j - 4);
+          const int col = 16 * t + hcol;
+          va[j] = __builtin_bit_cast(__bf16, vt[wave][row * D + 8 * ((col >> 3) ^ vswz(row)) + (col & 7)]);
+        }
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi, oacc[t], 0, 0, 0);
+        oacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo, oacc[t], 0, 0, 0);
+      }
+      wave_lds_sync();                     // vt is rewritten by the next piece
+    } else {
+      if (hcol < G) {
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) ps[wave][16 * mt + 4 * lgrp + i][hcol] = sc[mt][i];
+      }
+      // every head's accumulator is rescaled by its own alpha (held by lane g)
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float ag = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), g));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[g][e] *= ag;
+      }
+      wave_lds_sync();
+      // ---- values on the vector ALUs, V in row chunks
+#pragma unroll
+      for (int i = 0; i < VC; ++i) {
+        const int row = vrow0 + RPI * i;
+        float vf[8];
+        unpack16<false>(vr[i], vf);
+        float pg[GP];
+#pragma unroll
+        for (int g = 0; g < GP; g += 4) {
+          const float4 pp = *reinterpret_cast<const float4*>(&ps[wave][row][g]);
+          pg[g] = pp.x; pg[g + 1] = pp.y; pg[g + 2] = pp.z; pg[g + 3] = pp.w;
+        }
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o[g][e] += pg[g] * vf[e];
+      }
+      wave_lds_sync();
     }
-    wave_lds_sync();
    }
   }
 
-  // ---- combine the lanes sharing a column chunk, then the four waves
+  // ---- the four waves' states, then one partial per workgroup
+  if constexpr (kMatPV) {
+    if (hcol < G) {
+      if (lgrp == 0) { wm[wave][hcol] = m_run; wl[wave][hcol] = l_run; }
 #pragma unroll
-  for (int mask = CPR; mask < 64; mask <<= 1)
+      for (int t = 0; t < NDT; ++t)
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+        for (int v = 0; v < 4; ++v) wo[wave][hcol][16 * t + 4 * lgrp + v] = oacc[t][v];
+    }
+  } else {
+    // combine the lanes sharing a column chunk
 #pragma unroll
-      for (int e = 0; e < 8; ++e) o[g][e] += __shfl_xor(o[g][e], mask, 64);
+    for (int mask = CPR; mask < 64; mask <<= 1)
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const float mg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m_run), g));
-    const float lg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(l_run), g));
-    if (lane == 0) { wm[wave][g] = mg; wl[wave][g] = lg; }
-  }
-  if (lane < CPR) {
+      for (int g = 0; g < G; ++g)
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+        for (int e = 0; e < 8; ++e) o[g][e] += __shfl_xor(o[g][e], mask, 64);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) wo[wave][g][lane * 8 + e] = o[g][e];
+    for (int g = 0; g < G; ++g) {
+      const float mg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(m_run), g));
+      const float lg = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(l_run), g));
+      if (lane == 0) { wm[wave][g] = mg; wl[wave][g] = lg; }
+    }
+    if (lane < CPR) {
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) wo[wave][g][lane * 8 + e] = o[g][e];
+    }
   }
   __syncthreads();
   float* wpart = p.part + ((int64_t)unit * p.nwg + wg) * G * (D + 2);

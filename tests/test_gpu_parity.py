@@ -66,6 +66,8 @@ SELECT_CASES = [
     (128, 4, 16, "bf16", "f32", 40, 256),
     (128, 4, 4, "f32", "f32", 0, 128),
     (128, 4, 4, "f32", "f32", 100, 128),
+    (64, 8, 4, "e2m1", "e2m1", 6, 64),
+    (64, 4, 2, "bf16", "bf16", 9, 200),
 ]
 
 
@@ -128,6 +130,8 @@ DECODE_CASES = [
     (64, 2, "f32", 5, 1000),
     (128, 16, "bf16", 7, 300),
     (128, 4, "f32", 0, 200),
+    (64, 8, "bf16", 5, 128),
+    (64, 4, "bf16", 6, 64),
 ]
 
 
