@@ -18,6 +18,8 @@
 
 #include "cobs_kernels.h"
 
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
 namespace cobs {
 
 constexpr int kBuildThreads = 256;
@@ -90,8 +92,7 @@ struct StatsLds {
   static constexpr size_t ym = al(wm + 4 * kL * P);
   static constexpr size_t sm = al(ym + 4 * kL * P);
   static constexpr size_t lm = al(sm + 4 * P * (P + 1));
-  static constexpr size_t rdiag = al(lm + 4 * P * (P + 1));
-  static constexpr size_t hm = al(rdiag + 4 * P);          // [2][P(P+1)]
+  static constexpr size_t hm = al(lm + 4 * P * (P + 1));   // [2][P(P+1)]
   static constexpr size_t vm = al(hm + 8 * P * (P + 1));   // [2][P(P+1)]
   static constexpr size_t partner = al(vm + 8 * P * (P + 1));
   static constexpr size_t cself = al(partner + 4 * P);
@@ -119,7 +120,6 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   float* Ym = reinterpret_cast<float*>(pool + Lay::ym);
   float* Sm = reinterpret_cast<float*>(pool + Lay::sm);
   float* Lm = reinterpret_cast<float*>(pool + Lay::lm);
-  float* rdiag = reinterpret_cast<float*>(pool + Lay::rdiag);
   float (*Hm)[P * (P + 1)] = reinterpret_cast<float (*)[P * (P + 1)]>(pool + Lay::hm);
   float (*Vm)[P * (P + 1)] = reinterpret_cast<float (*)[P * (P + 1)]>(pool + Lay::vm);
   int* partner = reinterpret_cast<int*>(pool + Lay::partner);
@@ -229,72 +229,105 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     for (int idx = tid; idx < kL * P; idx += kBuildThreads) Wm[idx] = init_sign(idx / P, idx % P);
     __syncthreads();
 
+    // Matrix products of the iteration on the fp32 matrix cores
+    // (v_mfma_f32_16x16x4_f32: lane l holds A[l%16][l/16] and B[l/16][l%16] and
+    // gets D[4(l/16)+v][l%16]).  Wave w owns rows [16w, 16w+16) of the 64 x P
+    // products.
+    const int lane = tid & 63, wave = tid >> 6;
+    const int lr = lane & 15, lk = lane >> 4;
     for (int it = 0; it <= kPowerIters; ++it) {
-      // ---- Y = Gamma W (Gamma symmetric: read column-wise, conflict free)
+      // ---- Y = Gamma W (Gamma symmetric: read by column, conflict free)
       {
-        constexpr int CPT = P / 4;
-        const int i = tid / 4, c0 = (tid % 4) * CPT;
-        float acc[CPT] = {};
-        for (int k = 0; k < kL; ++k) {
-          const float g = Gm[k * kL + i];
+        f32x4_t acc[P / 16];
 #pragma unroll
-          for (int c = 0; c < CPT; ++c) acc[c] += g * Wm[k * P + c0 + c];
+        for (int ct = 0; ct < P / 16; ++ct) acc[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 4
+        for (int k0 = 0; k0 < kL; k0 += 4) {
+          const float a = Gm[(k0 + lk) * kL + 16 * wave + lr];
+#pragma unroll
+          for (int ct = 0; ct < P / 16; ++ct)
+            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Wm[(k0 + lk) * P + 16 * ct + lr], acc[ct], 0, 0, 0);
         }
 #pragma unroll
-        for (int c = 0; c < CPT; ++c) Ym[i * P + c0 + c] = acc[c];
+        for (int ct = 0; ct < P / 16; ++ct)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) Ym[(16 * wave + 4 * lk + v) * P + 16 * ct + lr] = acc[ct][v];
       }
       __syncthreads();
       if (it == kPowerIters) break;      // last product feeds the Rayleigh-Ritz step
 
-      // ---- Cholesky-QR: S = Y^T Y = L L^T, W = Y L^-T
-      for (int idx = tid; idx < P * P; idx += kBuildThreads) {
-        const int a = idx / P, c = idx % P;
-        float s = 0.0f;
-        for (int i = 0; i < kL; ++i) s += Ym[i * P + a] * Ym[i * P + c];
-        Sm[a * (P + 1) + c] = s;
+      // ---- S = Y^T Y, 16 x 16 tiles spread over the waves
+      for (int tl = wave; tl < (P / 16) * (P / 16); tl += 4) {
+        const int ta = tl / (P / 16), tc = tl % (P / 16);
+        f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 4
+        for (int k0 = 0; k0 < kL; k0 += 4)
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Ym[(k0 + lk) * P + 16 * ta + lr],
+                                                     Ym[(k0 + lk) * P + 16 * tc + lr], acc, 0, 0, 0);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) Sm[(16 * ta + 4 * lk + v) * (P + 1) + 16 * tc + lr] = acc[v];
       }
       __syncthreads();
-      if (tid < 64) {
+      // ---- S = L L^T (Cholesky) and X = L^-1, in wave 0: lane k < P holds row k
+      // of L, then column k of X; a pivot below 1e-6 trace (rank deficit) gives a
+      // zero column
+      if (wave == 0) {
         float row[P];
-        const int li = tid < P ? tid : 0;
+        const int li = lane < P ? lane : 0;
 #pragma unroll
         for (int c = 0; c < P; ++c) row[c] = Sm[li * (P + 1) + c];
         float trace = 0.0f;
 #pragma unroll
         for (int c = 0; c < P; ++c) trace += Sm[c * (P + 1) + c];
         const float thr = 1e-6f * trace;
+        float rd[P];
 #pragma unroll
         for (int k = 0; k < P; ++k) {
           const float piv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[k]), k));
           const bool ok = piv > thr && piv > 0.0f;
           const float dk = ok ? sqrtf(piv) : 0.0f;
           const float rdk = ok ? 1.0f / dk : 0.0f;
-          if (tid > k) row[k] *= rdk;
-          if (tid == k) row[k] = dk;
-          if (tid == 0) rdiag[k] = rdk;
+          rd[k] = rdk;
+          if (lane > k) row[k] *= rdk;
+          if (lane == k) row[k] = dk;
 #pragma unroll
           for (int c = k + 1; c < P; ++c) {
             const float lck = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[k]), c));
-            if (tid > k) row[c] -= row[k] * lck;
+            if (lane > k) row[c] -= row[k] * lck;
           }
         }
-        if (tid < P) {
+        // X = L^-1 by forward substitution, lane c computing column c
+        float x[P];
 #pragma unroll
-          for (int c = 0; c < P; ++c) Lm[tid * (P + 1) + c] = row[c];
+        for (int k = 0; k < P; ++k) {
+          float acc = (k == lane) ? 1.0f : 0.0f;
+#pragma unroll
+          for (int m = 0; m < k; ++m)
+            acc -= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[m]), k)) * x[m];
+          x[k] = acc * rd[k];
+        }
+        if (lane < P) {
+#pragma unroll
+          for (int k = 0; k < P; ++k) Lm[lane * (P + 1) + k] = x[k];     // Lm[c][k] = X[k][c]
         }
       }
       __syncthreads();
-      if (tid < kL) {
-        float w[P];
+      // ---- W = Y X^T: operand B[k][c] = X[c][k], which Lm holds at [k][c]
+      {
+        f32x4_t acc[P / 16];
 #pragma unroll
-        for (int k = 0; k < P; ++k) {
-          float acc = Ym[tid * P + k];
+        for (int ct = 0; ct < P / 16; ++ct) acc[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-          for (int m = 0; m < k; ++m) acc -= w[m] * Lm[k * (P + 1) + m];
-          w[k] = acc * rdiag[k];
+        for (int k0 = 0; k0 < P; k0 += 4) {
+          const float a = Ym[(16 * wave + lr) * P + k0 + lk];
+#pragma unroll
+          for (int ct = 0; ct < P / 16; ++ct)
+            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Lm[(k0 + lk) * (P + 1) + 16 * ct + lr], acc[ct], 0, 0, 0);
         }
 #pragma unroll
-        for (int k = 0; k < P; ++k) Wm[tid * P + k] = w[k];
+        for (int ct = 0; ct < P / 16; ++ct)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) Wm[(16 * wave + 4 * lk + v) * P + 16 * ct + lr] = acc[ct][v];
       }
       __syncthreads();
     }
