@@ -190,4 +190,38 @@ __device__ __forceinline__ float row16_sum(float x) {
   return x;
 }
 
+
+// Inclusive prefix sum over the 64 lanes (DPP only): row shifts by 1, 2, 4, 8,
+// then lane 15's total into rows 1 and 3 and lane 31's into rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);   // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);   // row_bcast:31
+  return x;
+}
+
+// Maximum of `mx` and minimum of `mn` over the 64 lanes, returned in every
+// lane (DPP within rows, row broadcasts into lane 63, then a read of lane 63).
+__device__ __forceinline__ void wave_umax_umin(uint32_t& mx, uint32_t& mn) {
+#define COBS_DPP_MAXMIN(ctrl, rmask)                                                          \
+  {                                                                                          \
+    const uint32_t a = (uint32_t)__builtin_amdgcn_update_dpp((int)mx, (int)mx, ctrl, rmask, 0xF, false); \
+    const uint32_t b = (uint32_t)__builtin_amdgcn_update_dpp((int)mn, (int)mn, ctrl, rmask, 0xF, false); \
+    mx = a > mx ? a : mx;                                                                    \
+    mn = b < mn ? b : mn;                                                                    \
+  }
+  COBS_DPP_MAXMIN(0xB1, 0xF)     // quad xor 1
+  COBS_DPP_MAXMIN(0x4E, 0xF)     // quad xor 2
+  COBS_DPP_MAXMIN(0x141, 0xF)    // row half mirror
+  COBS_DPP_MAXMIN(0x140, 0xF)    // row mirror: every lane of a row holds the row's result
+  COBS_DPP_MAXMIN(0x142, 0xA)    // row_bcast:15 into rows 1, 3
+  COBS_DPP_MAXMIN(0x143, 0xC)    // row_bcast:31 into rows 2, 3: lane 63 holds the wave's result
+#undef COBS_DPP_MAXMIN
+  mx = (uint32_t)__builtin_amdgcn_readlane((int)mx, 63);
+  mn = (uint32_t)__builtin_amdgcn_readlane((int)mn, 63);
+}
+
 }  // namespace cobs

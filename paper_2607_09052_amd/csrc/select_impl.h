@@ -81,12 +81,7 @@ constexpr int slice_words() { return elem_bytes<DT>(EPL) >= 4 ? elem_bytes<DT>(E
 // shuffle scans, then the four wave totals); *total gets the sum.
 __device__ inline int block_excl_scan(int v, int* wsum, int* total) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+  const int x = wave_incl_scan(v);
   if (lane == 63) wsum[wave] = x;
   __syncthreads();
   int pre = 0;
@@ -116,11 +111,18 @@ __device__ __forceinline__ void load_g(__amdgpu_buffer_rsrc_t view, uint32_t off
   }
 }
 
+// Radix histograms are kept in kHistCopies copies, lane l counting into copy
+// l % kHistCopies, so lanes whose keys share a digit mostly update different
+// LDS words (atomics on one word serialise).  A copy's row is padded to
+// kHistRow words: the copies of one bin sit in different banks.
+constexpr int kHistCopies = 8;
+constexpr int kHistRow = 260;
+
 // LDS of the finishing phase (one instance per kernel, whatever slot bound runs).
 struct FinishLds {
   float lse[kMaxG];
   uint32_t red[2][kSelThreads / 64];
-  __align__(16) int hist[2][256];
+  __align__(16) int hist[2][kHistCopies * kHistRow];
   int scan[kSelThreads / 64];
   int digit, rem, cnt;
   uint32_t gtw[kMaxBlocksPerSeq / 32], eqw[kMaxBlocksPerSeq / 32];
@@ -154,7 +156,14 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
   const __amdgpu_buffer_rsrc_t ellu = coherent_view(p.ell + (int64_t)unit * p.nbmax * G, 4u * p.nbmax * G);
   const int last = max(nc - 1, 0);
 
-  hist[0][tid] = 0;
+  // clear both histogram buffers (one 16-byte word of each copy row per thread)
+  const int4 zero4 = make_int4(0, 0, 0, 0);
+  auto clear_hist = [&](int buf) {
+#pragma unroll
+    for (int i = tid; i < kHistCopies * 64; i += kSelThreads)
+      *reinterpret_cast<int4*>(&hist[buf][(i / 64) * kHistRow + 4 * (i % 64)]) = zero4;
+  };
+  clear_hist(0);
   // first batch of scores, issued before the partial merge
   float v[UB][G];
 #pragma unroll
@@ -220,19 +229,16 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
   auto live = [&](int u) { return u * kSelThreads + tid < nc; };
 
   uint32_t kth = 0;
-  int need = k;           // keys equal to kth to take, lowest index first
-  int neq = nc;           // keys equal to kth
+  uint32_t kmask = 0xffffffffu;   // key bits that decide membership in the kth bin
+  int need = k;           // keys of the kth bin to take, lowest index first
+  int neq = nc;           // keys in the kth bin
   const bool all = (k == nc);   // every candidate is selected
   if (k > 0 && k < nc) {
     uint32_t kmax = 0u, kmin = 0xffffffffu;
 #pragma unroll
     for (int u = 0; u < KPT; ++u)
       if (u < U && live(u)) { kmax = max(kmax, key[u]); kmin = min(kmin, key[u]); }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o, 64));
-      kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o, 64));
-    }
+    wave_umax_umin(kmax, kmin);
     if (lane == 0) { red_s[0][wave] = kmax; red_s[1][wave] = kmin; }
     __syncthreads();
     kmax = max(max(red_s[0][0], red_s[0][1]), max(red_s[0][2], red_s[0][3]));
@@ -241,30 +247,35 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
     if (diff == 0u) {
       kth = kmax;          // all candidate keys equal: the k lowest indices
     } else {
-      int shift = ((31 - __clz(diff)) / 8) * 8;     // byte holding the highest differing bit
-      uint32_t mask = (shift == 24) ? 0u : (0xffffffffu << (shift + 8));
+      // Digits of up to 8 bits from the highest bit where the candidates differ
+      // down; the bits above it are common to all of them.  A pass whose
+      // chosen bin holds exactly the keys still needed ends the search: the
+      // whole bin is taken.
+      int lo = 32 - __clz(diff);                     // bits [0, lo) unresolved
+      uint32_t mask = (lo == 32) ? 0u : (0xffffffffu << lo);
       uint32_t prefix = kmax & mask;
-      int rem = k, cur = 0;
-      for (; shift >= 0; shift -= 8) {
-        // histogram of this byte over the keys matching the prefix; the other
-        // buffer is cleared for the next pass
+      int rem = k, cnt = nc, cur = 0;
+      while (lo > 0) {
+        const int shift = max(lo - 8, 0);
+        const uint32_t dmask = (1u << (lo - shift)) - 1u;
 #pragma unroll
         for (int u = 0; u < KPT; ++u)
-          if (u < U && live(u) && (key[u] & mask) == prefix) atomicAdd(&hist[cur][(key[u] >> shift) & 255u], 1);
-        hist[cur ^ 1][tid] = 0;
+          if (u < U && live(u) && (key[u] & mask) == prefix)
+            atomicAdd(&hist[cur][(lane % kHistCopies) * kHistRow + ((key[u] >> shift) & dmask)], 1);
+        clear_hist(cur ^ 1);             // the other buffer, for the next pass
         __syncthreads();
         if (wave == 0) {
           // lane l holds digits 255-4l .. 252-4l; the digit holding the rem-th
           // largest key is where the running count from the top reaches rem
-          const int4 hv = *reinterpret_cast<const int4*>(&hist[cur][252 - 4 * lane]);
+          int4 hv = zero4;
+#pragma unroll
+          for (int c = 0; c < kHistCopies; ++c) {
+            const int4 x = *reinterpret_cast<const int4*>(&hist[cur][c * kHistRow + 252 - 4 * lane]);
+            hv.x += x.x; hv.y += x.y; hv.z += x.z; hv.w += x.w;
+          }
           const int c4[4] = {hv.w, hv.z, hv.y, hv.x};
           const int sum = c4[0] + c4[1] + c4[2] + c4[3];
-          int incl = sum;
-#pragma unroll
-          for (int o = 1; o < 64; o <<= 1) {
-            const int y = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += y;
-          }
+          const int incl = wave_incl_scan(sum);
           int e = incl - sum;
           if (e < rem && incl >= rem) {
 #pragma unroll
@@ -276,12 +287,16 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
         }
         __syncthreads();
         prefix |= (uint32_t)s_digit << shift;
-        mask |= 255u << shift;
+        mask |= dmask << shift;
         rem = s_rem;
+        cnt = s_cnt;
         cur ^= 1;
+        lo = shift;
+        if (cnt == rem) break;
       }
-      neq = s_cnt;
+      neq = cnt;
       kth = prefix;
+      kmask = mask;
       need = rem;
     }
   }
@@ -292,8 +307,8 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
   for (int u = 0; u < KPT; ++u) {
     if (u < U) {
       const bool lv = live(u);
-      const uint64_t gt = __ballot(lv && (all || key[u] > kth));
-      const uint64_t eq = __ballot(lv && !all && key[u] == kth);
+      const uint64_t gt = __ballot(lv && (all || (key[u] & kmask) > kth));
+      const uint64_t eq = __ballot(lv && !all && (key[u] & kmask) == kth);
       if (lane == 0) {
         const int w0 = 8 * u + 2 * wave;
         gtw[w0] = (uint32_t)gt; gtw[w0 + 1] = (uint32_t)(gt >> 32);

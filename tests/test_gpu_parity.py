@@ -119,6 +119,42 @@ def test_select_ties_go_to_lower_index():
     assert sel.cpu().tolist() == [[[0, 1, 2, 3, 4]]]
 
 
+def test_select_long_context_and_boundary_tie_group():
+    """Up to 8192 blocks (every key-slot width of the top-s search) and a group of
+    identical records straddling the s-th place: the lowest-index copies win."""
+    d, G, Hkv, s, w = 128, 4, 1, 85, 512
+    seq = np.array([8192 * 64, 300005, 40000], np.int32)
+    B, Tmax = len(seq), int(seq.max())
+    cfg = _cfg(batch=B, num_q_heads=G, num_kv_heads=Hkv, max_seq_len=Tmax, budget=s, window=w)
+    rec = synth.make_records(B, Hkv, Tmax, 64, d, 4, "f32", "f32", seq, seed=41)
+    q = torch.randn(B, G, d, generator=torch.Generator().manual_seed(42))
+    planted = {}
+    for b in range(B):
+        sigma, nc, _ = oracle_select(rec[b, 0].numpy(), q[b].double().numpy(), int(seq[b]), cfg)
+        order = sorted(range(nc), key=lambda j: (-sigma[j], j))
+        src = order[s - 3]                       # copies take places s-3 .. s+3
+        dst = [j for j in order[s + 40:] if j % 7 == 3][:6]
+        for j in dst:
+            rec[b, 0, j] = rec[b, 0, src]
+        planted[b] = sorted([src] + dst)
+    sel = torch.full((B, Hkv, s), -7, dtype=torch.int32, device=DEV)
+    ws = cobs.new_workspace(cfg, cobs.OP_SELECT, DEV)
+    say(f"select long context, seq={seq.tolist()}")
+    cobs.cobs_select(cfg, q.to(DEV), rec.to(DEV), torch.from_numpy(seq).to(DEV), sel, ws)
+    sync()
+    sel_h = sel.cpu().numpy()
+    for b in range(B):
+        sigma, nc, want = oracle_select(rec[b, 0].numpy(), q[b].double().numpy(), int(seq[b]), cfg)
+        grp = planted[b]
+        assert np.all(sigma[grp] == sigma[grp[0]])
+        others = np.delete(sigma[:nc], grp)
+        # the group is the only near-tie at the boundary, so the set is exact
+        assert np.min(np.abs(others - sigma[grp[0]])) >= 1e-4
+        assert np.array_equal(sel_h[b, 0], np.sort(np.asarray(want))), (b, sel_h[b, 0], want)
+        taken = sorted(set(grp) & set(sel_h[b, 0].tolist()))
+        assert 0 < len(taken) < len(grp) and taken == grp[:len(taken)], (grp, taken)   # straddles; lowest win
+
+
 # ---------------------------------------------------------- sparse decode --
 
 DECODE_CASES = [
