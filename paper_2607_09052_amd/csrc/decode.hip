@@ -421,11 +421,9 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   const int nc = (ws + kL - 1) / kL;
   const int nwin = (T > ws) ? ((T - 1) / kL - ws / kL + 1) : 0;
   const int npiece = 2 * (p.s + nwin);
-  const int pc_lo = wg * p.spw, pc_end = min(npiece, pc_lo + p.spw);
   const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;        // elements between consecutive tokens
 
-  decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pc_lo, max(0, min(kDecThreads, pc_end - pc_lo)), true,
-                            qs, s_red, pn_s, pbase_s);
+  decode_prologue<D, G, PT>(p, b, h, T, ws, nc, 0, min(kDecThreads, npiece), true, qs, s_red, pn_s, pbase_s);
 
   // B operands: query head l % 16 (zero beyond G), columns 32*kk + 8*(l/16) + j
   const int hcol = lane & 15, lgrp = lane >> 4;
@@ -459,12 +457,27 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.0f;
 
-  for (int pb = pc_lo; pb < pc_end; pb += kDecThreads) {
-   const int cnt = min(kDecThreads, pc_end - pb);
-   if (pb != pc_lo) decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pb, cnt, false, qs, s_red, pn_s, pbase_s);
-   for (int it = wave; it < cnt; it += 4) {
+  // Pieces are handed out on demand, which evens out workgroups that stream at
+  // different rates: wave w of workgroup wg starts with piece 4 wg + w, and
+  // every later piece comes from the unit's counter (past the 4 nwg starting
+  // pieces), requested while the current piece's loads are in flight.  The
+  // pieces are described in tables of kDecThreads; a wave holding a piece of a
+  // later table waits for it at that table's barriers.
+  unsigned* pctr = p.pcnt + (int64_t)unit * kPieceCounterStride;
+  const int dyn0 = 4 * p.nwg;
+  int held = 4 * wg + wave;
+  for (int first = 0; first < npiece; first += kDecThreads) {
+   const int bend = min(npiece, first + kDecThreads);
+   if (first > 0) decode_prologue<D, G, PT>(p, b, h, T, ws, nc, first, bend - first, false, qs, s_red, pn_s, pbase_s);
+   while (held < bend) {
+    const int it = held - first;
     const int n = wave_uniform(pn_s[it]);
-    if (n == 0) continue;
+    unsigned grab = 0;
+    if (n == 0) {
+      if (lane == 0) grab = __hip_atomic_fetch_add(pctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      held = dyn0 + __builtin_amdgcn_readlane((int)grab, 0);
+      continue;
+    }
     // the piece's first token (scalar base), rows by 32-bit byte offsets
     const int64_t t0off = wave_uniform(pbase_s[it]);
     const char* kp = kbase + t0off * 2;
@@ -498,6 +511,7 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
       for (int i = 0; i < VC; ++i)
         vr[i] = reinterpret_cast<const uint4*>(vp + min(vrow0 + RPI * i, n - 1) * rsb)[vchunk];
     }
+    if (lane == 0) grab = __hip_atomic_fetch_add(pctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __builtin_amdgcn_sched_barrier(0);   // every load of the piece ahead of its arithmetic
 
     // ---- scores S[token][head] on the matrix cores
@@ -605,6 +619,7 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
       }
       wave_lds_sync();
     }
+    held = dyn0 + __builtin_amdgcn_readlane((int)grab, 0);
    }
   }
 
@@ -661,6 +676,8 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
     }
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
+  // every other workgroup of the unit has stopped asking for pieces
+  if (tid == 0) __hip_atomic_store(pctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   merge_partials<D, G>(p, unit, b, h);
 }
 
@@ -670,9 +687,15 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
   decode_task<D, G, F32>(p, blockIdx.z, blockIdx.y, blockIdx.x);
 }
 
+// One-dimensional grid of nwg * units workgroups: workgroup x of unit u sits at
+// index x * units + (u - x) mod units, so the workgroups of a unit are
+// dispatched in different rounds and, when units is a multiple of 8, to
+// different XCDs (consecutive indices go to consecutive XCDs).
 template <int D, int G>
 __global__ __launch_bounds__(kDecThreads, (G <= 4) ? 3 : (G <= 8 ? 2 : 1)) void decode_mfma_kernel(DecodeParams p) {
-  decode_mfma_task<D, G>(p, blockIdx.z, blockIdx.y, blockIdx.x);
+  const int x = blockIdx.x / p.units, up = blockIdx.x % p.units;
+  const int unit = (up + x) % p.units;
+  decode_mfma_task<D, G>(p, unit / p.hkv, unit % p.hkv, x);
 }
 
 // ------------------------------------------------------------- launchers --
@@ -716,7 +739,9 @@ hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int 
   const int nwg = std::max(1, (int)((items + spw - 1) / spw));
   p.nwg = nwg;
   p.spw = std::max(1, (items + nwg - 1) / nwg);
-  hipLaunchKernelGGL(k, dim3(nwg, p.hkv, batch), dim3(kDecThreads), 0, st, p);
+  p.units = (int)units;
+  if (f32) hipLaunchKernelGGL(k, dim3(nwg, p.hkv, batch), dim3(kDecThreads), 0, st, p);
+  else hipLaunchKernelGGL(k, dim3((unsigned)(nwg * units)), dim3(kDecThreads), 0, st, p);
   return hipGetLastError();
 }
 
