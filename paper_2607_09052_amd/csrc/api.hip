@@ -179,10 +179,17 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
   return hip_status(launch_select(p, v.d, v.G, v.B, st));
 }
 
+// `tail_rec` non-null (bf16 K/V only): the launch also refreshes the record of
+// each row's newest block in these summaries.
 cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
                          const int32_t* seq_lens, const int32_t* sel, float* out, float* lse,
-                         uint8_t* ws, hipStream_t st) {
+                         uint8_t* ws, hipStream_t st, void* tail_rec = nullptr) {
   DecodeParams p;
+  p.tail_rec = static_cast<uint8_t*>(tail_rec);
+  p.r = v.r;
+  p.mdt = v.mdt;
+  p.fdt = v.fdt;
+  p.lay = v.lay;
   p.q = q;
   p.kv = make_view(kv, v);
   p.seq_lens = seq_lens;
@@ -312,6 +319,13 @@ cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const c
   // the selection goes to the caller's buffer if given, else to the workspace
   int32_t* selp = sel ? sel : reinterpret_cast<int32_t*>(wsb + v.step_sel);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (v.w >= kL && !v.kv_f32 && v.r <= 4) {
+    // The block holding the newest token lies in the window: no candidate's
+    // record changes in this step, and the attention reads no record, so the
+    // refresh rides in the attention launch (extra workgroups, dispatched last).
+    if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st)) != COBS_OK) return s;
+    return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st, summaries);
+  }
   if ((s = run_build(v, kv, seq_lens, 0, 0, true, summaries, st)) != COBS_OK) return s;
   if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st)) != COBS_OK) return s;
   return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);

@@ -46,6 +46,11 @@ struct DecodeParams {
   int hkv, hq, tmax, s, w, nwg, spw;   // spw: work items (segments or pieces) per workgroup
   int units;        // B*Hkv
   float c;
+  // bf16 K/V: refresh of each row's newest block in the same launch (null: no
+  // refresh); the record geometry below is used only then
+  uint8_t* tail_rec;
+  int r, mdt, fdt;
+  RecLayout lay;
 };
 
 hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st);

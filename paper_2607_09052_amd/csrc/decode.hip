@@ -19,7 +19,7 @@
 // The four wave states are merged into one partial per workgroup; the last
 // workgroup of the unit to arrive merges the partials in workgroup order
 // (log-sum-exp) and writes out and lse.
-#include "cobs_kernels.h"
+#include "block_stats.h"
 
 namespace cobs {
 
@@ -117,10 +117,9 @@ __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, in
 // while the first KB partials' outputs load into registers in the same round
 // trip, and each thread forms the merge weights of its own heads.
 template <int D, int G>
-__device__ void merge_partials(const DecodeParams& p, int unit, int b, int h) {
+__device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, float (*mk)[G], float (*lk)[G]) {
   constexpr int OPT = (G * D + kDecThreads - 1) / kDecThreads;   // outputs per thread
   constexpr int KB = (OPT <= 4) ? 16 : 8;                        // partials per load batch
-  __shared__ float mk[kMaxDecodeWg][G], lk[kMaxDecodeWg][G];
   const int tid = threadIdx.x;
   const int nwg = p.nwg;
   const __amdgpu_buffer_rsrc_t up = coherent_view(p.part + (int64_t)unit * nwg * G * (D + 2), 4u * nwg * G * (D + 2));
@@ -359,7 +358,8 @@ __device__ __forceinline__ void decode_task(const DecodeParams& p, int b, int h,
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
 
-  merge_partials<D, G>(p, unit, b, h);
+  __shared__ float mk[kMaxDecodeWg][G], lk[kMaxDecodeWg][G];
+  merge_partials<D, G>(p, unit, b, h, mk, lk);
 }
 
 // ---------------------------------------------------------------------------
@@ -391,8 +391,24 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return __builtin
 // 16-byte chunk index with 2 g puts their reads on disjoint banks.
 __device__ __forceinline__ int vswz(int row) { return 2 * ((row >> 2) & 3); }
 
+// LDS of the bf16 decode workgroup, carved from the kernel's pool.
 template <int D, int G>
-__device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, int h, int wg) {
+struct DecodeLds {
+  static constexpr bool kMatPV = G >= 8;
+  static constexpr int PT = 32, GP = (G + 3) / 4 * 4;
+  alignas(16) float qs[G][D];
+  alignas(16) uint16_t vt[kMatPV ? 4 : 1][kMatPV ? PT * D : 1];   // V tiles, swizzled chunks
+  alignas(16) float ps[kMatPV ? 1 : 4][kMatPV ? 1 : PT][GP];      // P to the V layout
+  alignas(16) float wo[4][G][D];
+  float wm[4][G], wl[4][G];
+  float mk[kMaxDecodeWg][G], lk[kMaxDecodeWg][G];                 // merge statistics
+  int s_last, s_red[4];
+  int pn_s[kDecThreads];
+  int64_t pbase_s[kDecThreads];
+};
+
+template <int D, int G>
+__device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, int h, int wg, char* pool) {
   static_assert(G <= 16, "at most 16 query heads per KV head");
   constexpr int KST = D / 32;                 // k-steps of the score product
   constexpr int CPR = D / 8;                  // 16-byte chunks per row (bf16)
@@ -405,14 +421,17 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   // 16 head columns are mostly padding below that); fewer heads use the VALU
   constexpr bool kMatPV = G >= 8;
 
-  __shared__ __align__(16) float qs[G][D];
-  __shared__ __align__(16) uint16_t vt[kMatPV ? 4 : 1][kMatPV ? PT * D : 1];   // V tiles, swizzled chunks
-  __shared__ __align__(16) float ps[kMatPV ? 1 : 4][kMatPV ? 1 : PT][GP];      // P to the V layout
-  __shared__ float wm[4][G], wl[4][G];
-  __shared__ __align__(16) float wo[4][G][D];
-  __shared__ int s_last, s_red[4];
-  __shared__ int pn_s[kDecThreads];
-  __shared__ int64_t pbase_s[kDecThreads];
+  DecodeLds<D, G>& S = *reinterpret_cast<DecodeLds<D, G>*>(pool);
+  auto& qs = S.qs;
+  auto& vt = S.vt;
+  auto& ps = S.ps;
+  auto& wm = S.wm;
+  auto& wl = S.wl;
+  auto& wo = S.wo;
+  int& s_last = S.s_last;
+  int* s_red = S.s_red;
+  int* pn_s = S.pn_s;
+  int64_t* pbase_s = S.pbase_s;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int unit = b * p.hkv + h;
@@ -678,7 +697,27 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
   // every other workgroup of the unit has stopped asking for pieces
   if (tid == 0) __hip_atomic_store(pctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  merge_partials<D, G>(p, unit, b, h);
+  merge_partials<D, G>(p, unit, b, h, S.mk, S.lk);
+}
+
+// The newest block's refresh (block statistics of a bf16-key block with 16
+// power-iteration columns), run by the extra workgroups of the launch.
+template <int D>
+__device__ __forceinline__ void refresh_newest_block(const DecodeParams& p, int unit, char* pool) {
+  const int b = unit / p.hkv, h = unit % p.hkv;
+  const int T = clamp_len(p.seq_lens[b], p.tmax);
+  if (T <= 0) return;
+  const int j = (T - 1) / kL;
+  StatsArgs a;
+  a.kv = p.kv;
+  a.rec = p.tail_rec;
+  a.hkv = p.hkv;
+  a.nbmax = p.kv.nbmax;
+  a.r = p.r;
+  a.mdt = p.mdt;
+  a.fdt = p.fdt;
+  a.lay = p.lay;
+  block_stats<D, 16, false>(a, b, h, j, min(kL, T - j * kL), pool);
 }
 
 // Grid (workgroups per unit, Hkv, B).
@@ -687,15 +726,26 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
   decode_task<D, G, F32>(p, blockIdx.z, blockIdx.y, blockIdx.x);
 }
 
-// One-dimensional grid of nwg * units workgroups: workgroup x of unit u sits at
-// index x * units + (u - x) mod units, so the workgroups of a unit are
-// dispatched in different rounds and, when units is a multiple of 8, to
-// different XCDs (consecutive indices go to consecutive XCDs).
+template <size_t A, size_t B>
+constexpr size_t lds_max() { return A > B ? A : B; }
+
+// One-dimensional grid of nwg * units attention workgroups: workgroup x of
+// unit u sits at index x * units + (u - x) mod units, so the workgroups of a
+// unit are dispatched in different rounds and, when units is a multiple of 8,
+// to different XCDs (consecutive indices go to consecutive XCDs).  With a
+// fused refresh (tail_rec set), workgroups nwg * units + u, dispatched last,
+// refresh the record of unit u's newest block; the attention reads no record.
 template <int D, int G>
 __global__ __launch_bounds__(kDecThreads, (G <= 4) ? 3 : (G <= 8 ? 2 : 1)) void decode_mfma_kernel(DecodeParams p) {
+  __shared__ __align__(16) char pool[lds_max<sizeof(DecodeLds<D, G>), stats_lds_bytes<D, 16, false>()>()];
+  const int na = p.nwg * p.units;
+  if ((int)blockIdx.x >= na) {
+    refresh_newest_block<D>(p, blockIdx.x - na, pool);
+    return;
+  }
   const int x = blockIdx.x / p.units, up = blockIdx.x % p.units;
   const int unit = (up + x) % p.units;
-  decode_mfma_task<D, G>(p, unit / p.hkv, unit % p.hkv, x);
+  decode_mfma_task<D, G>(p, unit / p.hkv, unit % p.hkv, x, pool);
 }
 
 // ------------------------------------------------------------- launchers --
@@ -741,7 +791,7 @@ hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int 
   p.spw = std::max(1, (items + nwg - 1) / nwg);
   p.units = (int)units;
   if (f32) hipLaunchKernelGGL(k, dim3(nwg, p.hkv, batch), dim3(kDecThreads), 0, st, p);
-  else hipLaunchKernelGGL(k, dim3((unsigned)(nwg * units)), dim3(kDecThreads), 0, st, p);
+  else hipLaunchKernelGGL(k, dim3((unsigned)(nwg * units + (p.tail_rec ? units : 0))), dim3(kDecThreads), 0, st, p);
   return hipGetLastError();
 }
 

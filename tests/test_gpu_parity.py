@@ -389,11 +389,14 @@ def test_build_bf16_keys_and_storage_dtypes_consistent():
 
 # --------------------------------------------------------- decode step --
 
-def test_decode_step_is_build_select_decode():
-    prob = synth.make_problem("c3", seed=31, B=2, Hq=16, Hkv=4, T=3000, s=10, w=300)
+@pytest.mark.parametrize("w", [300, 40])
+def test_decode_step_is_build_select_decode(w):
+    """Window >= one block: the newest block's refresh runs beside selection and
+    decode; a shorter window makes it a candidate, refreshed before selection."""
+    prob = synth.make_problem("c3", seed=31, B=2, Hq=16, Hkv=4, T=3000, s=10, w=w)
     cfg_d = prob["cfg"]
     cfg = cobs.Config(batch=2, num_q_heads=16, num_kv_heads=4, head_dim=128, max_seq_len=3008, rank=4,
-                      budget=10, window=300)
+                      budget=10, window=w)
     assert cfg_d["T_max"] == 3008
     k, v, q = prob["k"].to(DEV), prob["v"].to(DEV), prob["q"].to(DEV)
     seq = torch.tensor([3000, 2049], dtype=torch.int32, device=DEV)
