@@ -43,14 +43,9 @@
  *     arrival counters zero again on completion, so the same workspace can be
  *     reused by later calls on the same stream.  Calls that share a workspace
  *     must not overlap in time (different streams race).
- *   - Records, scores and selections are deterministic: identical inputs give
- *     bitwise identical outputs (no floating-point atomics; fixed reduction
- *     orders).  The attention output and lse for bf16 K/V are reproducible to
- *     fp32 rounding: the work items of a (batch row, KV head) beyond each
- *     workgroup's first four are handed out on demand, so which workgroup
- *     sums which tokens, and with it the rounding of the partial sums, can
- *     change from call to call.  fp32 K/V are split statically (bitwise
- *     reproducible).
+ *   - Results are deterministic: identical inputs give bitwise identical
+ *     outputs (no floating-point atomics; work is split statically and
+ *     reduced in a fixed order).
  */
 #ifndef COBS_H
 #define COBS_H

@@ -51,7 +51,7 @@ struct Derived {
   int nch_max;          // selector: workgroups (chunks) per unit, upper bound
   int nwg_max;          // decode: workgroups (partials) per unit, upper bound
   size_t sel_ell, sel_part, sel_cnt, sel_bytes;
-  size_t dec_part, dec_cnt, dec_pcnt, dec_bytes;
+  size_t dec_part, dec_cnt, dec_bytes;
   size_t step_sel, step_bytes;   // decode step: select region, decode region, selection
 };
 
@@ -86,7 +86,6 @@ Derived derive(const cobs_config_t* c) {
   off = 0;
   v.dec_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nwg_max * v.G * (v.d + 2), kAlign);
   v.dec_cnt = off;  off = round_up(off + sizeof(unsigned) * (size_t)v.units, kAlign);
-  v.dec_pcnt = off; off = round_up(off + sizeof(unsigned) * kPieceCounterStride * (size_t)v.units, kAlign);
   v.dec_bytes = off;
   v.step_sel = v.sel_bytes + v.dec_bytes;
   v.step_bytes = round_up(v.step_sel + sizeof(int32_t) * (size_t)v.units * v.s, kAlign);
@@ -198,7 +197,6 @@ cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
   p.lse = lse;
   p.part = reinterpret_cast<float*>(ws + v.dec_part);
   p.cnt = reinterpret_cast<unsigned*>(ws + v.dec_cnt);
-  p.pcnt = reinterpret_cast<unsigned*>(ws + v.dec_pcnt);
   p.units = v.units;
   p.hkv = v.hkv;
   p.hq = v.hq;

@@ -29,10 +29,6 @@ struct SelectParams {
   RecLayout lay;
 };
 
-// Piece counters of different units sit 256 bytes apart: atomics on one
-// memory line are serialised, and every wave of a unit asks for its next piece.
-constexpr int kPieceCounterStride = 64;
-
 struct DecodeParams {
   const float* q;
   KvView kv;
@@ -42,7 +38,6 @@ struct DecodeParams {
   float* lse;
   float* part;      // [B*Hkv][nwg][G][D + 2]
   unsigned* cnt;    // [B*Hkv] arrival counters
-  unsigned* pcnt;   // [B*Hkv][kPieceCounterStride] piece counters (bf16 K/V: pieces handed out on demand)
   int hkv, hq, tmax, s, w, nwg, spw;   // spw: work items (segments or pieces) per workgroup
   int units;        // B*Hkv
   float c;

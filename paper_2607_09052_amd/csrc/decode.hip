@@ -440,9 +440,11 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   const int nc = (ws + kL - 1) / kL;
   const int nwin = (T > ws) ? ((T - 1) / kL - ws / kL + 1) : 0;
   const int npiece = 2 * (p.s + nwin);
+  const int pc_lo = wg * p.spw, pc_end = min(npiece, pc_lo + p.spw);
   const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;        // elements between consecutive tokens
 
-  decode_prologue<D, G, PT>(p, b, h, T, ws, nc, 0, min(kDecThreads, npiece), true, qs, s_red, pn_s, pbase_s);
+  decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pc_lo, max(0, min(kDecThreads, pc_end - pc_lo)), true,
+                            qs, s_red, pn_s, pbase_s);
 
   // B operands: query head l % 16 (zero beyond G), columns 32*kk + 8*(l/16) + j
   const int hcol = lane & 15, lgrp = lane >> 4;
@@ -476,27 +478,12 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.0f;
 
-  // Pieces are handed out on demand, which evens out workgroups that stream at
-  // different rates: wave w of workgroup wg starts with piece 4 wg + w, and
-  // every later piece comes from the unit's counter (past the 4 nwg starting
-  // pieces), requested while the current piece's loads are in flight.  The
-  // pieces are described in tables of kDecThreads; a wave holding a piece of a
-  // later table waits for it at that table's barriers.
-  unsigned* pctr = p.pcnt + (int64_t)unit * kPieceCounterStride;
-  const int dyn0 = 4 * p.nwg;
-  int held = 4 * wg + wave;
-  for (int first = 0; first < npiece; first += kDecThreads) {
-   const int bend = min(npiece, first + kDecThreads);
-   if (first > 0) decode_prologue<D, G, PT>(p, b, h, T, ws, nc, first, bend - first, false, qs, s_red, pn_s, pbase_s);
-   while (held < bend) {
-    const int it = held - first;
+  for (int pb = pc_lo; pb < pc_end; pb += kDecThreads) {
+   const int cnt = min(kDecThreads, pc_end - pb);
+   if (pb != pc_lo) decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pb, cnt, false, qs, s_red, pn_s, pbase_s);
+   for (int it = wave; it < cnt; it += 4) {
     const int n = wave_uniform(pn_s[it]);
-    unsigned grab = 0;
-    if (n == 0) {
-      if (lane == 0) grab = __hip_atomic_fetch_add(pctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      held = dyn0 + __builtin_amdgcn_readlane((int)grab, 0);
-      continue;
-    }
+    if (n == 0) continue;
     // the piece's first token (scalar base), rows by 32-bit byte offsets
     const int64_t t0off = wave_uniform(pbase_s[it]);
     const char* kp = kbase + t0off * 2;
@@ -530,7 +517,6 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
       for (int i = 0; i < VC; ++i)
         vr[i] = reinterpret_cast<const uint4*>(vp + min(vrow0 + RPI * i, n - 1) * rsb)[vchunk];
     }
-    if (lane == 0) grab = __hip_atomic_fetch_add(pctr, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __builtin_amdgcn_sched_barrier(0);   // every load of the piece ahead of its arithmetic
 
     // ---- scores S[token][head] on the matrix cores
@@ -638,7 +624,6 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
       }
       wave_lds_sync();
     }
-    held = dyn0 + __builtin_amdgcn_readlane((int)grab, 0);
    }
   }
 
@@ -695,8 +680,6 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
     }
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
-  // every other workgroup of the unit has stopped asking for pieces
-  if (tid == 0) __hip_atomic_store(pctr, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   merge_partials<D, G>(p, unit, b, h, S.mk, S.lk);
 }
 
