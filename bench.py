@@ -122,6 +122,26 @@ def measured_traffic(path, workload, kernel):
     return hit if (hit is not None and src == kernel_source_hash()) else None
 
 
+def prefill_summary(cfg, B, T, ms):
+    """Block-statistics build of a whole cache of T tokens: time, bytes and flops.
+
+    Flops are those of the method as built here, per full block: the centred
+    Gram matrix (2 L^2 d), the subspace iteration on it (kPowerIters + 1
+    products Gamma W of 2 L^2 P flops, and per re-orthonormalisation Y^T Y and
+    Y X^T, 2 L P^2 each), the Rayleigh-Ritz product (2 L P^2) and the factors
+    xi = Kc^T w (2 L d r); P = 16 columns for r <= 4, 32 beyond.
+    """
+    L, d, r = 64, cfg.head_dim, cfg.rank
+    P = 16 if r <= 4 else 32
+    iters = 16
+    full = B * cfg.num_kv_heads * (T // L)
+    blocks = B * cfg.num_kv_heads * (-(-T // L))
+    per_block = 2 * L * L * d + (iters + 1) * 2 * L * L * P + iters * 4 * L * P * P + 2 * L * P * P + 2 * L * d * r
+    kbytes = B * cfg.num_kv_heads * T * d * ESZ[cfg.kv_dtype] + blocks * cobs.record_bytes(cfg)
+    return {"us": round(ms * 1e3, 1), "blocks": blocks, "full_blocks": full,
+            "gflops": round(full * per_block / (ms * 1e-3) / 1e9, 1), "gbps": round(kbytes / (ms * 1e-3) / 1e9, 1)}
+
+
 def replay_time(graph, reps, stream):
     """Microseconds per replay of `graph`, HIP events on `stream`."""
     start = torch.cuda.Event(enable_timing=True)
@@ -304,6 +324,18 @@ def main():
     g_fill = capture(sweep_fill, stream)
     g_fill.replay()
     fill_us = replay_time(g_fill, max(2, reps // 4), stream) / copies
+    # prefill: statistics of every block of the cache (one layer copy), eager launches
+    r_pre = torch.empty_like(rec)
+    pre_ms = []
+    for it in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        cobs.cobs_build_block_stats(cfg, prob["k"], prob["v"], seq_hi, r_pre, stream=stream)
+        e1.record(stream)
+        e1.synchronize()
+        if it > 0:
+            pre_ms.append(e0.elapsed_time(e1))
+    del r_pre
     torch.cuda.set_stream(torch.cuda.default_stream())
 
     kbytes = {"select_kernel": ab["select"], "decode_kernel": ab["decode"], "build_stats_kernel": ab["tail"]}
@@ -336,6 +368,7 @@ def main():
             "kernels_us": {k_: round(v_, 3) for k_, v_ in kern_us.items()},
             "fill_step_us": round(fill_us, 3),
             "fill_step_bytes": ab_fill["step"],
+            "prefill_build": prefill_summary(cfg, B, T_hi, float(np.median(pre_ms))),
         },
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": round(dom_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(dom_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,

@@ -207,24 +207,28 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   }
   __syncthreads();
   {
-    // ---- Gram matrix Gamma = Kc Kc^T / n, 4x4 tile per thread
+    // ---- Gram matrix Gamma = Kc Kc^T / n on the fp32 matrix cores
+    // (v_mfma_f32_16x16x4_f32: lane l holds A[l%16][l/16] and B[l/16][l%16]
+    // and gets D[4(l/16)+v][l%16]): wave w forms rows [16w, 16w+16) as four
+    // 16 x 16 tiles, contracting over the d key elements four at a time
     {
-      const int i0 = 4 * (tid / 16), j0 = 4 * (tid % 16);
-      float acc[4][4] = {};
-      for (int e = 0; e < D; ++e) {
-        float av[4], cv[4];
+      const int lane = tid & 63, wave = tid >> 6, lr = lane & 15, lk = lane >> 4;
+      f32x4_t acc[kL / 16];
 #pragma unroll
-        for (int x = 0; x < 4; ++x) { av[x] = kc(e, i0 + x); cv[x] = kc(e, j0 + x); }
+      for (int ct = 0; ct < kL / 16; ++ct) acc[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 4
+      for (int e0 = 0; e0 < D; e0 += 4) {
+        const int e = e0 + lk;
+        const float a = kc(e, 16 * wave + lr);
 #pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-          for (int y = 0; y < 4; ++y) acc[x][y] += av[x] * cv[y];
+        for (int ct = 0; ct < kL / 16; ++ct)
+          acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, kc(e, 16 * ct + lr), acc[ct], 0, 0, 0);
       }
       const float inv_n = 1.0f / (float)n;
 #pragma unroll
-      for (int x = 0; x < 4; ++x)
+      for (int ct = 0; ct < kL / 16; ++ct)
 #pragma unroll
-        for (int y = 0; y < 4; ++y) Gm[(i0 + x) * kL + j0 + y] = acc[x][y] * inv_n;
+        for (int v = 0; v < 4; ++v) Gm[(16 * wave + 4 * lk + v) * kL + 16 * ct + lr] = acc[ct][v] * inv_n;
     }
     for (int idx = tid; idx < kL * P; idx += kBuildThreads) Wm[idx] = init_sign(idx / P, idx % P);
     __syncthreads();
