@@ -37,7 +37,7 @@ def round_bf16(x):
 
     Written from the definition: x = m * 2**e with 0.5 <= |m| < 1, keep
     round_half_even(m * 2**8) / 2**8.  Inputs are assumed to lie in the normal
-    bf16 range (true for every descriptor value this build stores).
+    bf16 range (true for every descriptor value the library stores).
     """
     x = np.asarray(x, dtype=np.float64)
     m, e = np.frexp(x)
