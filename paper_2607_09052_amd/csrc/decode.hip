@@ -119,15 +119,17 @@ __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, in
 template <int D, int G>
 __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, float (*mk)[G], float (*lk)[G]) {
   constexpr int OPT = (G * D + kDecThreads - 1) / kDecThreads;   // outputs per thread
-  constexpr int KB = (OPT <= 4) ? 16 : 8;                        // partials per load batch
+  constexpr int KB = (OPT <= 2) ? 32 : ((OPT <= 4) ? 16 : 8);     // partials per load batch (64 registers)
   const int tid = threadIdx.x;
   const int nwg = p.nwg;
   const __amdgpu_buffer_rsrc_t up = coherent_view(p.part + (int64_t)unit * nwg * G * (D + 2), 4u * nwg * G * (D + 2));
   float ov[KB][OPT];
+  // partials past the last one fall outside the view: those loads return 0
+  // without touching memory, and their values are not used
   auto load_batch = [&](int k0) {
 #pragma unroll
     for (int k = 0; k < KB; ++k) {
-      const int kc = min(k0 + k, nwg - 1);
+      const int kc = k0 + k;
 #pragma unroll
       for (int j = 0; j < OPT; ++j) {
         const int idx = min(tid + kDecThreads * j, G * D - 1);
