@@ -2,6 +2,8 @@
 // the selected blocks (tokens before the window start) and the last w tokens,
 // each token once, one softmax per query head.
 //
+// fp32 K/V (below; the bf16 kernel further down has its own notes).
+//
 // Work unit: a segment of at most L = 64 contiguous tokens: either the part of a
 // selected block before the window start, or the part of a block inside the
 // window.  Grid (wg, Hkv, B), 256 threads = 4 waves; workgroup wg owns segments
