@@ -317,7 +317,7 @@ cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const c
   // the selection goes to the caller's buffer if given, else to the workspace
   int32_t* selp = sel ? sel : reinterpret_cast<int32_t*>(wsb + v.step_sel);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (v.w >= kL && !v.kv_f32 && v.r <= 4) {
+  if (v.w >= kL && v.r <= 4 && decode_hosts_refresh(v.G, v.kv_f32 != 0)) {
     // The block holding the newest token lies in the window: no candidate's
     // record changes in this step, and the attention reads no record, so the
     // refresh rides in the attention launch (extra workgroups, dispatched last).

@@ -43,24 +43,27 @@ __device__ __forceinline__ float init_sign(int i, int p) {
 }
 
 // Encode one vector of `dim` fp32 values held in LDS (`x`) into `dst` with the
-// given storage dtype.  For E2M1 the scale is written to *scale_dst.  Executed
-// by the `nthr` threads whose local index is `lt`; `red` is LDS scratch of nthr floats.
+// given storage dtype.  For E2M1 the scale is written to *scale_dst.  The
+// `nthr` (a power of two) threads with local index lt < nthr do the work; every
+// thread of the workgroup calls it (it holds barriers), those with lt >= nthr
+// only take part in the barriers.  `red` is LDS scratch of nthr floats.
 __device__ void store_vector(const float* x, int dim, int dt, uint8_t* dst, float* scale_dst,
                              int lt, int nthr, float* red) {
+  const bool act = lt < nthr;
   if (dt == DT_F32) {
-    for (int e = lt; e < dim; e += nthr) reinterpret_cast<float*>(dst)[e] = x[e];
+    for (int e = lt; act && e < dim; e += nthr) reinterpret_cast<float*>(dst)[e] = x[e];
     return;
   }
   if (dt == DT_BF16) {
-    for (int e = lt; e < dim / 2; e += nthr) {
+    for (int e = lt; act && e < dim / 2; e += nthr) {
       uint32_t lo = f32_to_bf16_rne(x[2 * e]), hi = f32_to_bf16_rne(x[2 * e + 1]);
       reinterpret_cast<uint32_t*>(dst)[e] = lo | (hi << 16);
     }
     return;
   }
   float m = 0.0f;
-  for (int e = lt; e < dim; e += nthr) m = fmaxf(m, fabsf(x[e]));
-  red[lt] = m;
+  for (int e = lt; act && e < dim; e += nthr) m = fmaxf(m, fabsf(x[e]));
+  if (act) red[lt] = m;
   __syncthreads();
   for (int o = nthr / 2; o > 0; o >>= 1) {
     if (lt < o) red[lt] = fmaxf(red[lt], red[lt + o]);
@@ -70,7 +73,7 @@ __device__ void store_vector(const float* x, int dim, int dt, uint8_t* dst, floa
   __syncthreads();
   float scale = absmax / 6.0f;
   if (lt == 0) *scale_dst = scale;
-  for (int e = lt; e < dim / 8; e += nthr) {
+  for (int e = lt; act && e < dim / 8; e += nthr) {
     uint32_t w = 0;
     if (scale > 0.0f) {
 #pragma unroll
@@ -108,8 +111,11 @@ struct StatsLds {
 template <int D, int P, bool KF32>
 constexpr size_t stats_lds_bytes() { return StatsLds<D, P, KF32>::bytes; }
 
-template <int D, int P, bool KF32>
+// Run by a workgroup of NT >= kBuildThreads threads; the work is laid out on
+// the first kBuildThreads (four waves), every thread takes part in the barriers.
+template <int D, int P, bool KF32, int NT = kBuildThreads>
 __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, int j, int n, char* pool) {
+  static_assert(NT % 64 == 0 && NT >= kBuildThreads, "whole waves, at least four");
   using Lay = StatsLds<D, P, KF32>;
   constexpr int KS = Lay::KS;
   typedef typename std::conditional<KF32, float, uint16_t>::type kt_t;
@@ -136,6 +142,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   };
 
   const int tid = threadIdx.x;
+  const bool lw = tid < kBuildThreads;             // a thread of the work layout
   const int r = p.r;
   // ---- load the block's keys into registers: RPP rows per pass, 8 elements per thread
   constexpr int TPR = D / 8;                       // threads per row
@@ -151,7 +158,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     const int i = r0 + ps * RPP;
 #pragma unroll
     for (int q = 0; q < 8; ++q) v[ps][q] = 0.0f;
-    const int64_t off = (i < n) ? kv_offset(p.kv, b, h, j * kL + i) : -1;
+    const int64_t off = (lw && i < n) ? kv_offset(p.kv, b, h, j * kL + i) : -1;
     if (off >= 0) {
       if constexpr (KF32) {
         const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(p.kv.k) + off + e0);
@@ -173,8 +180,10 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
 #pragma unroll
     for (int q = 0; q < 8; ++q) cs[q] += (double)v[ps][q];
   double* red64 = reinterpret_cast<double*>(Gm);   // RPP x D doubles, free until the Gram
+  if (lw) {
 #pragma unroll
-  for (int q = 0; q < 8; ++q) red64[r0 * D + e0 + q] = cs[q];
+    for (int q = 0; q < 8; ++q) red64[r0 * D + e0 + q] = cs[q];
+  }
   __syncthreads();
   if (tid < D) {
     double sum = 0.0;
@@ -187,17 +196,17 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   const RecLayout lay = p.lay;
   if (!factors) {
     // partial block (or r = 0): count, mean, zero factors
-    for (int idx = tid; idx < lay.mean_off / 4; idx += kBuildThreads)
+    for (int idx = tid; idx < lay.mean_off / 4; idx += NT)
       reinterpret_cast<uint32_t*>(R)[idx] = (idx == 0) ? (uint32_t)n : 0u;
     __syncthreads();
     store_vector(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), tid, kBuildThreads, red);
-    for (int idx = lay.fac_off / 4 + tid; idx < lay.total / 4; idx += kBuildThreads)
+    for (int idx = lay.fac_off / 4 + tid; idx < lay.total / 4; idx += NT)
       reinterpret_cast<uint32_t*>(R)[idx] = 0u;
     return;
   }
   // stage the keys transposed in their stored type: KT[e][i] = k_{jL+i}[e]
 #pragma unroll
-  for (int ps = 0; ps < NPASS; ++ps) {
+  for (int ps = 0; ps < NPASS && lw; ++ps) {
     const int i = r0 + ps * RPP;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
@@ -211,7 +220,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     // (v_mfma_f32_16x16x4_f32: lane l holds A[l%16][l/16] and B[l/16][l%16]
     // and gets D[4(l/16)+v][l%16]): wave w forms rows [16w, 16w+16) as four
     // 16 x 16 tiles, contracting over the d key elements four at a time
-    {
+    if (lw) {
       const int lane = tid & 63, wave = tid >> 6, lr = lane & 15, lk = lane >> 4;
       f32x4_t acc[kL / 16];
 #pragma unroll
@@ -230,7 +239,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
 #pragma unroll
         for (int v = 0; v < 4; ++v) Gm[(16 * wave + 4 * lk + v) * kL + 16 * ct + lr] = acc[ct][v] * inv_n;
     }
-    for (int idx = tid; idx < kL * P; idx += kBuildThreads) Wm[idx] = init_sign(idx / P, idx % P);
+    for (int idx = tid; idx < kL * P; idx += NT) Wm[idx] = init_sign(idx / P, idx % P);
     __syncthreads();
 
     // Matrix products of the iteration on the fp32 matrix cores
@@ -241,7 +250,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     const int lr = lane & 15, lk = lane >> 4;
     for (int it = 0; it <= kPowerIters; ++it) {
       // ---- Y = Gamma W (Gamma symmetric: read by column, conflict free)
-      {
+      if (lw) {
         f32x4_t acc[P / 16];
 #pragma unroll
         for (int ct = 0; ct < P / 16; ++ct) acc[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
@@ -260,8 +269,8 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       __syncthreads();
       if (it == kPowerIters) break;      // last product feeds the Rayleigh-Ritz step
 
-      // ---- S = Y^T Y, 16 x 16 tiles spread over the waves
-      for (int tl = wave; tl < (P / 16) * (P / 16); tl += 4) {
+      // ---- S = Y^T Y, 16 x 16 tiles spread over the four waves
+      for (int tl = wave; lw && tl < (P / 16) * (P / 16); tl += kBuildThreads / 64) {
         const int ta = tl / (P / 16), tc = tl % (P / 16);
         f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll 4
@@ -317,7 +326,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       }
       __syncthreads();
       // ---- W = Y X^T: operand B[k][c] = X[c][k], which Lm holds at [k][c]
-      {
+      if (lw) {
         f32x4_t acc[P / 16];
 #pragma unroll
         for (int ct = 0; ct < P / 16; ++ct) acc[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
@@ -337,7 +346,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     }
 
     // ---- Rayleigh-Ritz: H = W^T Gamma W (symmetrised), eigenpairs by Jacobi
-    for (int idx = tid; idx < P * P; idx += kBuildThreads) {
+    for (int idx = tid; idx < P * P; idx += NT) {
       const int a = idx / P, c = idx % P;
       float s1 = 0.0f, s2 = 0.0f;
       for (int i = 0; i < kL; ++i) {
@@ -375,7 +384,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
         const float* V = Vm[cur];
         float* H2 = Hm[cur ^ 1];
         float* V2 = Vm[cur ^ 1];
-        for (int idx = tid; idx < P * P; idx += kBuildThreads) {
+        for (int idx = tid; idx < P * P; idx += NT) {
           const int a = idx / P, c = idx % P;
           const int pa = partner[a], pc = partner[c];
           const float sa = cself[a], ta = cpart[a], sc = cself[c], tc = cpart[c];
@@ -399,7 +408,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     }
     __syncthreads();
     // Ritz vectors w_i = W V[:, order_i] (into Ym), xi_i = Kc^T w_i / sqrt(n)
-    for (int idx = tid; idx < r * kL; idx += kBuildThreads) {
+    for (int idx = tid; idx < r * kL; idx += NT) {
       const int i = idx / kL, row = idx % kL;
       const int col = order[i];
       float s = 0.0f;
@@ -409,7 +418,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     __syncthreads();
     const float rs = 1.0f / sqrtf((float)n);
     const float top = ritzval[0];
-    for (int idx = tid; idx < r * D; idx += kBuildThreads) {
+    for (int idx = tid; idx < r * D; idx += NT) {
       const int i = idx / D, e = idx % D;
       float s = 0.0f;
       if (ritzval[i] > 1e-6f * top && top > 0.0f) {
@@ -446,7 +455,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   }
 
   // ---- write the record
-  for (int idx = tid; idx < lay.mean_off / 4; idx += kBuildThreads) {
+  for (int idx = tid; idx < lay.mean_off / 4; idx += NT) {
     uint32_t v = 0;
     if (idx == 0) v = (uint32_t)n;
     reinterpret_cast<uint32_t*>(R)[idx] = v;       // header, factor scales default 0
@@ -462,7 +471,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   }
   // zero the tail padding of the record
   const int used = lay.fac_off + r * lay.vec_bytes;
-  for (int idx = used / 4 + tid; idx < lay.total / 4; idx += kBuildThreads)
+  for (int idx = used / 4 + tid; idx < lay.total / 4; idx += NT)
     reinterpret_cast<uint32_t*>(R)[idx] = 0u;
 }
 

@@ -58,6 +58,7 @@ hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st
 bool select_on_matrix_cores(int mdt, int fdt);
 int select_min_bpw(int mdt, int fdt);
 hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int nbmax, hipStream_t st);
+bool decode_hosts_refresh(int g, bool f32);
 int decode_max_wg(int s, int w, int nbmax, bool f32);
 
 // Resident workgroups of `threads` threads per CU for a kernel, and the CU

@@ -77,10 +77,10 @@ __device__ __forceinline__ void item_range(const DecodeParams& p, int selv, int 
 
 // Prologue shared by the decode kernels: the queries (scaled by c) into LDS
 // when `load_q`, the valid selection prefix (its longest strictly ascending run
-// of candidate ids) and the table of the `cnt` <= kDecThreads work items from
-// `first` on.  The selection, query and validity loads are issued together
-// before the first barrier; the table is complete at the second.
-template <int D, int G, int PT>
+// of candidate ids) and the table of the `cnt` <= NT work items from `first`
+// on (NT threads per workgroup).  The selection, query and validity loads are
+// issued together before the first barrier; the table is complete at the second.
+template <int D, int G, int PT, int NT = kDecThreads>
 __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, int h, int T, int ws, int nc,
                                                 int first, int cnt, bool load_q, float (*qs)[D], int* red,
                                                 int* pn_s, int64_t* pbase_s) {
@@ -91,18 +91,20 @@ __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, in
   const int seg = it / (kL / PT);
   const int selv = (p.s > 0) ? sl[(tid < cnt && seg < p.s) ? seg : 0] : 0;
   int kv = p.s;                 // first entry breaking the ascending run of candidates
-  for (int i = tid; i < p.s; i += kDecThreads) {
+  for (int i = tid; i < p.s; i += NT) {
     const int bi = sl[i], prev = sl[i > 0 ? i - 1 : 0];
     if (bi < 0 || bi >= nc || (i > 0 && bi <= prev)) kv = min(kv, i);
   }
   if (load_q)
-    for (int idx = tid; idx < G * D; idx += kDecThreads)
+    for (int idx = tid; idx < G * D; idx += NT)
       qs[idx / D][idx % D] = p.q[((int64_t)b * p.hq + h * G) * D + idx] * p.c;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) kv = min(kv, __shfl_xor(kv, o, 64));
   if (lane == 0) red[wave] = kv;
   __syncthreads();
-  const int kvalid = min(min(red[0], red[1]), min(red[2], red[3]));
+  int kvalid = red[0];
+#pragma unroll
+  for (int w = 1; w < NT / 64; ++w) kvalid = min(kvalid, red[w]);
   if (tid < cnt) {
     int n;
     int64_t base;
@@ -118,9 +120,9 @@ __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, in
 // lse.  Thread t owns outputs t + 256 j; the partials' statistics go to LDS
 // while the first KB partials' outputs load into registers in the same round
 // trip, and each thread forms the merge weights of its own heads.
-template <int D, int G>
+template <int D, int G, int NT = kDecThreads>
 __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, float (*mk)[G], float (*lk)[G]) {
-  constexpr int OPT = (G * D + kDecThreads - 1) / kDecThreads;   // outputs per thread
+  constexpr int OPT = (G * D + NT - 1) / NT;                     // outputs per thread
   constexpr int KB = (OPT <= 2) ? 32 : ((OPT <= 4) ? 16 : 8);     // partials per load batch (64 registers)
   const int tid = threadIdx.x;
   const int nwg = p.nwg;
@@ -134,13 +136,13 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, fl
       const int kc = k0 + k;
 #pragma unroll
       for (int j = 0; j < OPT; ++j) {
-        const int idx = min(tid + kDecThreads * j, G * D - 1);
+        const int idx = min(tid + NT * j, G * D - 1);
         ov[k][j] = ld_coherent1(up, 4u * ((kc * G + idx / D) * (D + 2) + 2 + idx % D));
       }
     }
   };
   load_batch(0);
-  for (int idx = tid; idx < nwg * G; idx += kDecThreads) {
+  for (int idx = tid; idx < nwg * G; idx += NT) {
     const int k = idx / G, g = idx % G;
     const float2 ml = ld_coherent2(up, 4u * ((k * G + g) * (D + 2)));
     mk[k][g] = ml.x;
@@ -150,7 +152,7 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, fl
   float M[OPT], L[OPT], acc[OPT];
 #pragma unroll
   for (int j = 0; j < OPT; ++j) {
-    const int g = min(tid + kDecThreads * j, G * D - 1) / D;
+    const int g = min(tid + NT * j, G * D - 1) / D;
     float mx = -INFINITY;
     for (int k = 0; k < nwg; ++k) mx = fmaxf(mx, mk[k][g]);
     M[j] = mx;
@@ -164,7 +166,7 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, fl
       if (k0 + k < nwg) {
 #pragma unroll
         for (int j = 0; j < OPT; ++j) {
-          const int g = min(tid + kDecThreads * j, G * D - 1) / D;
+          const int g = min(tid + NT * j, G * D - 1) / D;
           const float mkg = mk[k0 + k][g];
           const float f = (M[j] == -INFINITY || mkg == -INFINITY) ? 0.0f : __expf(mkg - M[j]);
           L[j] += f * lk[k0 + k][g];
@@ -175,7 +177,7 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, fl
   }
 #pragma unroll
   for (int j = 0; j < OPT; ++j) {
-    const int idx = tid + kDecThreads * j;
+    const int idx = tid + NT * j;
     if (idx < G * D) {
       const int g = idx / D, dd = idx % D;
       const int64_t oq = (int64_t)b * p.hq + h * G + g;
@@ -396,23 +398,29 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return __builtin
 __device__ __forceinline__ int vswz(int row) { return 2 * ((row >> 2) & 3); }
 
 // LDS of the bf16 decode workgroup, carved from the kernel's pool.
-template <int D, int G>
+template <int D, int G, int NT>
 struct DecodeLds {
   static constexpr bool kMatPV = G >= 8;
-  static constexpr int PT = 32, GP = (G + 3) / 4 * 4;
+  static constexpr int PT = 32, GP = (G + 3) / 4 * 4, NW = NT / 64;
   alignas(16) float qs[G][D];
-  alignas(16) uint16_t vt[kMatPV ? 4 : 1][kMatPV ? PT * D : 1];   // V tiles, swizzled chunks
-  alignas(16) float ps[kMatPV ? 1 : 4][kMatPV ? 1 : PT][GP];      // P to the V layout
-  alignas(16) float wo[4][G][D];
-  float wm[4][G], wl[4][G];
+  alignas(16) uint16_t vt[kMatPV ? NW : 1][kMatPV ? PT * D : 1];  // V tiles, swizzled chunks
+  alignas(16) float ps[kMatPV ? 1 : NW][kMatPV ? 1 : PT][GP];     // P to the V layout
+  alignas(16) float wo[NW][G][D];
+  float wm[NW][G], wl[NW][G];
   float mk[kMaxDecodeWg][G], lk[kMaxDecodeWg][G];                 // merge statistics
-  int s_last, s_red[4];
-  int pn_s[kDecThreads];
-  int64_t pbase_s[kDecThreads];
+  int s_last, s_red[NW];
+  int pn_s[NT];
+  int64_t pbase_s[NT];
 };
 
-template <int D, int G>
+// Threads per bf16 decode workgroup: as many waves as one CU keeps resident
+// (the workgroup is alone on its CU), by the register budget of G.
+template <int G>
+constexpr int decode_threads() { return G <= 4 ? 768 : (G <= 8 ? 512 : 256); }
+
+template <int D, int G, int NT>
 __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, int h, int wg, char* pool) {
+  constexpr int NW = NT / 64;                 // waves
   static_assert(G <= 16, "at most 16 query heads per KV head");
   constexpr int KST = D / 32;                 // k-steps of the score product
   constexpr int CPR = D / 8;                  // 16-byte chunks per row (bf16)
@@ -425,7 +433,7 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   // 16 head columns are mostly padding below that); fewer heads use the VALU
   constexpr bool kMatPV = G >= 8;
 
-  DecodeLds<D, G>& S = *reinterpret_cast<DecodeLds<D, G>*>(pool);
+  DecodeLds<D, G, NT>& S = *reinterpret_cast<DecodeLds<D, G, NT>*>(pool);
   auto& qs = S.qs;
   auto& vt = S.vt;
   auto& ps = S.ps;
@@ -447,8 +455,8 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   const int pc_lo = wg * p.spw, pc_end = min(npiece, pc_lo + p.spw);
   const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;        // elements between consecutive tokens
 
-  decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pc_lo, max(0, min(kDecThreads, pc_end - pc_lo)), true,
-                            qs, s_red, pn_s, pbase_s);
+  decode_prologue<D, G, PT, NT>(p, b, h, T, ws, nc, pc_lo, max(0, min(NT, pc_end - pc_lo)), true,
+                                qs, s_red, pn_s, pbase_s);
 
   // B operands: query head l % 16 (zero beyond G), columns 32*kk + 8*(l/16) + j
   const int hcol = lane & 15, lgrp = lane >> 4;
@@ -482,10 +490,10 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[g][e] = 0.0f;
 
-  for (int pb = pc_lo; pb < pc_end; pb += kDecThreads) {
-   const int cnt = min(kDecThreads, pc_end - pb);
-   if (pb != pc_lo) decode_prologue<D, G, PT>(p, b, h, T, ws, nc, pb, cnt, false, qs, s_red, pn_s, pbase_s);
-   for (int it = wave; it < cnt; it += 4) {
+  for (int pb = pc_lo; pb < pc_end; pb += NT) {
+   const int cnt = min(NT, pc_end - pb);
+   if (pb != pc_lo) decode_prologue<D, G, PT, NT>(p, b, h, T, ws, nc, pb, cnt, false, qs, s_red, pn_s, pbase_s);
+   for (int it = wave; it < cnt; it += NW) {
     const int n = wave_uniform(pn_s[it]);
     if (n == 0) continue;
     // the piece's first token (scalar base), rows by 32-bit byte offsets
@@ -663,15 +671,15 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   }
   __syncthreads();
   float* wpart = p.part + ((int64_t)unit * p.nwg + wg) * G * (D + 2);
-  for (int idx = tid; idx < G * D; idx += kDecThreads) {
+  for (int idx = tid; idx < G * D; idx += NT) {
     const int g = idx / D, dd = idx % D;
     float M = -INFINITY;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) M = fmaxf(M, wm[k][g]);
+    for (int k = 0; k < NW; ++k) M = fmaxf(M, wm[k][g]);
     float acc = 0.0f, lsum = 0.0f;
     if (M != -INFINITY) {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < NW; ++k) {
         const float f = (wm[k][g] == -INFINITY) ? 0.0f : __expf(wm[k][g] - M);
         acc += f * wo[k][g][dd];
         lsum += f * wl[k][g];
@@ -684,12 +692,12 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
     }
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
-  merge_partials<D, G>(p, unit, b, h, S.mk, S.lk);
+  merge_partials<D, G, NT>(p, unit, b, h, S.mk, S.lk);
 }
 
 // The newest block's refresh (block statistics of a bf16-key block with 16
 // power-iteration columns), run by the extra workgroups of the launch.
-template <int D>
+template <int D, int NT>
 __device__ __forceinline__ void refresh_newest_block(const DecodeParams& p, int unit, char* pool) {
   const int b = unit / p.hkv, h = unit % p.hkv;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
@@ -704,7 +712,7 @@ __device__ __forceinline__ void refresh_newest_block(const DecodeParams& p, int 
   a.mdt = p.mdt;
   a.fdt = p.fdt;
   a.lay = p.lay;
-  block_stats<D, 16, false>(a, b, h, j, min(kL, T - j * kL), pool);
+  block_stats<D, 16, false, NT>(a, b, h, j, min(kL, T - j * kL), pool);
 }
 
 // Grid (workgroups per unit, Hkv, B).
@@ -722,17 +730,23 @@ constexpr size_t lds_max() { return A > B ? A : B; }
 // to different XCDs (consecutive indices go to consecutive XCDs).  With a
 // fused refresh (tail_rec set), workgroups nwg * units + u, dispatched last,
 // refresh the record of unit u's newest block; the attention reads no record.
-template <int D, int G>
-__global__ __launch_bounds__(kDecThreads, (G <= 4) ? 3 : (G <= 8 ? 2 : 1)) void decode_mfma_kernel(DecodeParams p) {
-  __shared__ __align__(16) char pool[lds_max<sizeof(DecodeLds<D, G>), stats_lds_bytes<D, 16, false>()>()];
+template <int D, int G, int NT = decode_threads<G>()>
+__global__ __launch_bounds__(NT, 1) void decode_mfma_kernel(DecodeParams p) {
+  __shared__ __align__(16) char pool[lds_max<sizeof(DecodeLds<D, G, NT>), stats_lds_bytes<D, 16, false>()>()];
   const int na = p.nwg * p.units;
   if ((int)blockIdx.x >= na) {
-    refresh_newest_block<D>(p, blockIdx.x - na, pool);
+    refresh_newest_block<D, NT>(p, blockIdx.x - na, pool);
     return;
   }
   const int x = blockIdx.x / p.units, up = blockIdx.x % p.units;
   const int unit = (up + x) % p.units;
-  decode_mfma_task<D, G>(p, unit / p.hkv, unit % p.hkv, x, pool);
+  decode_mfma_task<D, G, NT>(p, unit / p.hkv, unit % p.hkv, x, pool);
+}
+
+// The bf16 decode launch can carry the newest-block refresh (any head count).
+bool decode_hosts_refresh(int g, bool f32) {
+  (void)g;
+  return !f32;
 }
 
 // ------------------------------------------------------------- launchers --
@@ -765,9 +779,10 @@ int decode_max_wg(int s, int w, int nbmax, bool f32) {
 // one round (an underfilled last round streams at a fraction of the bandwidth).
 hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int nbmax, hipStream_t st) {
   const DecodeKernel k = (d == 128) ? decode_kernel_d<128>(g, f32) : decode_kernel_d<64>(g, f32);
+  const int nt = f32 ? kDecThreads : (g <= 4 ? decode_threads<4>() : (g <= 8 ? decode_threads<8>() : decode_threads<16>()));
   const int items = decode_items(p.s, p.w, nbmax, f32);
   const int64_t units = (int64_t)batch * p.hkv;
-  const int64_t slots = (int64_t)resident_workgroups(reinterpret_cast<const void*>(k), kDecThreads) * device_cus();
+  const int64_t slots = (int64_t)resident_workgroups(reinterpret_cast<const void*>(k), nt) * device_cus();
   // one round of the chip's resident workgroup slots, the items spread evenly
   // over a unit's workgroups
   int64_t spw = (units * items + slots - 1) / slots;
@@ -778,7 +793,7 @@ hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int 
   p.spw = std::max(1, (items + nwg - 1) / nwg);
   p.units = (int)units;
   if (f32) hipLaunchKernelGGL(k, dim3(nwg, p.hkv, batch), dim3(kDecThreads), 0, st, p);
-  else hipLaunchKernelGGL(k, dim3((unsigned)(nwg * units + (p.tail_rec ? units : 0))), dim3(kDecThreads), 0, st, p);
+  else hipLaunchKernelGGL(k, dim3((unsigned)(nwg * units + (p.tail_rec ? units : 0))), dim3(nt), 0, st, p);
   return hipGetLastError();
 }
 
