@@ -171,6 +171,8 @@ cobs_status_t cobs_sparse_decode(const cobs_config_t* cfg, const float* q, const
  * caller has already written the new token's K/V at position T-1 and counted
  * it in seq_lens), then select and attend.  Equivalent to
  * cobs_build_block_stats on block (T-1)/L, cobs_select and cobs_sparse_decode.
+ * With bf16 K/V and rank <= 4 it is two launches (the selector's workgroup
+ * that scores the newest block recomputes its record first), else three.
  *   summaries: in/out.   sel: optional device int32 [B, Hkv, budget] output.    */
 cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
                                const int32_t* seq_lens, void* summaries, int32_t* sel,

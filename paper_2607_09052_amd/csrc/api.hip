@@ -150,10 +150,14 @@ cobs_status_t run_build(const Derived& v, const cobs_kv_t* kv, const int32_t* se
   return hip_status(launch_build(p, v.d, grid, st));
 }
 
+// `kv` non-null (decode step, bf16 K/V, r <= 4): the launch also recomputes
+// each row's newest block's record in these summaries before scoring it.
 cobs_status_t run_select(const Derived& v, const float* q, const void* summaries,
                          const int32_t* seq_lens, int32_t* sel, float* scores, uint8_t* ws,
-                         hipStream_t st) {
+                         hipStream_t st, const cobs_kv_t* kv = nullptr) {
   SelectParams p;
+  p.tail_rec = kv ? static_cast<uint8_t*>(const_cast<void*>(summaries)) : nullptr;
+  p.kv = kv ? make_view(kv, v) : KvView{};
   p.q = q;
   p.rec = static_cast<const uint8_t*>(summaries);
   p.seq_lens = seq_lens;
@@ -178,17 +182,10 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
   return hip_status(launch_select(p, v.d, v.G, v.B, st));
 }
 
-// `tail_rec` non-null (bf16 K/V only): the launch also refreshes the record of
-// each row's newest block in these summaries.
 cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
                          const int32_t* seq_lens, const int32_t* sel, float* out, float* lse,
-                         uint8_t* ws, hipStream_t st, void* tail_rec = nullptr) {
+                         uint8_t* ws, hipStream_t st) {
   DecodeParams p;
-  p.tail_rec = static_cast<uint8_t*>(tail_rec);
-  p.r = v.r;
-  p.mdt = v.mdt;
-  p.fdt = v.fdt;
-  p.lay = v.lay;
   p.q = q;
   p.kv = make_view(kv, v);
   p.seq_lens = seq_lens;
@@ -317,12 +314,10 @@ cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const c
   // the selection goes to the caller's buffer if given, else to the workspace
   int32_t* selp = sel ? sel : reinterpret_cast<int32_t*>(wsb + v.step_sel);
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (v.w >= kL && v.r <= 4 && decode_hosts_refresh(v.G, v.kv_f32 != 0)) {
-    // The block holding the newest token lies in the window: no candidate's
-    // record changes in this step, and the attention reads no record, so the
-    // refresh rides in the attention launch (extra workgroups, dispatched last).
-    if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st)) != COBS_OK) return s;
-    return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st, summaries);
+  if (select_refreshes(v.r, v.kv_f32 != 0)) {
+    // the selector's launch recomputes the newest block's record before scoring
+    if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st, kv)) != COBS_OK) return s;
+    return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
   }
   if ((s = run_build(v, kv, seq_lens, 0, 0, true, summaries, st)) != COBS_OK) return s;
   if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st)) != COBS_OK) return s;

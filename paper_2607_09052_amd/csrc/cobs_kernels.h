@@ -27,6 +27,11 @@ struct SelectParams {
   int hkv, hq, nbmax, tmax, r, s, w, mdt, fdt, nch, bpw;
   float c;
   RecLayout lay;
+  // decode step (bf16 K/V, r <= 4): the workgroup whose chunk holds a row's
+  // newest block first recomputes that block's record in `tail_rec` (the same
+  // records as `rec`) from the keys in `kv`; null: no refresh
+  uint8_t* tail_rec;
+  KvView kv;
 };
 
 struct DecodeParams {
@@ -41,11 +46,6 @@ struct DecodeParams {
   int hkv, hq, tmax, s, w, nwg, spw;   // spw: work items (segments or pieces) per workgroup
   int units;        // B*Hkv
   float c;
-  // bf16 K/V: refresh of each row's newest block in the same launch (null: no
-  // refresh); the record geometry below is used only then
-  uint8_t* tail_rec;
-  int r, mdt, fdt;
-  RecLayout lay;
 };
 
 hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st);
@@ -58,7 +58,7 @@ hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st
 bool select_on_matrix_cores(int mdt, int fdt);
 int select_min_bpw(int mdt, int fdt);
 hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int nbmax, hipStream_t st);
-bool decode_hosts_refresh(int g, bool f32);
+bool select_refreshes(int r, bool kv_f32);
 int decode_max_wg(int s, int w, int nbmax, bool f32);
 
 // Resident workgroups of `threads` threads per CU for a kernel, and the CU

@@ -695,58 +695,22 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   merge_partials<D, G, NT>(p, unit, b, h, S.mk, S.lk);
 }
 
-// The newest block's refresh (block statistics of a bf16-key block with 16
-// power-iteration columns), run by the extra workgroups of the launch.
-template <int D, int NT>
-__device__ __forceinline__ void refresh_newest_block(const DecodeParams& p, int unit, char* pool) {
-  const int b = unit / p.hkv, h = unit % p.hkv;
-  const int T = clamp_len(p.seq_lens[b], p.tmax);
-  if (T <= 0) return;
-  const int j = (T - 1) / kL;
-  StatsArgs a;
-  a.kv = p.kv;
-  a.rec = p.tail_rec;
-  a.hkv = p.hkv;
-  a.nbmax = p.kv.nbmax;
-  a.r = p.r;
-  a.mdt = p.mdt;
-  a.fdt = p.fdt;
-  a.lay = p.lay;
-  block_stats<D, 16, false, NT>(a, b, h, j, min(kL, T - j * kL), pool);
-}
-
 // Grid (workgroups per unit, Hkv, B).
 template <int D, int G, bool F32>
 __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
   decode_task<D, G, F32>(p, blockIdx.z, blockIdx.y, blockIdx.x);
 }
 
-template <size_t A, size_t B>
-constexpr size_t lds_max() { return A > B ? A : B; }
-
-// One-dimensional grid of nwg * units attention workgroups: workgroup x of
-// unit u sits at index x * units + (u - x) mod units, so the workgroups of a
-// unit are dispatched in different rounds and, when units is a multiple of 8,
-// to different XCDs (consecutive indices go to consecutive XCDs).  With a
-// fused refresh (tail_rec set), workgroups nwg * units + u, dispatched last,
-// refresh the record of unit u's newest block; the attention reads no record.
+// One-dimensional grid of nwg * units workgroups: workgroup x of unit u sits
+// at index x * units + (u - x) mod units, so the workgroups of a unit are
+// dispatched in different rounds and, when units is a multiple of 8, to
+// different XCDs (consecutive indices go to consecutive XCDs).
 template <int D, int G, int NT = decode_threads<G>()>
 __global__ __launch_bounds__(NT, 1) void decode_mfma_kernel(DecodeParams p) {
-  __shared__ __align__(16) char pool[lds_max<sizeof(DecodeLds<D, G, NT>), stats_lds_bytes<D, 16, false>()>()];
-  const int na = p.nwg * p.units;
-  if ((int)blockIdx.x >= na) {
-    refresh_newest_block<D, NT>(p, blockIdx.x - na, pool);
-    return;
-  }
+  __shared__ __align__(16) char pool[sizeof(DecodeLds<D, G, NT>)];
   const int x = blockIdx.x / p.units, up = blockIdx.x % p.units;
   const int unit = (up + x) % p.units;
   decode_mfma_task<D, G, NT>(p, unit / p.hkv, unit % p.hkv, x, pool);
-}
-
-// The bf16 decode launch can carry the newest-block refresh (any head count).
-bool decode_hosts_refresh(int g, bool f32) {
-  (void)g;
-  return !f32;
 }
 
 // ------------------------------------------------------------- launchers --
@@ -793,7 +757,7 @@ hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int 
   p.spw = std::max(1, (items + nwg - 1) / nwg);
   p.units = (int)units;
   if (f32) hipLaunchKernelGGL(k, dim3(nwg, p.hkv, batch), dim3(kDecThreads), 0, st, p);
-  else hipLaunchKernelGGL(k, dim3((unsigned)(nwg * units + (p.tail_rec ? units : 0))), dim3(nt), 0, st, p);
+  else hipLaunchKernelGGL(k, dim3((unsigned)(nwg * units)), dim3(nt), 0, st, p);
   return hipGetLastError();
 }
 

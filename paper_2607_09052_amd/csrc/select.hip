@@ -13,6 +13,10 @@ SelectKernel select_mfma_kernel_for(const SelectParams& p, int d, int g);
 
 bool select_on_matrix_cores(int mdt, int fdt) { return mdt != DT_F32 && fdt != DT_F32; }
 
+// The selector can recompute the newest block's record itself (bf16 keys,
+// rank <= 4).
+bool select_refreshes(int r, bool kv_f32) { return !kv_f32 && r <= 4; }
+
 int select_min_bpw(int mdt, int fdt) { return select_on_matrix_cores(mdt, fdt) ? 64 : 16; }
 
 hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st) {

@@ -16,7 +16,7 @@
 // arithmetic, which keeps the loads free of per-lane branches.
 #pragma once
 
-#include "cobs_kernels.h"
+#include "block_stats.h"
 
 namespace cobs {
 
@@ -134,7 +134,7 @@ template <size_t MAIN>
 constexpr size_t select_pool_bytes() { return sizeof(FinishLds) > MAIN ? sizeof(FinishLds) : MAIN; }
 
 template <int G, int KPT>
-__device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds& F) {
+__device__ __forceinline__ void finish_select(const SelectParams& p, int unit, int T, FinishLds& F) {
   static_assert(KPT * kSelThreads <= kMaxBlocksPerSeq, "key slots");
   constexpr int UB = (64 / G) < KPT ? (64 / G) : KPT;    // slots whose scores load together
   static_assert(kMaxBlocksPerSeq / 32 == kSelThreads, "one bitmap word per thread");
@@ -346,12 +346,15 @@ __device__ void finish_select(const SelectParams& p, int unit, int T, FinishLds&
 // stored vector; the lanes' partial dot products for the G query heads are
 // combined by a 16-lane DPP reduction.
 // ---------------------------------------------------------------------------
+template <int G>
+constexpr size_t select_valu_lds() { return select_pool_bytes<2 * 16 * G * 4>(); }
+
+// `pool`: select_valu_lds<G>() bytes of LDS.
 template <int D, int G, int RMAX, int MDT, int FDT>
-__device__ __forceinline__ void select_task(const SelectParams& p, int b, int h, int chunk) {
+__device__ __forceinline__ void select_task(const SelectParams& p, int b, int h, int chunk, char* pool) {
   constexpr int EPL = D / 16;
   constexpr int MW = slice_words<MDT, EPL>(), FW = slice_words<FDT, EPL>();
   constexpr int SW = (FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0;    // 16-byte words of factor scales
-  __shared__ __align__(16) char pool[select_pool_bytes<2 * 16 * G * 4>()];
   float (*gm)[G] = reinterpret_cast<float (*)[G]>(pool);
   float (*gs)[G] = reinterpret_cast<float (*)[G]>(pool + 16 * G * 4);
   __shared__ int s_last;
@@ -515,13 +518,18 @@ __device__ __forceinline__ sbf16x8_t tile_operand(const uint32_t* w, int kk) {
   }
 }
 
+template <int G, int RMAX, int FDT>
+constexpr size_t select_mfma_lds() {
+  return select_pool_bytes<4 * 16 * (1 + ((FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0)) * 16 + 2 * 4 * G * 4>();
+}
+
+// `pool`: select_mfma_lds<G, RMAX, FDT>() bytes of LDS.
 template <int D, int G, int RMAX, int MDT, int FDT>
-__device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, int h, int chunk) {
+__device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, int h, int chunk, char* pool) {
   static_assert(MDT != DT_F32 && FDT != DT_F32, "matrix-core scorer takes bf16 / E2M1 descriptors");
   constexpr int KST = D / 32;                                  // k-steps per lane group
   constexpr int MW = elem_bytes<MDT>(D / 4) / 4, FW = elem_bytes<FDT>(D / 4) / 4;
   constexpr int HU = 1 + ((FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0);   // 16-byte header words used
-  __shared__ __align__(16) char pool[select_pool_bytes<4 * 16 * HU * 16 + 2 * 4 * G * 4>()];
   uint4 (*hdr_s)[16][HU] = reinterpret_cast<uint4 (*)[16][HU]>(pool);
   float (*gm)[G] = reinterpret_cast<float (*)[G]>(pool + 4 * 16 * HU * 16);
   float (*gs)[G] = reinterpret_cast<float (*)[G]>(pool + 4 * 16 * HU * 16 + 4 * G * 4);
@@ -668,12 +676,49 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
 // Grid (chunks, Hkv, B).
 template <int D, int G, int RMAX, int MDT, int FDT>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
-  select_task<D, G, RMAX, MDT, FDT>(p, blockIdx.z, blockIdx.y, blockIdx.x);
+  __shared__ __align__(16) char pool[select_valu_lds<G>()];
+  select_task<D, G, RMAX, MDT, FDT>(p, blockIdx.z, blockIdx.y, blockIdx.x, pool);
 }
 
 template <int D, int G, int RMAX, int MDT, int FDT>
 __global__ __launch_bounds__(kSelThreads) void select_mfma_kernel(SelectParams p) {
-  select_mfma_task<D, G, RMAX, MDT, FDT>(p, blockIdx.z, blockIdx.y, blockIdx.x);
+  __shared__ __align__(16) char pool[select_mfma_lds<G, RMAX, FDT>()];
+  select_mfma_task<D, G, RMAX, MDT, FDT>(p, blockIdx.z, blockIdx.y, blockIdx.x, pool);
+}
+
+template <size_t A, size_t B>
+constexpr size_t lds_max() { return A > B ? A : B; }
+
+// The decode step's selector (bf16 keys, r <= 4): the workgroup whose chunk
+// holds row b's newest block first recomputes that block's record (its count,
+// mean and, once full, factors: the statistics follow the block as it fills,
+// §5.6), so the block's score and the normaliser over all blocks see the
+// cache as it is now.  The block statistics routine runs with 16 power
+// iteration columns on the same LDS pool.
+template <int D, int G, int MDT, int FDT>
+__global__ __launch_bounds__(kSelThreads) void select_refresh_kernel(SelectParams p) {
+  constexpr bool kMat = MDT != DT_F32 && FDT != DT_F32;
+  constexpr size_t kSel = kMat ? select_mfma_lds<G, 4, FDT>() : select_valu_lds<G>();
+  __shared__ __align__(16) char pool[lds_max<kSel, stats_lds_bytes<D, 16, false>()>()];
+  const int b = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
+  const int T = clamp_len(p.seq_lens[b], p.tmax);
+  if (T > 0 && ((T - 1) / kL) / p.bpw == chunk) {
+    const int j = (T - 1) / kL;
+    StatsArgs a;
+    a.kv = p.kv;
+    a.rec = p.tail_rec;
+    a.hkv = p.hkv;
+    a.nbmax = p.nbmax;
+    a.r = p.r;
+    a.mdt = p.mdt;
+    a.fdt = p.fdt;
+    a.lay = p.lay;
+    block_stats<D, 16, false>(a, b, h, j, min(kL, T - j * kL), pool);
+    __builtin_amdgcn_s_waitcnt(0);       // the record is written before it is scored
+    __syncthreads();
+  }
+  if constexpr (kMat) select_mfma_task<D, G, 4, MDT, FDT>(p, b, h, chunk, pool);
+  else select_task<D, G, 4, MDT, FDT>(p, b, h, chunk, pool);
 }
 
 }  // namespace cobs

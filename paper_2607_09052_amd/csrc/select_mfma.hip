@@ -7,6 +7,7 @@ typedef void (*SelectKernel)(SelectParams);
 
 template <int D, int G, int MDT, int FDT>
 static SelectKernel pick(const SelectParams& p) {
+  if (p.tail_rec) return (p.r <= 4) ? select_refresh_kernel<D, G, MDT, FDT> : nullptr;
   return (p.r <= 4) ? select_mfma_kernel<D, G, 4, MDT, FDT> : select_mfma_kernel<D, G, kMaxRank, MDT, FDT>;
 }
 

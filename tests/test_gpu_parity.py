@@ -391,8 +391,10 @@ def test_build_bf16_keys_and_storage_dtypes_consistent():
 
 @pytest.mark.parametrize("w", [300, 40])
 def test_decode_step_is_build_select_decode(w):
-    """Window >= one block: the newest block's refresh runs beside selection and
-    decode; a shorter window makes it a candidate, refreshed before selection."""
+    """The step recomputes each row's newest block before scoring it (the tail
+    records start stale here), so it selects and attends exactly as the
+    selector and the attention do on fresh records, with the newest block in
+    the window (w = 300) or a candidate (w = 40)."""
     prob = synth.make_problem("c3", seed=31, B=2, Hq=16, Hkv=4, T=3000, s=10, w=w)
     cfg_d = prob["cfg"]
     cfg = cobs.Config(batch=2, num_q_heads=16, num_kv_heads=4, head_dim=128, max_seq_len=3008, rank=4,
