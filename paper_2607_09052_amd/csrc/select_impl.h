@@ -696,10 +696,13 @@ constexpr size_t lds_max() { return A > B ? A : B; }
 // cache as it is now.  The block statistics routine runs with 16 power
 // iteration columns on the same LDS pool.
 template <int D, int G, int MDT, int FDT>
-__global__ __launch_bounds__(kSelThreads) void select_refresh_kernel(SelectParams p) {
+constexpr size_t select_refresh_lds() {
   constexpr bool kMat = MDT != DT_F32 && FDT != DT_F32;
-  constexpr size_t kSel = kMat ? select_mfma_lds<G, 4, FDT>() : select_valu_lds<G>();
-  __shared__ __align__(16) char pool[lds_max<kSel, stats_lds_bytes<D, 16, false>()>()];
+  return lds_max<kMat ? select_mfma_lds<G, 4, FDT>() : select_valu_lds<G>(), stats_lds_bytes<D, 16, false>()>();
+}
+
+template <int D, int G, int MDT, int FDT>
+__device__ __forceinline__ void select_refresh_task(const SelectParams& p, char* pool) {
   const int b = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   if (T > 0 && ((T - 1) / kL) / p.bpw == chunk) {
@@ -717,8 +720,30 @@ __global__ __launch_bounds__(kSelThreads) void select_refresh_kernel(SelectParam
     __builtin_amdgcn_s_waitcnt(0);       // the record is written before it is scored
     __syncthreads();
   }
-  if constexpr (kMat) select_mfma_task<D, G, 4, MDT, FDT>(p, b, h, chunk, pool);
+  if constexpr (MDT != DT_F32 && FDT != DT_F32) select_mfma_task<D, G, 4, MDT, FDT>(p, b, h, chunk, pool);
   else select_task<D, G, 4, MDT, FDT>(p, b, h, chunk, pool);
+}
+
+// Instantiations whose registers fit three workgroups per CU without spills
+// get that cap (the routine's accumulators would otherwise push them to two);
+// the others keep the compiler's choice.
+template <int D, int G, int MDT, int FDT>
+constexpr bool select_refresh_capped() {
+  if (MDT != DT_F32 && FDT != DT_F32) return !(D == 128 && FDT == DT_BF16);
+  return G <= 4 || (D == 64 && G <= 8 && MDT != DT_E2M1);
+}
+
+template <int D, int G, int MDT, int FDT>
+__global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_waves_per_eu(3)))
+void select_refresh_kernel(SelectParams p) {
+  __shared__ __align__(16) char pool[select_refresh_lds<D, G, MDT, FDT>()];
+  select_refresh_task<D, G, MDT, FDT>(p, pool);
+}
+
+template <int D, int G, int MDT, int FDT>
+__global__ __launch_bounds__(kSelThreads) void select_refresh_kernel_wide(SelectParams p) {
+  __shared__ __align__(16) char pool[select_refresh_lds<D, G, MDT, FDT>()];
+  select_refresh_task<D, G, MDT, FDT>(p, pool);
 }
 
 }  // namespace cobs
