@@ -22,7 +22,9 @@ and replayed, so host launch overhead is not in the measurement.
 Prints one JSON line: the metric (us per decode step per layer), achieved GB/s
 on the step's algorithmic bytes, the roofline of the dominant kernel (timed on
 its own the same way, HIP events on the launch stream) and the fp64 oracle's
-time on the host cores as a baseline.
+time on the host cores as a baseline.  config.eager_call_us adds per-call
+median / p10 / p90 of eager (not graph) steps, launch included: steady, over
+the rotating copies, and cold, after a 1 GiB read that evicts the caches.
 """
 
 import argparse
@@ -336,6 +338,37 @@ def main():
         if it > 0:
             pre_ms.append(e0.elapsed_time(e1))
     del r_pre
+    # per-call distributions, eager launches timed one by one with HIP events on
+    # the launch stream: steady (rotating layer copies, as in the timed loop) and
+    # cold (a 1 GiB write between calls evicts the caches)
+    def one_call(i):
+        q, k, v, r_ = layers[i % copies]
+        cobs.cobs_decode_step(cfg, q, k, v, seqs[i % copies], r_, out, wss[i % copies], sel=sels[i % copies],
+                              lse=lse, stream=stream)
+
+    def per_call(n, before=None):
+        xs = []
+        for i in range(n):
+            if before is not None:
+                before(i)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            one_call(i)
+            e1.record(stream)
+            e1.synchronize()
+            xs.append(e0.elapsed_time(e1) * 1e3)
+        return {"median": round(float(np.median(xs)), 3), "p10": round(float(np.percentile(xs, 10)), 3),
+                "p90": round(float(np.percentile(xs, 90)), 3), "calls": n}
+
+    n_calls = max(64, min(400, 4 * copies))
+    steady = per_call(n_calls)
+    # the eviction reads 1 GiB (a write would leave the caches full of dirty
+    # lines whose write-back would then land in the timed call)
+    flush = torch.ones(256 * 1024 * 1024, dtype=torch.float32, device=dev)
+    sink = torch.empty((), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    cold = per_call(min(n_calls, 100), before=lambda i: torch.amax(flush, dim=0, out=sink))
+    del flush, sink
     torch.cuda.set_stream(torch.cuda.default_stream())
 
     kbytes = {"select_kernel": ab["select"], "decode_kernel": ab["decode"], "build_stats_kernel": ab["tail"]}
@@ -367,6 +400,7 @@ def main():
             "layer_copies_rotated": copies,
             "kernels_us": {k_: round(v_, 3) for k_, v_ in kern_us.items()},
             "fill_step_us": round(fill_us, 3),
+            "eager_call_us": {"steady": steady, "cold": cold},
             "fill_step_bytes": ab_fill["step"],
             "prefill_build": prefill_summary(cfg, B, T_hi, float(np.median(pre_ms))),
         },
