@@ -670,13 +670,13 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
     }
   }
   __syncthreads();
-  float* wpart = p.part + ((int64_t)unit * p.nwg + wg) * G * (D + 2);
-  for (int idx = tid; idx < G * D; idx += NT) {
-    const int g = idx / D, dd = idx % D;
-    float M = -INFINITY;
+  // the waves' states combined, output (g, dd) of the workgroup
+  auto combine = [&](int g, int dd, float& M, float& acc, float& lsum) {
+    M = -INFINITY;
 #pragma unroll
     for (int k = 0; k < NW; ++k) M = fmaxf(M, wm[k][g]);
-    float acc = 0.0f, lsum = 0.0f;
+    acc = 0.0f;
+    lsum = 0.0f;
     if (M != -INFINITY) {
 #pragma unroll
       for (int k = 0; k < NW; ++k) {
@@ -685,6 +685,25 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
         lsum += f * wl[k][g];
       }
     }
+  };
+  if (p.nwg == 1) {
+    // the unit's only workgroup: its state is the unit's, written as the merge
+    // of a single partial would write it (weight exp(0) = 1)
+    for (int idx = tid; idx < G * D; idx += NT) {
+      const int g = idx / D, dd = idx % D;
+      float M, acc, lsum;
+      combine(g, dd, M, acc, lsum);
+      const int64_t oq = (int64_t)b * p.hq + h * G + g;
+      p.out[oq * D + dd] = (lsum > 0.0f) ? acc / lsum : 0.0f;
+      if (dd == 0 && p.lse) p.lse[oq] = (lsum > 0.0f) ? M + logf(lsum) : -INFINITY;
+    }
+    return;
+  }
+  float* wpart = p.part + ((int64_t)unit * p.nwg + wg) * G * (D + 2);
+  for (int idx = tid; idx < G * D; idx += NT) {
+    const int g = idx / D, dd = idx % D;
+    float M, acc, lsum;
+    combine(g, dd, M, acc, lsum);
     st_agent(&wpart[g * (D + 2) + 2 + dd], acc);
     if (dd == 0) {
       st_agent(&wpart[g * (D + 2)], M);

@@ -201,6 +201,33 @@ def test_sparse_decode_matches_oracle(d, G, kv, s, w):
             check_out(out_h[b, h * G:(h + 1) * G], lse_h[b, h * G:(h + 1) * G], o, l, kv)
 
 
+def test_sparse_decode_one_workgroup_per_unit():
+    """256 units: each unit's pieces fit one attention workgroup, which writes
+    out and lse itself instead of a partial for a merge."""
+    d, G, Hkv, Tmax, s, w = 128, 4, 4, 1024, 4, 128
+    rng = np.random.default_rng(17)
+    seq = rng.integers(300, Tmax + 1, size=64).astype(np.int32)
+    seq[0], seq[1] = Tmax, 65
+    prob = _decode_problem(d, G, "bf16", seq, Hkv, Tmax, seed=23)
+    cfg = _cfg(batch=len(seq), num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=Tmax,
+               budget=s, window=w)
+    sel = synth.make_selection(len(seq), Hkv, seq, 64, w, s, seed=29, fill="random")[:, :, :s]
+    q, k, v = prob["q"], prob["k"], prob["v"]
+    out = torch.empty((len(seq), G * Hkv, d), dtype=torch.float32, device=DEV)
+    lse = torch.empty((len(seq), G * Hkv), dtype=torch.float32, device=DEV)
+    ws = cobs.new_workspace(cfg, cobs.OP_DECODE, DEV)
+    say("sparse_decode 256 units")
+    cobs.cobs_sparse_decode(cfg, q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(seq).to(DEV),
+                            sel.contiguous().to(DEV), out, ws, lse=lse)
+    sync()
+    out_h, lse_h = out.cpu().numpy(), lse.cpu().numpy()
+    for b in [0, 1, 2, 17, 40, 63]:
+        for h in range(Hkv):
+            o, l = oracle_decode(q[b, h * G:(h + 1) * G].double().numpy(), f64(k[b, h]), f64(v[b, h]),
+                                 int(seq[b]), sel[b, h].numpy(), cfg)
+            check_out(out_h[b, h * G:(h + 1) * G], lse_h[b, h * G:(h + 1) * G], o, l, "bf16")
+
+
 def test_sparse_decode_edge_cases():
     """T = 0, T <= w (dense window), w = 0 with a partial tail candidate, invalid selection entries."""
     d, G, Hkv, Tmax, s, w = 128, 4, 1, 1024, 4, 128
