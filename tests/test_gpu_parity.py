@@ -416,25 +416,32 @@ def test_build_bf16_keys_and_storage_dtypes_consistent():
 
 # --------------------------------------------------------- decode step --
 
-@pytest.mark.parametrize("w", [300, 40])
-def test_decode_step_is_build_select_decode(w):
+@pytest.mark.parametrize("w,t0,rank,kv", [
+    (300, 3000, 4, "bf16"),     # newest block partial, in the window
+    (40, 3000, 4, "bf16"),      # newest block a candidate
+    (300, 3008, 4, "bf16"),     # block-fill step: the selector launch computes factors
+    (300, 3000, 6, "bf16"),     # rank above 4: refresh launched before the selector
+    (40, 3008, 2, "f32"),       # fp32 keys: refresh launched before the selector
+])
+def test_decode_step_is_build_select_decode(w, t0, rank, kv):
     """The step recomputes each row's newest block before scoring it (the tail
     records start stale here), so it selects and attends exactly as the
-    selector and the attention do on fresh records, with the newest block in
-    the window (w = 300) or a candidate (w = 40)."""
-    prob = synth.make_problem("c3", seed=31, B=2, Hq=16, Hkv=4, T=3000, s=10, w=w)
+    selector and the attention do on fresh records, whichever launches carry
+    the refresh."""
+    prob = synth.make_problem("c3", seed=31, B=2, Hq=16, Hkv=4, T=3000, s=10, w=w, kv_dtype=kv)
     cfg_d = prob["cfg"]
-    cfg = cobs.Config(batch=2, num_q_heads=16, num_kv_heads=4, head_dim=128, max_seq_len=3008, rank=4,
-                      budget=10, window=w)
+    cfg = cobs.Config(batch=2, num_q_heads=16, num_kv_heads=4, head_dim=128, max_seq_len=3008, rank=rank,
+                      budget=10, window=w, kv_dtype=kv)
     assert cfg_d["T_max"] == 3008
     k, v, q = prob["k"].to(DEV), prob["v"].to(DEV), prob["q"].to(DEV)
-    seq = torch.tensor([3000, 2049], dtype=torch.int32, device=DEV)
+    lens = [t0, 2049]
+    seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
     rec0 = cobs.new_summaries(cfg, DEV)
-    say("step composition: build")
+    say(f"step composition: build (w={w} T={t0} r={rank} {kv})")
     cobs.cobs_build_block_stats(cfg, k, v, seq, rec0)
     # decode step on a copy whose tail records are stale (zeroed)
     rec1 = rec0.clone()
-    for b, T in enumerate([3000, 2049]):
+    for b, T in enumerate(lens):
         rec1[b, :, (T - 1) // 64] = 0
     out1 = torch.empty((2, 16, 128), dtype=torch.float32, device=DEV)
     lse1 = torch.empty((2, 16), dtype=torch.float32, device=DEV)
