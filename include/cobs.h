@@ -71,7 +71,8 @@ typedef enum {
   COBS_OP_BUILD = 0,  /* cobs_build_block_stats */
   COBS_OP_SELECT = 1, /* cobs_select            */
   COBS_OP_DECODE = 2, /* cobs_sparse_decode     */
-  COBS_OP_STEP = 3    /* cobs_decode_step       */
+  COBS_OP_STEP = 3,   /* cobs_decode_step       */
+  COBS_OP_SELECT_EXACT = 4 /* cobs_select_exact  */
 } cobs_op_t;
 
 /* Problem description shared by every call (host struct, passed by pointer). */
@@ -156,6 +157,21 @@ cobs_status_t cobs_build_block_stats(const cobs_config_t* cfg, const cobs_kv_t* 
 cobs_status_t cobs_select(const cobs_config_t* cfg, const float* q, const void* summaries,
                           const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
                           size_t ws_bytes, void* stream);
+
+/* Exact-mass block selection: the Oracle Sparse Attention ranking of Sec. 3.5.
+ * For every block b and query head g of a KV head, the exact log-mass
+ * l_b^g = ln sum_{t in b} exp(c q_g . k_t) over the block's T-clamped tokens
+ * (eq. bg-defs) replaces the descriptor estimate; normaliser, group score
+ * (eq. prop-gqa in log form), candidates, top-s and outputs are those of
+ * cobs_select.  Reads every key of the cache once (a recall ceiling for the
+ * summary-based selectors, not a decode-time path).
+ *   kv:   bf16 keys only (COBS_ERR_UNSUPPORTED for fp32); V is not read.
+ *   ws:   cobs_workspace_bytes(cfg, COBS_OP_SELECT_EXACT), zero-filled before
+ *         its first use and left zeroed by every call.
+ *   q, seq_lens, sel, scores: as for cobs_select.                              */
+cobs_status_t cobs_select_exact(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
+                                size_t ws_bytes, void* stream);
 
 /* Block-sparse decode attention (eq. oracle-true over the kept-token union).
  *   sel:  device int32 [B, Hkv, budget] block ids.  The longest prefix that is

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcobs.so"
 
 F32, BF16, E2M1 = 0, 1, 2
 DTYPES = {"f32": F32, "bf16": BF16, "e2m1": E2M1}
-OP_BUILD, OP_SELECT, OP_DECODE, OP_STEP = 0, 1, 2, 3
+OP_BUILD, OP_SELECT, OP_DECODE, OP_STEP, OP_SELECT_EXACT = 0, 1, 2, 3, 4
 BLOCK = 64
 
 
@@ -48,6 +48,7 @@ _SIGS = {
     "cobs_build_block_stats": (ctypes.c_int, [_P, _P, _P, ctypes.c_int32, ctypes.c_int32, _P, _P,
                                               ctypes.c_size_t, _P]),
     "cobs_select": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "cobs_select_exact": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_sparse_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_decode_step": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_pack_e2m1": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P]),
@@ -166,6 +167,14 @@ def cobs_select(cfg, q, summaries, seq_lens, sel, ws, scores=None, stream=None):
     _check(lib().cobs_select(ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(summaries),
                              _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws),
                              ws.numel() * ws.element_size(), _stream(stream, q)))
+
+
+def cobs_select_exact(cfg, q, k, v, seq_lens, sel, ws, scores=None, block_table=None, num_pages=0,
+                      stream=None):
+    kv = _kv(k, v, block_table, num_pages)
+    _check(lib().cobs_select_exact(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
+                                   _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws),
+                                   ws.numel() * ws.element_size(), _stream(stream, q)))
 
 
 def cobs_sparse_decode(cfg, q, k, v, seq_lens, sel, out, ws, lse=None, block_table=None,

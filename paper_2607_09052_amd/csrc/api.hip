@@ -53,6 +53,8 @@ struct Derived {
   size_t sel_ell, sel_part, sel_cnt, sel_bytes;
   size_t dec_part, dec_cnt, dec_bytes;
   size_t step_sel, step_bytes;   // decode step: select region, decode region, selection
+  int nchx_max;                  // exact-mass selector: chunks per unit, upper bound
+  size_t selx_part, selx_cnt, selx_bytes;
 };
 
 Derived derive(const cobs_config_t* c) {
@@ -87,6 +89,12 @@ Derived derive(const cobs_config_t* c) {
   v.dec_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nwg_max * v.G * (v.d + 2), kAlign);
   v.dec_cnt = off;  off = round_up(off + sizeof(unsigned) * (size_t)v.units, kAlign);
   v.dec_bytes = off;
+  // the exact-mass selector: the selector's layout with its own chunk bound
+  v.nchx_max = (v.nbmax + select_exact_min_bpw() - 1) / select_exact_min_bpw();
+  off = round_up(sizeof(float) * (size_t)v.units * v.G * v.nbmax, kAlign);
+  v.selx_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nchx_max * v.G * 2, kAlign);
+  v.selx_cnt = off;  off = round_up(off + sizeof(unsigned) * (size_t)v.units, kAlign);
+  v.selx_bytes = off;
   v.step_sel = v.sel_bytes + v.dec_bytes;
   v.step_bytes = round_up(v.step_sel + sizeof(int32_t) * (size_t)v.units * v.s, kAlign);
   return v;
@@ -182,6 +190,36 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
   return hip_status(launch_select(p, v.d, v.G, v.B, st));
 }
 
+cobs_status_t run_select_exact(const Derived& v, const float* q, const cobs_kv_t* kv,
+                               const int32_t* seq_lens, int32_t* sel, float* scores, uint8_t* ws,
+                               hipStream_t st) {
+  SelectParams p;
+  p.q = q;
+  p.rec = nullptr;
+  p.tail_rec = nullptr;
+  p.kv = make_view(kv, v);
+  p.seq_lens = seq_lens;
+  p.sel = sel;
+  p.scores = scores;
+  p.ell = reinterpret_cast<float*>(ws + v.sel_ell);
+  p.part = reinterpret_cast<float*>(ws + v.selx_part);
+  p.cnt = reinterpret_cast<unsigned*>(ws + v.selx_cnt);
+  p.hkv = v.hkv;
+  p.hq = v.hq;
+  p.nbmax = v.nbmax;
+  p.tmax = v.tmax;
+  p.r = v.r;
+  p.s = v.s;
+  p.w = v.w;
+  p.mdt = v.mdt;
+  p.fdt = v.fdt;
+  p.nch = v.nchx_max;
+  p.bpw = 0;
+  p.c = v.c;
+  p.lay = v.lay;
+  return hip_status(launch_select_exact(p, v.d, v.G, v.B, st));
+}
+
 cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
                          const int32_t* seq_lens, const int32_t* sel, float* out, float* lse,
                          uint8_t* ws, hipStream_t st) {
@@ -255,6 +293,7 @@ size_t cobs_workspace_bytes(const cobs_config_t* cfg, cobs_op_t op) {
     case COBS_OP_SELECT: return v.sel_bytes;
     case COBS_OP_DECODE: return v.dec_bytes;
     case COBS_OP_STEP: return v.step_bytes;
+    case COBS_OP_SELECT_EXACT: return v.selx_bytes;
     default: return 0;
   }
 }
@@ -286,6 +325,20 @@ cobs_status_t cobs_select(const cobs_config_t* cfg, const float* q, const void* 
   if ((s = check_ws(ws, ws_bytes, v.sel_bytes)) != COBS_OK) return s;
   return run_select(v, q, summaries, seq_lens, sel, scores, static_cast<uint8_t*>(ws),
                     static_cast<hipStream_t>(stream));
+}
+
+cobs_status_t cobs_select_exact(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
+                                size_t ws_bytes, void* stream) {
+  cobs_status_t s = check_config(cfg);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if ((s = check_kv(kv, v)) != COBS_OK) return s;
+  if (v.kv_f32) return COBS_ERR_UNSUPPORTED;
+  if (!q || !seq_lens || !sel) return COBS_ERR_INVALID_ARG;
+  if ((s = check_ws(ws, ws_bytes, v.selx_bytes)) != COBS_OK) return s;
+  return run_select_exact(v, q, kv, seq_lens, sel, scores, static_cast<uint8_t*>(ws),
+                          static_cast<hipStream_t>(stream));
 }
 
 cobs_status_t cobs_sparse_decode(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,

@@ -1,0 +1,172 @@
+// Exact-mass block selector (OSA, §3.5): blocks ranked by the exact
+// normalised masses of eq. prop-gqa instead of the descriptor estimate.  It
+// reads every key of the cache once, so it bounds what any block-summary
+// selector can reach at the same budget.
+//
+// Grid (chunks, Hkv, B), 256 threads.  Each wave takes blocks blk_lo + wave,
+// + 4, ... of its workgroup's chunk.  For one block it issues all its key loads
+// at once, in the A layout of v_mfma_f32_16x16x32_bf16 (lane l: row 16 mt +
+// l % 16, d-range [(l / 16) D / 4, (l / 16 + 1) D / 4)), and forms the 64 x 16
+// score tile against the G scaled queries split into three bf16 parts (every
+// product with a bf16 key is exact in fp32).  Lane l ends with 16 scores of head
+// l % 16; a max and a sum of exponentials over the block's tokens, combined
+// across the four lane groups, give ln m_b^g = ln sum_t exp(c q_g . k_t).
+// From there the path is the selector's: l_b^g and a per-chunk (max, sum exp)
+// per head to the workspace, and the unit's last workgroup normalises, forms
+// sigma_b (now the log of the exact group score) and picks the top s.
+#include "select_impl.h"
+
+namespace cobs {
+
+constexpr int kExactBlocksPerPass = 4;   // one block per wave
+
+template <int G>
+constexpr size_t select_exact_lds() { return select_pool_bytes<2 * 4 * G * 4>(); }
+
+template <int D, int G>
+__device__ __forceinline__ void select_exact_task(const SelectParams& p, int b, int h, int chunk, char* pool) {
+  constexpr int KST = D / 32;                  // k-steps; lane group g owns d in [g D/4, (g+1) D/4)
+  float (*gm)[G] = reinterpret_cast<float (*)[G]>(pool);
+  float (*gs)[G] = reinterpret_cast<float (*)[G]>(pool + 4 * G * 4);
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int hcol = lane & 15, grp = lane >> 4;
+  const int unit = b * p.hkv + h;
+  const int T = clamp_len(p.seq_lens[b], p.tmax);
+  const int nb = (T + kL - 1) / kL;
+  const int blk_lo = chunk * p.bpw, blk_hi = min(nb, blk_lo + p.bpw);
+  const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;    // elements between consecutive tokens of a block
+  const char* kbase = static_cast<const char*>(p.kv.k);
+
+  // B operands: head hcol (zero beyond G), d = grp D/4 + 8 kk + j, three bf16 parts
+  sbf16x8_t qb[3][KST];
+  {
+    const float4* qg = reinterpret_cast<const float4*>(
+        p.q + ((int64_t)b * p.hq + h * G + min(hcol, G - 1)) * D + grp * (D / 4));
+    const float qs = (hcol < G) ? p.c : 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < KST; ++kk) {
+      const float4 x0 = qg[2 * kk], x1 = qg[2 * kk + 1];
+      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        float x = xs[j] * qs;
+#pragma unroll
+        for (int part = 0; part < 3; ++part) {
+          const uint32_t bb = f32_to_bf16_rne(x);
+          qb[part][kk][j] = __builtin_bit_cast(__bf16, (uint16_t)bb);
+          x -= __uint_as_float(bb << 16);
+        }
+      }
+    }
+  }
+
+  float run_m = -INFINITY, run_s = 0.0f;       // this wave's blocks, head hcol
+  for (int blk = blk_lo + wave; blk < blk_hi; blk += kExactBlocksPerPass) {
+    const int n = min(kL, T - blk * kL);
+    const int64_t t0 = kv_offset(p.kv, b, h, blk * kL);
+    float l = -INFINITY;
+    if (t0 >= 0) {
+      // rows past n re-read row n - 1; their scores are masked
+      uint4 kr[4][KST];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const uint4* row = reinterpret_cast<const uint4*>(
+            kbase + (t0 + (int64_t)min(16 * mt + hcol, n - 1) * rs) * 2 + grp * (D / 4) * 2);
+#pragma unroll
+        for (int kk = 0; kk < KST; ++kk) kr[mt][kk] = row[kk];
+      }
+      float sc[4][4];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int kk = 0; kk < KST; ++kk) {
+          const sbf16x8_t a = __builtin_bit_cast(sbf16x8_t, kr[mt][kk]);
+#pragma unroll
+          for (int part = 0; part < 3; ++part) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qb[part][kk], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sc[mt][v] = (16 * mt + 4 * grp + v < n) ? acc[v] : -INFINITY;
+      }
+      // log-sum-exp over the block's tokens, head hcol (lanes hcol + 16 g)
+      float mx = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) mx = fmaxf(mx, sc[mt][v]);
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      float se = 0.0f;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) se += (sc[mt][v] == -INFINITY) ? 0.0f : __expf(sc[mt][v] - mx);
+      se += __shfl_xor(se, 16, 64);
+      se += __shfl_xor(se, 32, 64);
+      l = mx + __logf(se);
+    }
+    if (grp == 0 && hcol < G) {
+      st_agent(&p.ell[((int64_t)unit * p.nbmax + blk) * G + hcol], l);
+      lse_merge(run_m, run_s, l, 1.0f);
+    }
+  }
+  if (grp == 0 && hcol < G) {
+    gm[wave][hcol] = run_m;
+    gs[wave][hcol] = run_s;
+  }
+  __syncthreads();
+  if (tid < G) {
+    float m = -INFINITY, s = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) lse_merge(m, s, gm[k][tid], gs[k][tid]);
+    float* pp = p.part + (((int64_t)unit * p.nch + chunk) * G + tid) * 2;
+    st_agent(&pp[0], m);
+    st_agent(&pp[1], s);
+  }
+  if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
+  FinishLds& fin = *reinterpret_cast<FinishLds*>(pool);
+  const int nc = (max(0, T - p.w) + kL - 1) / kL;
+  if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
+  else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
+  else finish_select<G, kMaxBlocksPerSeq / kSelThreads>(p, unit, T, fin);
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(kSelThreads) void select_exact_kernel(SelectParams p) {
+  __shared__ __align__(16) char pool[select_exact_lds<G>()];
+  select_exact_task<D, G>(p, blockIdx.z, blockIdx.y, blockIdx.x, pool);
+}
+
+typedef void (*SelectKernel)(SelectParams);
+
+template <int D>
+static SelectKernel exact_kernel_d(int g) {
+  switch (g) {
+    case 1: return select_exact_kernel<D, 1>;
+    case 2: return select_exact_kernel<D, 2>;
+    case 4: return select_exact_kernel<D, 4>;
+    case 8: return select_exact_kernel<D, 8>;
+    default: return select_exact_kernel<D, 16>;
+  }
+}
+
+int select_exact_min_bpw() { return kExactBlocksPerPass; }
+
+// Chunks of a multiple of four blocks, sized so that the grid fills the chip's
+// resident workgroup slots in one round.
+hipError_t launch_select_exact(SelectParams p, int d, int g, int batch, hipStream_t st) {
+  const SelectKernel k = (d == 128) ? exact_kernel_d<128>(g) : exact_kernel_d<64>(g);
+  const int base = kExactBlocksPerPass;
+  const int64_t units = (int64_t)batch * p.hkv;
+  const int64_t slots = (int64_t)resident_workgroups(reinterpret_cast<const void*>(k), kSelThreads) * device_cus();
+  int64_t bpw = (units * p.nbmax + slots - 1) / slots;
+  bpw = std::max<int64_t>(base, (bpw + base - 1) / base * base);
+  p.bpw = (int)std::min<int64_t>(bpw, ((int64_t)p.nbmax + base - 1) / base * base);
+  p.nch = (p.nbmax + p.bpw - 1) / p.bpw;
+  hipLaunchKernelGGL(k, dim3(p.nch, p.hkv, batch), dim3(kSelThreads), 0, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace cobs

@@ -24,7 +24,7 @@ def _declared_functions():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared_functions()
-    assert len(declared) == 8, declared
+    assert len(declared) == 9, declared
     lib = cobs.lib()
     for name in declared:
         assert hasattr(lib, name), name
@@ -55,6 +55,9 @@ def test_workspace_sizes_are_aligned_and_ordered():
     assert cobs.workspace_bytes(cfg, 0) == 0
     assert sel % 256 == 0 and dec % 256 == 0 and step % 256 == 0
     assert step >= sel + dec
+    exact = cobs.workspace_bytes(cfg, 4)
+    # the exact-mass selector's scores and chunk partials (chunks of >= 4 blocks)
+    assert exact % 256 == 0 and exact >= 4 * cfg.batch * cfg.num_kv_heads * 4 * cfg.num_blocks
 
 
 @pytest.mark.parametrize("over,code", [
@@ -100,4 +103,13 @@ def test_null_and_workspace_errors_on_host():
     assert lib.cobs_build_block_stats(ctypes.byref(cfg), ctypes.byref(kv), fake, 60, 10, fake, None, 0,
                                       None) == 1
     assert lib.cobs_pack_e2m1(fake, 4, 3, fake, fake, None) == 1
+    # exact-mass selector: fp32 keys unsupported, null selection, small workspace
+    kv = cobs._KV(fake.value, fake.value, 0, 0, 128, None, 0)
+    cfg32 = _cfg(kv_dtype="f32").c_struct()
+    assert lib.cobs_select_exact(ctypes.byref(cfg32), fake, ctypes.byref(kv), fake, fake, None, fake,
+                                 1 << 30, None) == 2
+    assert lib.cobs_select_exact(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, None, None, fake,
+                                 1 << 30, None) == 1
+    assert lib.cobs_select_exact(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, fake, None, fake,
+                                 16, None) == 3
     assert lib.cobs_status_string(3).startswith(b"COBS_ERR_WORKSPACE")

@@ -155,6 +155,87 @@ def test_select_long_context_and_boundary_tie_group():
         assert 0 < len(taken) < len(grp) and taken == grp[:len(taken)], (grp, taken)   # straddles; lowest win
 
 
+# ------------------------------------------------ exact-mass (OSA) selector --
+
+EXACT_CASES = [
+    # d, G, s, w
+    (128, 4, 8, 256),
+    (128, 8, 20, 64),
+    (128, 1, 5, 0),
+    (64, 2, 3, 100),
+    (128, 16, 12, 300),
+    (64, 4, 6, 64),
+    (128, 4, 0, 128),
+]
+
+
+@pytest.mark.parametrize("d,G,s,w", EXACT_CASES)
+def test_select_exact_matches_oracle(d, G, s, w):
+    """Exact block log-masses from every key (eq. bg-defs), group score of
+    eq. prop-gqa, top-s: against the oracle's OSA ranking on the same bf16 keys."""
+    Hkv, Tmax = 2, 4096
+    seq = np.array([4096, 2500, 300, 65], np.int32)
+    B = len(seq)
+    prob = _decode_problem(d, G, "bf16", seq, Hkv, Tmax, seed=d + 3 * G + s)
+    cfg = _cfg(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=Tmax,
+               budget=s, window=w)
+    q, k, v = prob["q"], prob["k"], prob["v"]
+    seq_d = torch.from_numpy(seq).to(DEV)
+    sel = torch.full((B, Hkv, max(s, 1)), -7, dtype=torch.int32, device=DEV)
+    scores = torch.empty((B, Hkv, cfg.num_blocks), dtype=torch.float32, device=DEV)
+    ws = cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, DEV)
+    say(f"select_exact d={d} G={G} s={s} w={w}")
+    cobs.cobs_select_exact(cfg, q.to(DEV), k.to(DEV), v.to(DEV), seq_d, sel, ws, scores=scores)
+    sync()
+    sel_h, sc_h = sel.cpu().numpy(), scores.cpu().numpy()
+    for b in range(B):
+        T = int(seq[b])
+        nc = M.candidate_count(T, 64, w)
+        for h in range(Hkv):
+            sigma = M.osa_group_scores(q[b, h * G:(h + 1) * G].double().numpy(), f64(k[b, h]), T, 64, cfg.scale)
+            got = sc_h[b, h]
+            assert np.all(np.abs(got[:nc] - sigma[:nc]) <= SIGMA_TOL), np.max(np.abs(got[:nc] - sigma[:nc]))
+            assert np.all(np.isneginf(got[nc:]))
+            if s > 0:
+                check_selection(sel_h[b, h, :s], sigma, nc, s)
+    # counters are left at zero: a second call is bitwise identical
+    sel2 = torch.full_like(sel, -7)
+    scores2 = torch.empty_like(scores)
+    cobs.cobs_select_exact(cfg, q.to(DEV), k.to(DEV), v.to(DEV), seq_d, sel2, ws, scores=scores2)
+    sync()
+    assert torch.equal(sel, sel2) and torch.equal(scores, scores2)
+
+
+def test_select_exact_paged_matches_contiguous():
+    d, G, Hkv, Tmax, s, w = 128, 4, 2, 2048, 6, 200
+    seq = np.array([2048, 1500], np.int32)
+    prob = _decode_problem(d, G, "bf16", seq, Hkv, Tmax, seed=22)
+    q, k, v = prob["q"].to(DEV), prob["k"].to(DEV), prob["v"].to(DEV)
+    B, nbm = len(seq), Tmax // 64
+    cfg = _cfg(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, max_seq_len=Tmax, budget=s, window=w)
+    perm = torch.randperm(B * nbm, generator=torch.Generator().manual_seed(5))
+    table = perm.view(B, nbm).to(torch.int32)
+    kp = torch.empty((B * nbm, Hkv, 64, d), dtype=k.dtype, device=DEV)
+    for b in range(B):
+        for j in range(nbm):
+            kp[table[b, j]] = k[b, :, j * 64:(j + 1) * 64]
+    seq_d = torch.from_numpy(seq).to(DEV)
+    res = []
+    for paged in (False, True):
+        sel = torch.empty((B, Hkv, s), dtype=torch.int32, device=DEV)
+        scores = torch.empty((B, Hkv, nbm), dtype=torch.float32, device=DEV)
+        ws = cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, DEV)
+        say(f"select_exact paged={paged}")
+        if paged:
+            cobs.cobs_select_exact(cfg, q, kp, kp, seq_d, sel, ws, scores=scores, block_table=table.to(DEV),
+                                   num_pages=B * nbm)
+        else:
+            cobs.cobs_select_exact(cfg, q, k, v, seq_d, sel, ws, scores=scores)
+        sync()
+        res.append((sel, scores))
+    assert torch.equal(res[0][0], res[1][0]) and torch.equal(res[0][1], res[1][1])
+
+
 # ---------------------------------------------------------- sparse decode --
 
 DECODE_CASES = [
