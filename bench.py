@@ -80,22 +80,25 @@ def algorithmic_bytes(cfg, seq_lens, sel):
     select: every block's descriptor (unpadded), q, sel written.
     decode: K and V of every attended token, q, sel, out and lse written.
     tail:   the keys of the block holding the newest token, its record written.
+    keys:   every key of the cache once, q and sel (the exact-mass selector).
     """
     B, Hkv, Hq, d = cfg.batch, cfg.num_kv_heads, cfg.num_q_heads, cfg.head_dim
     kv = ESZ[cfg.kv_dtype]
     q_bytes = B * Hq * d * 4
     sel_bytes = B * Hkv * cfg.budget * 4
     out_bytes = B * Hq * (d + 1) * 4
-    score = dec = tail = 0
+    score = dec = tail = keys = 0
     for b in range(B):
         T = int(seq_lens[b])
+        keys += Hkv * T * d * kv
         score += Hkv * (-(-T // 64)) * descriptor_bytes(cfg)
         n_tail = T - (T - 1) // 64 * 64
         tail += Hkv * (n_tail * d * kv + cobs.record_bytes(cfg))
         for h in range(Hkv):
             dec += union_tokens(T, cfg.window, sel[b, h].tolist()) * d * kv * 2
     return dict(select=score + q_bytes + sel_bytes, decode=dec + q_bytes + sel_bytes + out_bytes,
-                tail=tail, step=score + dec + tail + q_bytes + sel_bytes + out_bytes)
+                tail=tail, step=score + dec + tail + q_bytes + sel_bytes + out_bytes,
+                keys=keys + q_bytes + sel_bytes)
 
 
 def kernel_source_hash():
@@ -301,11 +304,17 @@ def main():
             cobs.cobs_build_block_stats(cfg, k, v, seqs[i], r_, first_block=cfg.num_blocks - 1, num_blocks=1,
                                         stream=stream)
 
+    osa_ws = [cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, dev) for _ in layers]
+
+    def sweep_osa():
+        for i, (q, k, v, r_) in enumerate(layers):
+            cobs.cobs_select_exact(cfg, q, k, v, seqs[i], sels[i], osa_ws[i], stream=stream)
+
     def sweep_fill():
         for i, (q, k, v, r_) in enumerate(layers):
             cobs.cobs_decode_step(cfg, q, k, v, seq_hi, r_, out, wss[i], sel=sels[i], lse=lse, stream=stream)
 
-    for fn in (sweep_step, sweep_select, sweep_decode, sweep_tail, sweep_fill):   # eager warm-up
+    for fn in (sweep_step, sweep_select, sweep_decode, sweep_tail, sweep_fill, sweep_osa):   # eager warm-up
         fn()
     torch.cuda.synchronize()
     g_step = capture(sweep_step, stream)
@@ -326,6 +335,11 @@ def main():
     g_fill = capture(sweep_fill, stream)
     g_fill.replay()
     fill_us = replay_time(g_fill, max(2, reps // 4), stream) / copies
+    # the exact-mass (OSA) selector, same protocol: it reads every key once
+    g_osa = capture(sweep_osa, stream)
+    g_osa.replay()
+    osa_us = replay_time(g_osa, max(2, reps // 4), stream) / copies
+    osa_bytes = ab["keys"]
     # prefill: statistics of every block of the cache (one layer copy), eager launches
     r_pre = torch.empty_like(rec)
     pre_ms = []
@@ -401,6 +415,9 @@ def main():
             "kernels_us": {k_: round(v_, 3) for k_, v_ in kern_us.items()},
             "fill_step_us": round(fill_us, 3),
             "eager_call_us": {"steady": steady, "cold": cold},
+            "osa_select": {"us": round(osa_us, 3), "key_bytes": round(osa_bytes),
+                           "gbps": round(osa_bytes / (osa_us * 1e-6) / 1e9, 1),
+                           "frac": round(osa_bytes / (osa_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)},
             "fill_step_bytes": ab_fill["step"],
             "prefill_build": prefill_summary(cfg, B, T_hi, float(np.median(pre_ms))),
         },
