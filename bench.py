@@ -28,6 +28,7 @@ the rotating copies, and cold, after a 1 GiB read that evicts the caches.
 """
 
 import argparse
+import dataclasses
 import json
 import math
 import os
@@ -165,6 +166,39 @@ def capture(fn, stream):
     with torch.cuda.graph(g, stream=stream):
         fn()
     return g
+
+
+def needle_recall(prob, cfg, seq, dev):
+    """Share of the planted needle blocks that each selector keeps, by kind.
+
+    The c3 cache carries mean-shift needles (k + 2u) and curvature needles
+    (k + a u with a ~ N(0, 4): the mean is unchanged, only the spread along u
+    grows).  A first-order selector (rank 0) is blind to the second kind;
+    the second-order estimate (the configured rank) and the exact masses are not.
+    """
+    sels = {}
+    for name, rank in (("rank%d" % cfg.rank, cfg.rank), ("rank0", 0)):
+        c = dataclasses.replace(cfg, rank=rank)
+        rec = cobs.new_summaries(c, dev)
+        cobs.cobs_build_block_stats(c, prob["k"], prob["v"], seq, rec)
+        sel = torch.empty((c.batch, c.num_kv_heads, c.budget), dtype=torch.int32, device=dev)
+        cobs.cobs_select(c, prob["q"], rec, seq, sel, cobs.new_workspace(c, cobs.OP_SELECT, dev))
+        sels[name] = sel.cpu()
+        del rec
+    sel = torch.empty((cfg.batch, cfg.num_kv_heads, cfg.budget), dtype=torch.int32, device=dev)
+    cobs.cobs_select_exact(cfg, prob["q"], prob["k"], prob["v"], seq, sel,
+                           cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, dev))
+    sels["exact_mass"] = sel.cpu()
+    out = {}
+    for name, sl in sels.items():
+        hit = {"mean": [0, 0], "curvature": [0, 0]}
+        for (b, h), kinds in prob["needle_kinds"].items():
+            chosen = set(sl[b, h].tolist())
+            for blk, kind in kinds.items():
+                hit[kind][0] += blk in chosen
+                hit[kind][1] += 1
+        out[name] = {k: round(v[0] / v[1], 4) for k, v in hit.items()}
+    return out
 
 
 def cpu_baseline(prob, cfg, t_lo, budget_s=12.0):
@@ -426,6 +460,8 @@ def main():
                      "algorithmic_bytes": round(kbytes[dom])},
         "cpu_baseline": None,
     }
+    if "needles" in prob and prob["needles"]:
+        res["config"]["needle_recall"] = needle_recall(prob, cfg, seq_hi, dev)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(prob, cfg, t_lo)
     print(json.dumps(res), flush=True)

@@ -116,7 +116,7 @@ def _keys_c3(cfg, q, g, device):
         K[b] = mu + torch.matmul(A, z).transpose(-1, -2) + eps
     K = K.reshape(B, Hkv, nb * L, d)
     nc = -(-max(0, T - w) // L)
-    needles = {}
+    needles, kinds = {}, {}
     if nc >= 5:
         for b in range(B):
             for h in range(Hkv):
@@ -131,7 +131,8 @@ def _keys_c3(cfg, q, g, device):
                         a = _randn((L, 1), g, device, 2.0)
                         K[b, h, sl] += a * u
                 needles[(b, h)] = sorted(pick)
-    return K[:, :, :Tm], needles
+                kinds[(b, h)] = {blk: ("mean" if j < 3 else "curvature") for j, blk in enumerate(pick)}
+    return K[:, :, :Tm], needles, kinds
 
 
 def _keys_c4(cfg, g, device):
@@ -161,7 +162,7 @@ def make_problem(name, seed=None, device="cpu", **over):
 
     Returns dict(cfg, q [B,Hq,d] fp32, k, v [B,Hkv,T_max,d] in the K/V dtype,
     seq_lens [B] int32 (all T), and for c5 q_steps [steps,B,Hq,d]; for c1 the
-    planted block and for c3 the needle blocks, per (b, h)).
+    planted block and for c3 the needle blocks, per (b, h), and their kinds).
     """
     cfg = config(name, **over)
     seed = SEED_BASE + int(name[1:]) if seed is None else seed
@@ -175,7 +176,7 @@ def make_problem(name, seed=None, device="cpu", **over):
     elif law == "c2":
         K = _keys_c2(cfg, g, device)
     elif law == "c3":
-        K, extra["needles"] = _keys_c3(cfg, q, g, device)
+        K, extra["needles"], extra["needle_kinds"] = _keys_c3(cfg, q, g, device)
     elif law == "c4":
         K = _keys_c4(cfg, g, device)
     elif law == "c5":
