@@ -183,6 +183,19 @@ cobs_status_t cobs_sparse_decode(const cobs_config_t* cfg, const float* q, const
                                  const int32_t* seq_lens, const int32_t* sel, float* out,
                                  float* lse, void* ws, size_t ws_bytes, void* stream);
 
+/* The decode attention split into the two branches a caller-side gate
+ * combines (the selection and sliding-window branches of the NSA layout the
+ * paper builds on, Sec. 2): out_sel / lse_sel over the selected blocks' tokens
+ * before the window start, out_win / lse_win over the last w tokens.  The two
+ * token sets are disjoint and their union is cobs_sparse_decode's, so merging
+ * the pairs by log-sum-exp gives its out and lse.  An empty branch gives 0 and
+ * -inf.  Arguments as for cobs_sparse_decode (same workspace size); bf16 K/V
+ * only (COBS_ERR_UNSUPPORTED for fp32).  lse_sel, lse_win optional.           */
+cobs_status_t cobs_sparse_decode_branches(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                          const int32_t* seq_lens, const int32_t* sel, float* out_sel,
+                                          float* lse_sel, float* out_win, float* lse_win, void* ws,
+                                          size_t ws_bytes, void* stream);
+
 /* One decode step: refresh the record of the block holding token T-1 (the
  * caller has already written the new token's K/V at position T-1 and counted
  * it in seq_lens), then select and attend.  Equivalent to

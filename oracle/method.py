@@ -213,6 +213,27 @@ def sparse_attention(q, K, V, U, c):
     return (p @ Vu) / l, (m + np.log(l))[:, 0]
 
 
+def branch_tokens(T, L, w, sel):
+    """The two disjoint token sets of the union: tokens of the selected blocks
+    before the window start, and the last w tokens (the selection and window
+    branches of the NSA layout of Sec. 2)."""
+    ws = max(0, int(T) - int(w))
+    sel_set = set()
+    for b in np.asarray(sel).tolist():
+        if b >= 0:
+            sel_set.update(range(b * L, min(b * L + L, ws)))
+    return np.array(sorted(sel_set), dtype=np.int64), np.arange(ws, int(T), dtype=np.int64)
+
+
+def branch_attention(q, K, V, T, L, w, sel, c):
+    """Softmax attention of each branch on its own: (out, lse) over the selected
+    blocks' tokens and (out, lse) over the window, eq. (oracle-true) on each set."""
+    Us, Uw = branch_tokens(T, L, w, sel)
+    o_s, l_s = sparse_attention(q, K, V, Us, c)
+    o_w, l_w = sparse_attention(q, K, V, Uw, c)
+    return o_s, l_s, o_w, l_w
+
+
 def decode_unit(q, K, V, T, L, r, s, w, c, mean_dtype, factor_dtype, stats=None):
     """One decode step of one (batch, KV head) unit, every stage in order.
 

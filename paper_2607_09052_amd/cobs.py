@@ -50,6 +50,7 @@ _SIGS = {
     "cobs_select": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_select_exact": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_sparse_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "cobs_sparse_decode_branches": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_decode_step": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_pack_e2m1": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P]),
     "cobs_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -183,6 +184,15 @@ def cobs_sparse_decode(cfg, q, k, v, seq_lens, sel, out, ws, lse=None, block_tab
     _check(lib().cobs_sparse_decode(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
                                     _ptr(seq_lens), _ptr(sel), _ptr(out), _ptr(lse), _ptr(ws),
                                     ws.numel() * ws.element_size(), _stream(stream, q)))
+
+
+def cobs_sparse_decode_branches(cfg, q, k, v, seq_lens, sel, out_sel, out_win, ws, lse_sel=None, lse_win=None,
+                                block_table=None, num_pages=0, stream=None):
+    kv = _kv(k, v, block_table, num_pages)
+    _check(lib().cobs_sparse_decode_branches(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
+                                             _ptr(seq_lens), _ptr(sel), _ptr(out_sel), _ptr(lse_sel),
+                                             _ptr(out_win), _ptr(lse_win), _ptr(ws),
+                                             ws.numel() * ws.element_size(), _stream(stream, q)))
 
 
 def cobs_decode_step(cfg, q, k, v, seq_lens, summaries, out, ws, sel=None, lse=None,

@@ -220,10 +220,15 @@ cobs_status_t run_select_exact(const Derived& v, const float* q, const cobs_kv_t
   return hip_status(launch_select_exact(p, v.d, v.G, v.B, st));
 }
 
+// `out_w` non-null: the selection branch goes to out/lse and the window branch
+// to out_w/lse_w (bf16 K/V).
 cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
                          const int32_t* seq_lens, const int32_t* sel, float* out, float* lse,
-                         uint8_t* ws, hipStream_t st) {
+                         uint8_t* ws, hipStream_t st, float* out_w = nullptr, float* lse_w = nullptr) {
   DecodeParams p;
+  p.nwg_s = out_w ? 0 : -1;
+  p.out_w = out_w;
+  p.lse_w = lse_w;
   p.q = q;
   p.kv = make_view(kv, v);
   p.seq_lens = seq_lens;
@@ -352,6 +357,21 @@ cobs_status_t cobs_sparse_decode(const cobs_config_t* cfg, const float* q, const
   if ((s = check_ws(ws, ws_bytes, v.dec_bytes)) != COBS_OK) return s;
   return run_decode(v, q, kv, seq_lens, sel, out, lse, static_cast<uint8_t*>(ws),
                     static_cast<hipStream_t>(stream));
+}
+
+cobs_status_t cobs_sparse_decode_branches(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                          const int32_t* seq_lens, const int32_t* sel, float* out_sel,
+                                          float* lse_sel, float* out_win, float* lse_win, void* ws,
+                                          size_t ws_bytes, void* stream) {
+  cobs_status_t s = check_config(cfg);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if ((s = check_kv(kv, v)) != COBS_OK) return s;
+  if (v.kv_f32) return COBS_ERR_UNSUPPORTED;
+  if (!q || !seq_lens || !out_sel || !out_win || (!sel && v.s > 0)) return COBS_ERR_INVALID_ARG;
+  if ((s = check_ws(ws, ws_bytes, v.dec_bytes)) != COBS_OK) return s;
+  return run_decode(v, q, kv, seq_lens, sel, out_sel, lse_sel, static_cast<uint8_t*>(ws),
+                    static_cast<hipStream_t>(stream), out_win, lse_win);
 }
 
 cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,

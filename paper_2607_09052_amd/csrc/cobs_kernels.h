@@ -46,6 +46,12 @@ struct DecodeParams {
   int hkv, hq, tmax, s, w, nwg, spw;   // spw: work items (segments or pieces) per workgroup
   int units;        // B*Hkv
   float c;
+  // nwg_s < 0: one output over the union.  nwg_s >= 0 (bf16 K/V): the
+  // selected blocks (out, lse) and the window (out_w, lse_w) separately; the
+  // launcher sets nwg_s to the selected branch's workgroup count.
+  int nwg_s;
+  float* out_w;
+  float* lse_w;
 };
 
 hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st);

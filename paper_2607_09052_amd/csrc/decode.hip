@@ -115,18 +115,20 @@ __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, in
   __syncthreads();
 }
 
-// Last workgroup of a unit: merge the unit's nwg (<= kMaxDecodeWg) partials
-// (max, sum, unnormalised output per head) in workgroup order and write out and
-// lse.  Thread t owns outputs t + 256 j; the partials' statistics go to LDS
-// while the first KB partials' outputs load into registers in the same round
-// trip, and each thread forms the merge weights of its own heads.
+// Last workgroup of a unit: merge `nwg` of the unit's partials (max, sum,
+// unnormalised output per head), from partial `first` on, in workgroup order
+// and write `out` and `lse`.  Thread t owns outputs t + NT j; the partials'
+// statistics go to LDS while the first KB partials' outputs load into
+// registers in the same round trip, and each thread forms the merge weights of
+// its own heads.  No partials: out 0 and lse -inf.
 template <int D, int G, int NT = kDecThreads>
-__device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, float (*mk)[G], float (*lk)[G]) {
+__device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, float (*mk)[G], float (*lk)[G],
+                               int first, int nwg, float* out, float* lse) {
   constexpr int OPT = (G * D + NT - 1) / NT;                     // outputs per thread
   constexpr int KB = (OPT <= 2) ? 32 : ((OPT <= 4) ? 16 : 8);     // partials per load batch (64 registers)
   const int tid = threadIdx.x;
-  const int nwg = p.nwg;
-  const __amdgpu_buffer_rsrc_t up = coherent_view(p.part + (int64_t)unit * nwg * G * (D + 2), 4u * nwg * G * (D + 2));
+  const __amdgpu_buffer_rsrc_t up =
+      coherent_view(p.part + ((int64_t)unit * p.nwg + first) * G * (D + 2), 4u * nwg * G * (D + 2));
   float ov[KB][OPT];
   // partials past the last one fall outside the view: those loads return 0
   // without touching memory, and their values are not used
@@ -181,8 +183,8 @@ __device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, fl
     if (idx < G * D) {
       const int g = idx / D, dd = idx % D;
       const int64_t oq = (int64_t)b * p.hq + h * G + g;
-      p.out[oq * D + dd] = (L[j] > 0.0f) ? acc[j] / L[j] : 0.0f;
-      if (dd == 0 && p.lse) p.lse[oq] = (L[j] > 0.0f) ? M[j] + logf(L[j]) : -INFINITY;
+      out[oq * D + dd] = (L[j] > 0.0f) ? acc[j] / L[j] : 0.0f;
+      if (dd == 0 && lse) lse[oq] = (L[j] > 0.0f) ? M[j] + logf(L[j]) : -INFINITY;
     }
   }
 }
@@ -365,7 +367,7 @@ __device__ __forceinline__ void decode_task(const DecodeParams& p, int b, int h,
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
 
   __shared__ float mk[kMaxDecodeWg][G], lk[kMaxDecodeWg][G];
-  merge_partials<D, G>(p, unit, b, h, mk, lk);
+  merge_partials<D, G>(p, unit, b, h, mk, lk, 0, p.nwg, p.out, p.lse);
 }
 
 // ---------------------------------------------------------------------------
@@ -452,7 +454,17 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   const int nc = (ws + kL - 1) / kL;
   const int nwin = (T > ws) ? ((T - 1) / kL - ws / kL + 1) : 0;
   const int npiece = 2 * (p.s + nwin);
-  const int pc_lo = wg * p.spw, pc_end = min(npiece, pc_lo + p.spw);
+  // one output: the unit's pieces in order; two: the first nwg_s workgroups
+  // take the selected blocks' pieces, the others the window's
+  int pc_lo = wg * p.spw, pc_end = min(npiece, pc_lo + p.spw);
+  if (p.nwg_s >= 0) {
+    if (wg < p.nwg_s) {
+      pc_end = min(2 * p.s, pc_lo + p.spw);
+    } else {
+      pc_lo = 2 * p.s + (wg - p.nwg_s) * p.spw;
+      pc_end = min(npiece, pc_lo + p.spw);
+    }
+  }
   const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;        // elements between consecutive tokens
 
   decode_prologue<D, G, PT, NT>(p, b, h, T, ws, nc, pc_lo, max(0, min(NT, pc_end - pc_lo)), true,
@@ -686,7 +698,7 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
       }
     }
   };
-  if (p.nwg == 1) {
+  if (p.nwg == 1 && p.nwg_s < 0) {
     // the unit's only workgroup: its state is the unit's, written as the merge
     // of a single partial would write it (weight exp(0) = 1)
     for (int idx = tid; idx < G * D; idx += NT) {
@@ -711,7 +723,13 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
     }
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
-  merge_partials<D, G, NT>(p, unit, b, h, S.mk, S.lk);
+  if (p.nwg_s < 0) {
+    merge_partials<D, G, NT>(p, unit, b, h, S.mk, S.lk, 0, p.nwg, p.out, p.lse);
+  } else {
+    merge_partials<D, G, NT>(p, unit, b, h, S.mk, S.lk, 0, p.nwg_s, p.out, p.lse);
+    __syncthreads();                       // the statistics in LDS are reused
+    merge_partials<D, G, NT>(p, unit, b, h, S.mk, S.lk, p.nwg_s, p.nwg - p.nwg_s, p.out_w, p.lse_w);
+  }
 }
 
 // Grid (workgroups per unit, Hkv, B).
@@ -771,9 +789,19 @@ hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int 
   int64_t spw = (units * items + slots - 1) / slots;
   spw = std::max<int64_t>(spw, (items + kMaxDecodeWg - 1) / kMaxDecodeWg);
   spw = std::max<int64_t>(spw, 4);
-  const int nwg = std::max(1, (int)((items + spw - 1) / spw));
+  int nwg = std::max(1, (int)((items + spw - 1) / spw));
   p.nwg = nwg;
   p.spw = std::max(1, (items + nwg - 1) / nwg);
+  if (p.nwg_s >= 0) {
+    // two outputs: no workgroup mixes the branches; the split stays within
+    // the workspace's partial count
+    const int is = 2 * p.s, iw = items - is, cap = decode_max_wg(p.s, p.w, nbmax, false);
+    int sp = (int)spw;
+    while ((is + sp - 1) / sp + (iw + sp - 1) / sp > cap) ++sp;
+    p.spw = sp;
+    p.nwg_s = (is + sp - 1) / sp;
+    nwg = p.nwg = std::max(1, p.nwg_s + (iw + sp - 1) / sp);
+  }
   p.units = (int)units;
   if (f32) hipLaunchKernelGGL(k, dim3(nwg, p.hkv, batch), dim3(kDecThreads), 0, st, p);
   else hipLaunchKernelGGL(k, dim3((unsigned)(nwg * units)), dim3(nt), 0, st, p);

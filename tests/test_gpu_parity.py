@@ -282,6 +282,50 @@ def test_sparse_decode_matches_oracle(d, G, kv, s, w):
             check_out(out_h[b, h * G:(h + 1) * G], lse_h[b, h * G:(h + 1) * G], o, l, kv)
 
 
+@pytest.mark.parametrize("d,G,s,w", [(128, 4, 6, 256), (128, 8, 10, 100), (64, 2, 0, 128), (128, 1, 5, 0),
+                                      (128, 16, 7, 300)])
+def test_sparse_decode_branches_match_oracle(d, G, s, w):
+    """Selection and window branches each against the oracle's attention on its
+    own token set; merged by log-sum-exp they give cobs_sparse_decode's output."""
+    seq = np.array([2048, 1000, 77, 700], np.int32)
+    Hkv, Tmax = 2, 2048
+    prob = _decode_problem(d, G, "bf16", seq, Hkv, Tmax, seed=d + 5 * G + s)
+    cfg = _cfg(batch=len(seq), num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=Tmax,
+               budget=s, window=w)
+    sel = synth.make_selection(len(seq), Hkv, seq, 64, w, max(s, 1), seed=13 + s, fill="random")[:, :, :s]
+    q, k, v = prob["q"], prob["k"], prob["v"]
+    shp = (len(seq), G * Hkv, d)
+    o_s, o_w, o_u = (torch.empty(shp, dtype=torch.float32, device=DEV) for _ in range(3))
+    l_s, l_w, l_u = (torch.empty(shp[:2], dtype=torch.float32, device=DEV) for _ in range(3))
+    ws = cobs.new_workspace(cfg, cobs.OP_DECODE, DEV)
+    qd, kd, vd, sd = q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(seq).to(DEV)
+    seld = sel.contiguous().to(DEV)
+    say(f"sparse_decode_branches d={d} G={G} s={s} w={w}")
+    cobs.cobs_sparse_decode_branches(cfg, qd, kd, vd, sd, seld, o_s, o_w, ws, lse_sel=l_s, lse_win=l_w)
+    cobs.cobs_sparse_decode(cfg, qd, kd, vd, sd, seld, o_u, ws, lse=l_u)
+    sync()
+    hs, hw = o_s.cpu().numpy(), o_w.cpu().numpy()
+    ls, lw = l_s.cpu().numpy(), l_w.cpu().numpy()
+    for b in range(len(seq)):
+        for h in range(Hkv):
+            gs = slice(h * G, (h + 1) * G)
+            ref = M.branch_attention(q[b, gs].double().numpy(), f64(k[b, h]), f64(v[b, h]), int(seq[b]), 64, w,
+                                     sel[b, h].numpy(), cfg.scale)
+            check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16")
+            check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16")
+    # the log-sum-exp merge of the branches is the union's attention
+    ls64, lw64 = ls.astype(np.float64), lw.astype(np.float64)
+    m = np.maximum(ls64, lw64)
+    m = np.where(np.isfinite(m), m, 0.0)
+    a, bw = np.exp(ls64 - m), np.exp(lw64 - m)
+    den = np.where(a + bw > 0, a + bw, 1.0)
+    merged = (a[..., None] * hs + bw[..., None] * hw) / den[..., None]
+    np.testing.assert_allclose(merged, o_u.cpu().numpy(), rtol=2e-5, atol=2e-6)
+    lu = l_u.cpu().numpy()
+    fin = np.isfinite(lu)
+    np.testing.assert_allclose((m + np.log(den))[fin], lu[fin], rtol=0, atol=2e-5)
+
+
 def test_sparse_decode_one_workgroup_per_unit():
     """256 units: each unit's pieces fit one attention workgroup, which writes
     out and lse itself instead of a partial for a merge."""

@@ -351,3 +351,24 @@ def test_record_algorithmic_bytes_match_descriptor_accounting():
             lay = R.layout(128, 4, md, fd)
             assert lay["total"] % 16 == 0
             assert lay["total"] - R.algorithmic_bytes(128, 4, md, fd) < 16
+
+
+def test_branch_outputs_merge_to_the_union_attention():
+    """The selection and window branches partition the union: their log-sum-exp
+    merge is the union attention, an empty branch is (0, -inf), and a selection
+    reaching into the window is cut at the window start."""
+    rng = np.random.default_rng(91)
+    T, L, d, G, c = 700, 64, 32, 3, 0.2
+    K, V, q = rng.standard_normal((T, d)), rng.standard_normal((T, d)), rng.standard_normal((G, d))
+    for w, sel in [(100, [0, 3, 9, -1]), (0, [2, 5]), (700, [1]), (150, [-1, -1]), (90, [8, 10])]:
+        o_s, l_s, o_w, l_w = M.branch_attention(q, K, V, T, L, w, sel, c)
+        o_u, l_u = M.sparse_attention(q, K, V, M.union_tokens(T, L, w, sel), c)
+        m = np.maximum(l_s, l_w)
+        a, b = np.exp(l_s - m), np.exp(l_w - m)
+        np.testing.assert_allclose(m + np.log(a + b), l_u, rtol=0, atol=1e-12)
+        np.testing.assert_allclose((a[:, None] * o_s + b[:, None] * o_w) / (a + b)[:, None], o_u, rtol=0, atol=1e-12)
+        Us, Uw = M.branch_tokens(T, L, w, sel)
+        assert len(np.intersect1d(Us, Uw)) == 0 and np.all(Us < T - w)
+    # empty selection branch
+    o_s, l_s, _, _ = M.branch_attention(q, K, V, T, L, 100, [-1], c)
+    assert np.all(o_s == 0) and np.all(np.isneginf(l_s))
