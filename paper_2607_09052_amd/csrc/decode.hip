@@ -122,7 +122,7 @@ __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, in
 // registers in the same round trip, and each thread forms the merge weights of
 // its own heads.  No partials: out 0 and lse -inf.
 template <int D, int G, int NT = kDecThreads>
-__device__ void merge_partials(const DecodeParams& p, int unit, int b, int h, float (*mk)[G], float (*lk)[G],
+__device__ __forceinline__ void merge_partials(const DecodeParams& p, int unit, int b, int h, float (*mk)[G], float (*lk)[G],
                                int first, int nwg, float* out, float* lse) {
   constexpr int OPT = (G * D + NT - 1) / NT;                     // outputs per thread
   constexpr int KB = (OPT <= 2) ? 32 : ((OPT <= 4) ? 16 : 8);     // partials per load batch (64 registers)
@@ -420,7 +420,8 @@ struct DecodeLds {
 template <int G>
 constexpr int decode_threads() { return G <= 4 ? 768 : (G <= 8 ? 512 : 256); }
 
-template <int D, int G, int NT>
+// BR: the two-branch form (selected blocks and window in separate outputs).
+template <int D, int G, int NT, bool BR>
 __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, int h, int wg, char* pool) {
   constexpr int NW = NT / 64;                 // waves
   static_assert(G <= 16, "at most 16 query heads per KV head");
@@ -457,7 +458,7 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   // one output: the unit's pieces in order; two: the first nwg_s workgroups
   // take the selected blocks' pieces, the others the window's
   int pc_lo = wg * p.spw, pc_end = min(npiece, pc_lo + p.spw);
-  if (p.nwg_s >= 0) {
+  if constexpr (BR) {
     if (wg < p.nwg_s) {
       pc_end = min(2 * p.s, pc_lo + p.spw);
     } else {
@@ -698,7 +699,7 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
       }
     }
   };
-  if (p.nwg == 1 && p.nwg_s < 0) {
+  if (!BR && p.nwg == 1) {
     // the unit's only workgroup: its state is the unit's, written as the merge
     // of a single partial would write it (weight exp(0) = 1)
     for (int idx = tid; idx < G * D; idx += NT) {
@@ -723,7 +724,7 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
     }
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nwg, &s_last)) return;
-  if (p.nwg_s < 0) {
+  if constexpr (!BR) {
     merge_partials<D, G, NT>(p, unit, b, h, S.mk, S.lk, 0, p.nwg, p.out, p.lse);
   } else {
     merge_partials<D, G, NT>(p, unit, b, h, S.mk, S.lk, 0, p.nwg_s, p.out, p.lse);
@@ -742,25 +743,31 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(DecodeParams p) {
 // at index x * units + (u - x) mod units, so the workgroups of a unit are
 // dispatched in different rounds and, when units is a multiple of 8, to
 // different XCDs (consecutive indices go to consecutive XCDs).
-template <int D, int G, int NT = decode_threads<G>()>
+template <int D, int G, bool BR = false, int NT = decode_threads<G>()>
 __global__ __launch_bounds__(NT, 1) void decode_mfma_kernel(DecodeParams p) {
   __shared__ __align__(16) char pool[sizeof(DecodeLds<D, G, NT>)];
   const int x = blockIdx.x / p.units, up = blockIdx.x % p.units;
   const int unit = (up + x) % p.units;
-  decode_mfma_task<D, G, NT>(p, unit / p.hkv, unit % p.hkv, x, pool);
+  decode_mfma_task<D, G, NT, BR>(p, unit / p.hkv, unit % p.hkv, x, pool);
 }
 
 // ------------------------------------------------------------- launchers --
 typedef void (*DecodeKernel)(DecodeParams);
 
+template <int D, int G>
+static DecodeKernel decode_kernel_g(bool f32, bool br) {
+  if (f32) return decode_kernel<D, G, true>;
+  return br ? decode_mfma_kernel<D, G, true> : decode_mfma_kernel<D, G, false>;
+}
+
 template <int D>
-static DecodeKernel decode_kernel_d(int g, bool f32) {
+static DecodeKernel decode_kernel_d(int g, bool f32, bool br) {
   switch (g) {
-    case 1: return f32 ? decode_kernel<D, 1, true> : decode_mfma_kernel<D, 1>;
-    case 2: return f32 ? decode_kernel<D, 2, true> : decode_mfma_kernel<D, 2>;
-    case 4: return f32 ? decode_kernel<D, 4, true> : decode_mfma_kernel<D, 4>;
-    case 8: return f32 ? decode_kernel<D, 8, true> : decode_mfma_kernel<D, 8>;
-    default: return f32 ? decode_kernel<D, 16, true> : decode_mfma_kernel<D, 16>;
+    case 1: return decode_kernel_g<D, 1>(f32, br);
+    case 2: return decode_kernel_g<D, 2>(f32, br);
+    case 4: return decode_kernel_g<D, 4>(f32, br);
+    case 8: return decode_kernel_g<D, 8>(f32, br);
+    default: return decode_kernel_g<D, 16>(f32, br);
   }
 }
 
@@ -779,7 +786,8 @@ int decode_max_wg(int s, int w, int nbmax, bool f32) {
 // each), sized so that the grid fills the chip's resident workgroup slots in
 // one round (an underfilled last round streams at a fraction of the bandwidth).
 hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int nbmax, hipStream_t st) {
-  const DecodeKernel k = (d == 128) ? decode_kernel_d<128>(g, f32) : decode_kernel_d<64>(g, f32);
+  const bool br = p.nwg_s >= 0;
+  const DecodeKernel k = (d == 128) ? decode_kernel_d<128>(g, f32, br) : decode_kernel_d<64>(g, f32, br);
   const int nt = f32 ? kDecThreads : (g <= 4 ? decode_threads<4>() : (g <= 8 ? decode_threads<8>() : decode_threads<16>()));
   const int items = decode_items(p.s, p.w, nbmax, f32);
   const int64_t units = (int64_t)batch * p.hkv;
