@@ -174,7 +174,8 @@ def needle_recall(prob, cfg, seq, dev):
     The c3 cache carries mean-shift needles (k + 2u) and curvature needles
     (k + a u with a ~ N(0, 4): the mean is unchanged, only the spread along u
     grows).  A first-order selector (rank 0) is blind to the second kind;
-    the second-order estimate (the configured rank) and the exact masses are not.
+    the second-order estimate (the configured rank), Quest's key boxes and the
+    exact masses are not.
     """
     sels = {}
     for name, rank in (("rank%d" % cfg.rank, cfg.rank), ("rank0", 0)):
@@ -189,6 +190,9 @@ def needle_recall(prob, cfg, seq, dev):
     cobs.cobs_select_exact(cfg, prob["q"], prob["k"], prob["v"], seq, sel,
                            cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, dev))
     sels["exact_mass"] = sel.cpu()
+    cobs.cobs_select_quest(cfg, prob["q"], prob["k"], prob["v"], seq, sel,
+                           cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, dev))
+    sels["quest_box"] = sel.cpu()
     out = {}
     for name, sl in sels.items():
         hit = {"mean": [0, 0], "curvature": [0, 0]}

@@ -72,7 +72,7 @@ typedef enum {
   COBS_OP_SELECT = 1, /* cobs_select            */
   COBS_OP_DECODE = 2, /* cobs_sparse_decode     */
   COBS_OP_STEP = 3,   /* cobs_decode_step       */
-  COBS_OP_SELECT_EXACT = 4 /* cobs_select_exact  */
+  COBS_OP_SELECT_EXACT = 4 /* cobs_select_exact, cobs_select_quest */
 } cobs_op_t;
 
 /* Problem description shared by every call (host struct, passed by pointer). */
@@ -182,6 +182,17 @@ cobs_status_t cobs_select_exact(const cobs_config_t* cfg, const float* q, const 
 cobs_status_t cobs_sparse_decode(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
                                  const int32_t* seq_lens, const int32_t* sel, float* out,
                                  float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* Quest block selection, an alternate selector for diagnostics (Sec. 6.4):
+ * per block the element-wise minimum and maximum of its keys (eq.
+ * rw-quest-box), per query head the box's largest inner product with the query
+ * (eq. rw-quest-score), and c times that bound in place of l_b^g in the group
+ * score; candidates, top-s and outputs as for cobs_select.  Reads every key
+ * once.  Arguments and workspace (COBS_OP_SELECT_EXACT) as for
+ * cobs_select_exact; bf16 keys only.                                           */
+cobs_status_t cobs_select_quest(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
+                                size_t ws_bytes, void* stream);
 
 /* The decode attention split into the two branches a caller-side gate
  * combines (the selection and sliding-window branches of the NSA layout the

@@ -272,6 +272,28 @@ def osa_group_scores(q, K, T, L, c):
     return group_scores(exact_block_log_mass(q, K, T, L, c))
 
 
+def quest_block_scores(q, K, T, L):
+    """Quest's box score of eq. (rw-quest-score): per block the element-wise
+    minimum and maximum of its keys (eq. rw-quest-box), and per query head the
+    largest inner product a point of that box attains.  [NB, G]."""
+    q = np.asarray(q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    nb = num_blocks(T, L)
+    out = np.zeros((nb, q.shape[0]))
+    for b in range(nb):
+        Kb = K[b * L:min(b * L + L, T)]
+        kmin, kmax = Kb.min(axis=0), Kb.max(axis=0)
+        out[b] = np.maximum(q * kmin[None, :], q * kmax[None, :]).sum(axis=1)
+    return out
+
+
+def quest_group_scores(q, K, T, L, c):
+    """Reading for a GQA group: c times the box score stands in for ln m_b^g in
+    the group score of eq. (gqa-secondorder) (log form, as for the other
+    selectors)."""
+    return group_scores(c * quest_block_scores(q, K, T, L))
+
+
 def block_mixture(q1, K, V, T, L, c):
     """Block probabilities P_b and value centroids v^c_b of one query head.
 

@@ -49,6 +49,7 @@ _SIGS = {
                                               ctypes.c_size_t, _P]),
     "cobs_select": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_select_exact": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "cobs_select_quest": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_sparse_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_sparse_decode_branches": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_decode_step": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
@@ -174,6 +175,14 @@ def cobs_select_exact(cfg, q, k, v, seq_lens, sel, ws, scores=None, block_table=
                       stream=None):
     kv = _kv(k, v, block_table, num_pages)
     _check(lib().cobs_select_exact(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
+                                   _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws),
+                                   ws.numel() * ws.element_size(), _stream(stream, q)))
+
+
+def cobs_select_quest(cfg, q, k, v, seq_lens, sel, ws, scores=None, block_table=None, num_pages=0,
+                      stream=None):
+    kv = _kv(k, v, block_table, num_pages)
+    _check(lib().cobs_select_quest(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
                                    _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws),
                                    ws.numel() * ws.element_size(), _stream(stream, q)))
 

@@ -192,7 +192,7 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
 
 cobs_status_t run_select_exact(const Derived& v, const float* q, const cobs_kv_t* kv,
                                const int32_t* seq_lens, int32_t* sel, float* scores, uint8_t* ws,
-                               hipStream_t st) {
+                               hipStream_t st, bool quest) {
   SelectParams p;
   p.q = q;
   p.rec = nullptr;
@@ -217,7 +217,7 @@ cobs_status_t run_select_exact(const Derived& v, const float* q, const cobs_kv_t
   p.bpw = 0;
   p.c = v.c;
   p.lay = v.lay;
-  return hip_status(launch_select_exact(p, v.d, v.G, v.B, st));
+  return hip_status(launch_select_exact(p, v.d, v.G, v.B, st, quest));
 }
 
 // `out_w` non-null: the selection branch goes to out/lse and the window branch
@@ -332,9 +332,10 @@ cobs_status_t cobs_select(const cobs_config_t* cfg, const float* q, const void* 
                     static_cast<hipStream_t>(stream));
 }
 
-cobs_status_t cobs_select_exact(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
-                                const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
-                                size_t ws_bytes, void* stream) {
+namespace {
+cobs_status_t dense_key_select(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                               const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
+                               size_t ws_bytes, void* stream, bool quest) {
   cobs_status_t s = check_config(cfg);
   if (s != COBS_OK) return s;
   const Derived v = derive(cfg);
@@ -343,7 +344,20 @@ cobs_status_t cobs_select_exact(const cobs_config_t* cfg, const float* q, const 
   if (!q || !seq_lens || !sel) return COBS_ERR_INVALID_ARG;
   if ((s = check_ws(ws, ws_bytes, v.selx_bytes)) != COBS_OK) return s;
   return run_select_exact(v, q, kv, seq_lens, sel, scores, static_cast<uint8_t*>(ws),
-                          static_cast<hipStream_t>(stream));
+                          static_cast<hipStream_t>(stream), quest);
+}
+}  // namespace
+
+cobs_status_t cobs_select_exact(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
+                                size_t ws_bytes, void* stream) {
+  return dense_key_select(cfg, q, kv, seq_lens, sel, scores, ws, ws_bytes, stream, false);
+}
+
+cobs_status_t cobs_select_quest(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
+                                size_t ws_bytes, void* stream) {
+  return dense_key_select(cfg, q, kv, seq_lens, sel, scores, ws, ws_bytes, stream, true);
 }
 
 cobs_status_t cobs_sparse_decode(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,

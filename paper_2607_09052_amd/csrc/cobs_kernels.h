@@ -65,8 +65,9 @@ bool select_on_matrix_cores(int mdt, int fdt);
 int select_min_bpw(int mdt, int fdt);
 hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int nbmax, hipStream_t st);
 bool select_refreshes(int r, bool kv_f32);
-// Exact-mass selector: the SelectParams of the selector with `kv` set (bf16 keys).
-hipError_t launch_select_exact(SelectParams p, int d, int g, int batch, hipStream_t st);
+// Dense-key selectors (exact masses; `quest`: Quest boxes): the SelectParams of
+// the selector with `kv` set (bf16 keys).
+hipError_t launch_select_exact(SelectParams p, int d, int g, int batch, hipStream_t st, bool quest);
 int select_exact_min_bpw();
 int decode_max_wg(int s, int w, int nbmax, bool f32);
 

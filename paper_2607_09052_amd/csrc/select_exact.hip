@@ -155,12 +155,133 @@ static SelectKernel exact_kernel_d(int g) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Quest box selector (eq. rw-quest-box, eq. rw-quest-score), an alternate
+// selector for diagnostics.  Per block the element-wise minimum and maximum of
+// its keys bound the box of its keys; per query head the largest inner product
+// a point of the box attains, sum_i max(q_i kmin_i, q_i kmax_i), times c stands
+// in for ln m_b^g in the group score.  One wave per block: lane l owns channels
+// [l D/64, (l+1) D/64) and reads them from every row (rows past n re-read row
+// n - 1, which leaves the minimum and maximum unchanged); the head sums are
+// wave reductions.
+// ---------------------------------------------------------------------------
+template <int D, int G>
+__device__ __forceinline__ void select_quest_task(const SelectParams& p, int b, int h, int chunk, char* pool) {
+  constexpr int CPL = D / 64;                   // channels per lane
+  float (*gm)[G] = reinterpret_cast<float (*)[G]>(pool);
+  float (*gs)[G] = reinterpret_cast<float (*)[G]>(pool + 4 * G * 4);
+  __shared__ int s_last;
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int unit = b * p.hkv + h;
+  const int T = clamp_len(p.seq_lens[b], p.tmax);
+  const int nb = (T + kL - 1) / kL;
+  const int blk_lo = chunk * p.bpw, blk_hi = min(nb, blk_lo + p.bpw);
+  const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;
+  const char* kbase = static_cast<const char*>(p.kv.k);
+
+  float qv[G][CPL];                             // c q_g on this lane's channels
+#pragma unroll
+  for (int g = 0; g < G; ++g)
+#pragma unroll
+    for (int e = 0; e < CPL; ++e) qv[g][e] = p.q[((int64_t)b * p.hq + h * G + g) * D + lane * CPL + e] * p.c;
+
+  float run_m[G], run_s[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) { run_m[g] = -INFINITY; run_s[g] = 0.0f; }
+  for (int blk = blk_lo + wave; blk < blk_hi; blk += kExactBlocksPerPass) {
+    const int n = min(kL, T - blk * kL);
+    const int64_t t0 = kv_offset(p.kv, b, h, blk * kL);
+    float l[G];
+    if (t0 >= 0) {
+      float mn[CPL], mx[CPL];
+#pragma unroll
+      for (int e = 0; e < CPL; ++e) { mn[e] = INFINITY; mx[e] = -INFINITY; }
+      const char* col = kbase + t0 * 2 + lane * CPL * 2;
+#pragma unroll
+      for (int r0 = 0; r0 < kL; r0 += 16) {
+        uint32_t w[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const char* rp = col + (int64_t)min(r0 + r, n - 1) * rs * 2;
+          w[r] = (CPL == 2) ? *reinterpret_cast<const uint32_t*>(rp) : (uint32_t)*reinterpret_cast<const uint16_t*>(rp);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float x0 = bf16_lo(w[r]);
+          mn[0] = fminf(mn[0], x0);
+          mx[0] = fmaxf(mx[0], x0);
+          if constexpr (CPL == 2) {
+            const float x1 = bf16_hi(w[r]);
+            mn[1] = fminf(mn[1], x1);
+            mx[1] = fmaxf(mx[1], x1);
+          }
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float a = 0.0f;
+#pragma unroll
+        for (int e = 0; e < CPL; ++e) a += fmaxf(qv[g][e] * mn[e], qv[g][e] * mx[e]);
+        l[g] = wave_sum(a);
+      }
+    } else {
+#pragma unroll
+      for (int g = 0; g < G; ++g) l[g] = -INFINITY;
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) st_agent(&p.ell[((int64_t)unit * p.nbmax + blk) * G + g], l[g]);
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) lse_merge(run_m[g], run_s[g], l[g], 1.0f);
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) { gm[wave][g] = run_m[g]; gs[wave][g] = run_s[g]; }
+  }
+  __syncthreads();
+  if (tid < G) {
+    float m = -INFINITY, s = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) lse_merge(m, s, gm[k][tid], gs[k][tid]);
+    float* pp = p.part + (((int64_t)unit * p.nch + chunk) * G + tid) * 2;
+    st_agent(&pp[0], m);
+    st_agent(&pp[1], s);
+  }
+  if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
+  FinishLds& fin = *reinterpret_cast<FinishLds*>(pool);
+  const int nc = (max(0, T - p.w) + kL - 1) / kL;
+  if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
+  else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
+  else finish_select<G, kMaxBlocksPerSeq / kSelThreads>(p, unit, T, fin);
+}
+
+template <int D, int G>
+__global__ __launch_bounds__(kSelThreads) void select_quest_kernel(SelectParams p) {
+  __shared__ __align__(16) char pool[select_exact_lds<G>()];
+  select_quest_task<D, G>(p, blockIdx.z, blockIdx.y, blockIdx.x, pool);
+}
+
+template <int D>
+static SelectKernel quest_kernel_d(int g) {
+  switch (g) {
+    case 1: return select_quest_kernel<D, 1>;
+    case 2: return select_quest_kernel<D, 2>;
+    case 4: return select_quest_kernel<D, 4>;
+    case 8: return select_quest_kernel<D, 8>;
+    default: return select_quest_kernel<D, 16>;
+  }
+}
+
 int select_exact_min_bpw() { return kExactBlocksPerPass; }
 
-// Chunks of a multiple of four blocks, sized so that the grid fills the chip's
-// resident workgroup slots in one round.
-hipError_t launch_select_exact(SelectParams p, int d, int g, int batch, hipStream_t st) {
-  const SelectKernel k = (d == 128) ? exact_kernel_d<128>(g) : exact_kernel_d<64>(g);
+// Both dense-key selectors (exact masses, or `quest` boxes): chunks of a
+// multiple of four blocks, sized so that the grid fills the chip's resident
+// workgroup slots in one round.
+hipError_t launch_select_exact(SelectParams p, int d, int g, int batch, hipStream_t st, bool quest) {
+  const SelectKernel k = quest ? ((d == 128) ? quest_kernel_d<128>(g) : quest_kernel_d<64>(g))
+                               : ((d == 128) ? exact_kernel_d<128>(g) : exact_kernel_d<64>(g));
   const int base = kExactBlocksPerPass;
   const int64_t units = (int64_t)batch * p.hkv;
   const int64_t slots = (int64_t)resident_workgroups(reinterpret_cast<const void*>(k), kSelThreads) * device_cus();

@@ -24,7 +24,7 @@ def _declared_functions():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared_functions()
-    assert len(declared) == 10, declared
+    assert len(declared) == 11, declared
     lib = cobs.lib()
     for name in declared:
         assert hasattr(lib, name), name
@@ -111,6 +111,10 @@ def test_null_and_workspace_errors_on_host():
     assert lib.cobs_select_exact(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, None, None, fake,
                                  1 << 30, None) == 1
     assert lib.cobs_select_exact(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, fake, None, fake,
+                                 16, None) == 3
+    assert lib.cobs_select_quest(ctypes.byref(cfg32), fake, ctypes.byref(kv), fake, fake, None, fake,
+                                 1 << 30, None) == 2
+    assert lib.cobs_select_quest(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, fake, None, fake,
                                  16, None) == 3
     # branch outputs: fp32 K/V unsupported, a missing branch output rejected
     assert lib.cobs_sparse_decode_branches(ctypes.byref(cfg32), fake, ctypes.byref(kv), fake, fake, fake, None,

@@ -206,6 +206,38 @@ def test_select_exact_matches_oracle(d, G, s, w):
     assert torch.equal(sel, sel2) and torch.equal(scores, scores2)
 
 
+@pytest.mark.parametrize("d,G,s,w", [(128, 4, 8, 256), (128, 8, 20, 64), (64, 1, 5, 0), (128, 16, 12, 300),
+                                      (64, 4, 6, 64)])
+def test_select_quest_matches_oracle(d, G, s, w):
+    """Quest boxes (eq. rw-quest-box, eq. rw-quest-score) from every key, c times the
+    bound in the group score: against the oracle on the same bf16 keys."""
+    Hkv, Tmax = 2, 4096
+    seq = np.array([4096, 2500, 300, 65], np.int32)
+    B = len(seq)
+    prob = _decode_problem(d, G, "bf16", seq, Hkv, Tmax, seed=d + 7 * G + s)
+    cfg = _cfg(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=Tmax,
+               budget=s, window=w)
+    q, k, v = prob["q"], prob["k"], prob["v"]
+    seq_d = torch.from_numpy(seq).to(DEV)
+    sel = torch.full((B, Hkv, max(s, 1)), -7, dtype=torch.int32, device=DEV)
+    scores = torch.empty((B, Hkv, cfg.num_blocks), dtype=torch.float32, device=DEV)
+    ws = cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, DEV)
+    say(f"select_quest d={d} G={G} s={s} w={w}")
+    cobs.cobs_select_quest(cfg, q.to(DEV), k.to(DEV), v.to(DEV), seq_d, sel, ws, scores=scores)
+    sync()
+    sel_h, sc_h = sel.cpu().numpy(), scores.cpu().numpy()
+    for b in range(B):
+        T = int(seq[b])
+        nc = M.candidate_count(T, 64, w)
+        for h in range(Hkv):
+            sigma = M.quest_group_scores(q[b, h * G:(h + 1) * G].double().numpy(), f64(k[b, h]), T, 64, cfg.scale)
+            got = sc_h[b, h]
+            assert np.all(np.abs(got[:nc] - sigma[:nc]) <= SIGMA_TOL), np.max(np.abs(got[:nc] - sigma[:nc]))
+            assert np.all(np.isneginf(got[nc:]))
+            if s > 0:
+                check_selection(sel_h[b, h, :s], sigma, nc, s)
+
+
 def test_select_exact_paged_matches_contiguous():
     d, G, Hkv, Tmax, s, w = 128, 4, 2, 2048, 6, 200
     seq = np.array([2048, 1500], np.int32)

@@ -372,3 +372,30 @@ def test_branch_outputs_merge_to_the_union_attention():
     # empty selection branch
     o_s, l_s, _, _ = M.branch_attention(q, K, V, T, L, 100, [-1], c)
     assert np.all(o_s == 0) and np.all(np.isneginf(l_s))
+
+
+def test_quest_box_score_bounds_and_forms():
+    """Box score (eq. rw-quest-score): an upper bound of every key's inner product
+    in the block, exact for a one-token block, equal to its second printed form,
+    and a bound the box's own corners attain."""
+    rng = np.random.default_rng(92)
+    T, L, d, G = 200, 64, 16, 3
+    K, q = rng.standard_normal((T, d)), rng.standard_normal((G, d))
+    sb = M.quest_block_scores(q, K, T, L)
+    for b in range(M.num_blocks(T, L)):
+        Kb = K[b * L:min(b * L + L, T)]
+        assert np.all(sb[b] >= (q @ Kb.T).max(axis=1) - 1e-12)
+        kmin, kmax = Kb.min(0), Kb.max(0)
+        second = (np.maximum(q, 0) * kmax + np.minimum(q, 0) * kmin).sum(1)
+        np.testing.assert_allclose(sb[b], second, rtol=0, atol=1e-12)
+        corner = np.where(q > 0, kmax, kmin)            # the maximising corner, per head
+        np.testing.assert_allclose(sb[b], (q * corner).sum(1), rtol=0, atol=1e-12)
+    # a block of one token: the bound is that token's inner product
+    one = M.quest_block_scores(q, K, 1, L)
+    np.testing.assert_allclose(one[0], q @ K[0], rtol=0, atol=1e-12)
+    # brute force over the box's corners on a tiny case
+    Kt, qt = rng.standard_normal((5, 3)), rng.standard_normal((1, 3))
+    lo, hi = Kt.min(0), Kt.max(0)
+    corners = np.array([[lo[0] if a else hi[0], lo[1] if b_ else hi[1], lo[2] if c_ else hi[2]]
+                        for a in (0, 1) for b_ in (0, 1) for c_ in (0, 1)])
+    np.testing.assert_allclose(M.quest_block_scores(qt, Kt, 5, 8)[0, 0], (corners @ qt[0]).max(), atol=1e-12)
