@@ -10,6 +10,7 @@ namespace cobs {
 typedef void (*SelectKernel)(SelectParams);
 SelectKernel select_valu_kernel_for(const SelectParams& p, int d, int g);
 SelectKernel select_mfma_kernel_for(const SelectParams& p, int d, int g);
+SelectKernel select_refresh_kernel_for(const SelectParams& p, int d, int g);
 
 bool select_on_matrix_cores(int mdt, int fdt) { return mdt != DT_F32 && fdt != DT_F32; }
 
@@ -21,7 +22,8 @@ int select_min_bpw(int mdt, int fdt) { return select_on_matrix_cores(mdt, fdt) ?
 
 hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st) {
   const bool mfma = select_on_matrix_cores(p.mdt, p.fdt);
-  const SelectKernel k = mfma ? select_mfma_kernel_for(p, d, g) : select_valu_kernel_for(p, d, g);
+  const SelectKernel k = p.tail_rec ? select_refresh_kernel_for(p, d, g)
+                                    : (mfma ? select_mfma_kernel_for(p, d, g) : select_valu_kernel_for(p, d, g));
   if (!k) return hipErrorInvalidValue;
   const int base = select_min_bpw(p.mdt, p.fdt);
   const int64_t units = (int64_t)batch * p.hkv;

@@ -7,11 +7,6 @@ typedef void (*SelectKernel)(SelectParams);
 
 template <int D, int G, int MDT, int FDT>
 static SelectKernel pick(const SelectParams& p) {
-  if (p.tail_rec) {
-    if (p.r > 4) return nullptr;
-    if constexpr (select_refresh_capped<D, G, MDT, FDT>()) return select_refresh_kernel<D, G, MDT, FDT>;
-    else return select_refresh_kernel_wide<D, G, MDT, FDT>;
-  }
   return (p.r <= 4) ? select_mfma_kernel<D, G, 4, MDT, FDT> : select_mfma_kernel<D, G, kMaxRank, MDT, FDT>;
 }
 
