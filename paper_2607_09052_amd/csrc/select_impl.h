@@ -66,12 +66,23 @@ __device__ __forceinline__ void unpack_elems(const uint32_t* w, float* x) {
   }
 }
 
-// E2M1 slices of 4 elements are 2 bytes: load them as the low half of a word.
+// Lane ln of the 16 sharing a block holds elements [4 ln, 4 ln + 4) and, for
+// EPL = 8 (d = 128), also [64 + 4 ln, 64 + 4 ln + 4): each load instruction of
+// the 16 lanes then reads one contiguous run of the vector (256 bytes of an
+// fp32 vector instead of every other 16 bytes of 512).  The words come out in
+// element order: E2M1 halves are 2 bytes each, packed into one word.
 template <int DT, int EPL>
 __device__ __forceinline__ void load_slice(const uint8_t* vec, int ln, uint32_t* w) {
-  constexpr int B = elem_bytes<DT>(EPL);
-  if constexpr (B >= 4) load_words<B / 4>(vec + ln * B, w);
-  else w[0] = *reinterpret_cast<const uint16_t*>(vec + ln * B);
+  static_assert(EPL == 4 || EPL == 8, "d = 64 or 128");
+  constexpr int B = elem_bytes<DT>(4);                 // bytes of 4 elements
+  constexpr int H = elem_bytes<DT>(64);                // bytes of the first half at d = 128
+  if constexpr (DT == DT_E2M1) {
+    const uint32_t lo = *reinterpret_cast<const uint16_t*>(vec + ln * B);
+    w[0] = (EPL == 8) ? (lo | ((uint32_t)*reinterpret_cast<const uint16_t*>(vec + H + ln * B) << 16)) : lo;
+  } else {
+    load_words<B / 4>(vec + ln * B, w);
+    if constexpr (EPL == 8) load_words<B / 4>(vec + H + ln * B, w + B / 4);
+  }
 }
 
 template <int DT, int EPL>
@@ -342,9 +353,10 @@ __device__ __forceinline__ void finish_select(const SelectParams& p, int unit, i
 // ---------------------------------------------------------------------------
 // Vector-ALU scorer (fp32 descriptors, two flops per stored byte per head).
 //
-// 16 lanes share one block, each lane owning d/16 contiguous elements of every
-// stored vector; the lanes' partial dot products for the G query heads are
-// combined by a 16-lane DPP reduction.
+// 16 lanes share one block, each lane owning d/16 elements of every stored
+// vector (one run of 4 at d = 64, two at d = 128: see load_slice); the lanes'
+// partial dot products for the G query heads are combined by a 16-lane DPP
+// reduction.
 // ---------------------------------------------------------------------------
 template <int G>
 constexpr size_t select_valu_lds() { return select_pool_bytes<2 * 16 * G * 4>(); }
@@ -398,10 +410,11 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
   float qv[G][EPL];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    const float4* qg = reinterpret_cast<const float4*>(p.q + ((int64_t)b * p.hq + h * G + g) * D + ln * EPL);
+    // the elements of the lane's slices (load_slice): 4 ln .., and 64 + 4 ln ..
+    const float* qrow_g = p.q + ((int64_t)b * p.hq + h * G + g) * D + 4 * ln;
 #pragma unroll
     for (int e = 0; e < EPL / 4; ++e) {
-      const float4 x = qg[e];
+      const float4 x = *reinterpret_cast<const float4*>(qrow_g + 64 * e);
       qv[g][4 * e] = x.x * p.c; qv[g][4 * e + 1] = x.y * p.c;
       qv[g][4 * e + 2] = x.z * p.c; qv[g][4 * e + 3] = x.w * p.c;
     }
