@@ -15,7 +15,7 @@ Readings of passages the paper leaves open (kept identical in the HIP path):
   * Top-s ties go to the lower block index; the set is returned ascending,
     padded with -1.
   * A partial block (n_b < L) stores zero factors; its factors are computed
-    when it fills (Sec. 5.6, "recomputed once per block ... as the block fills").
+    when it fills (Sec. 5.6: a block's statistics are rebuilt as it fills).
   * The sign of a stored eigenvector is chosen so that its largest-magnitude
     entry (lowest index on ties) is positive; the score does not depend on it.
 
