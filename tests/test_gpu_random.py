@@ -2,7 +2,12 @@
 heads, group size, head dim, rank, budget, window, descriptor and K/V types,
 ragged lengths including T < L and T <= w), each checked end to end against the
 oracle: the selector on the GPU's own records, the attention on the GPU's
-selection, and the decode step against the three entry points."""
+selection, and the decode step against the three entry points.  A second draw
+takes contexts of up to 64k tokens (many selector chunks and decode workgroups
+per unit).  COBS_RANDOM_SEEDS sets the number of seeds of each draw (default 24
+and 6) for a longer sweep."""
+
+import os
 
 import numpy as np
 import pytest
@@ -38,12 +43,37 @@ def _draw(seed):
     return dict(G=G, d=d, Hkv=Hkv, B=B, tmax=tmax, kv=kv, md=md, fd=fd, r=r, s=s, w=w, seq=seq)
 
 
-@pytest.mark.parametrize("seed", list(range(24)))
+def _draw_long(seed):
+    """As _draw, with T_max up to 1024 blocks, budgets up to 119 and windows up to 3000."""
+    c = _draw(seed)
+    rng = np.random.default_rng(seed + 777)
+    tmax = 64 * int(rng.integers(40, 1025))
+    seq = rng.integers(1, tmax + 1, size=c["B"]).astype(np.int32)
+    seq[0] = tmax
+    if c["B"] > 1:
+        seq[1] = int(rng.integers(1, 64))
+    c.update(tmax=tmax, seq=seq, s=int(rng.integers(0, 120)),
+             w=int(rng.choice([0, 512, 1024, int(rng.integers(1, 3000))])))
+    return c
+
+
+_N = os.environ.get("COBS_RANDOM_SEEDS")
+
+
+@pytest.mark.parametrize("seed", list(range(int(_N) if _N else 24)))
 def test_random_configuration_end_to_end(seed):
-    c = _draw(1000 + seed)
+    _check(_draw(1000 + seed), 2000 + seed, f"random config {seed}")
+
+
+@pytest.mark.parametrize("seed", list(range(int(_N) if _N else 6)))
+def test_random_long_context_end_to_end(seed):
+    _check(_draw_long(3000 + seed), 4000 + seed, f"random long-context config {seed}")
+
+
+def _check(c, data_seed, tag):
     G, d, Hkv, B, tmax = c["G"], c["d"], c["Hkv"], c["B"], c["tmax"]
-    say(f"random config {seed}: {c}")
-    prob = synth.make_problem("c2", seed=2000 + seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"])
+    say(f"{tag}: {c}")
+    prob = synth.make_problem("c2", seed=data_seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"])
     cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
                       rank=c["r"], budget=c["s"], window=c["w"], kv_dtype=c["kv"], mean_dtype=c["md"],
                       factor_dtype=c["fd"])
