@@ -4,8 +4,9 @@ ragged lengths including T < L and T <= w), each checked end to end against the
 oracle: the selector on the GPU's own records, the attention on the GPU's
 selection, and the decode step against the three entry points.  A second draw
 takes contexts of up to 64k tokens (many selector chunks and decode workgroups
-per unit).  COBS_RANDOM_SEEDS sets the number of seeds of each draw (default 24
-and 6) for a longer sweep."""
+per unit), and a third checks the exact-mass and Quest selectors and the
+two-branch decode.  COBS_RANDOM_SEEDS sets the number of seeds of each draw
+(default 24, 6 and 8) for a longer sweep."""
 
 import os
 
@@ -117,3 +118,53 @@ def _check(c, data_seed, tag):
     if c["s"] > 0:
         assert torch.equal(sel1, sel_c)
     assert torch.equal(out1, out) and torch.equal(lse1, lse)
+
+
+@pytest.mark.parametrize("seed", list(range(int(_N) if _N else 8)))
+def test_random_diagnostic_entry_points(seed):
+    """The exact-mass and Quest selectors and the two-branch decode on random
+    bf16-cache draws: scores and selections against the oracle's, each branch
+    against the oracle's attention on its own token set (on the exact-mass
+    selection the GPU made)."""
+    c = _draw(5000 + seed)
+    c["kv"] = "bf16"
+    G, d, Hkv, B, tmax, s, w = c["G"], c["d"], c["Hkv"], c["B"], c["tmax"], c["s"], c["w"]
+    say(f"random diagnostic config {seed}: {c}")
+    prob = synth.make_problem("c2", seed=6000 + seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype="bf16")
+    cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
+                      rank=c["r"], budget=s, window=w, kv_dtype="bf16")
+    q, k, v = prob["q"], prob["k"], prob["v"]
+    qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
+    seq_d = torch.from_numpy(c["seq"]).to(DEV)
+    ws = cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, DEV)
+    outs = {}
+    for name, fn in (("exact", cobs.cobs_select_exact), ("quest", cobs.cobs_select_quest)):
+        sel = torch.full((B, Hkv, max(s, 1)), -7, dtype=torch.int32, device=DEV)
+        scores = torch.empty((B, Hkv, cfg.num_blocks), dtype=torch.float32, device=DEV)
+        fn(cfg, qd, kd, vd, seq_d, sel, ws, scores=scores)
+        outs[name] = (sel, scores)
+    sel_e = outs["exact"][0][:, :, :s].contiguous()
+    shp = (B, G * Hkv, d)
+    o_s, o_w = (torch.empty(shp, dtype=torch.float32, device=DEV) for _ in range(2))
+    l_s, l_w = (torch.empty(shp[:2], dtype=torch.float32, device=DEV) for _ in range(2))
+    cobs.cobs_sparse_decode_branches(cfg, qd, kd, vd, seq_d, sel_e, o_s, o_w,
+                                     cobs.new_workspace(cfg, cobs.OP_DECODE, DEV), lse_sel=l_s, lse_win=l_w)
+    sync()
+    hs, hw, ls, lw = o_s.cpu().numpy(), o_w.cpu().numpy(), l_s.cpu().numpy(), l_w.cpu().numpy()
+    oracles = {"exact": M.osa_group_scores, "quest": M.quest_group_scores}
+    for b in range(B):
+        T = int(c["seq"][b])
+        nc = M.candidate_count(T, 64, w)
+        for h in range(Hkv):
+            gs = slice(h * G, (h + 1) * G)
+            qg, Kg = q[b, gs].double().numpy(), f64(k[b, h])
+            for name, (sel, scores) in outs.items():
+                sigma = oracles[name](qg, Kg, T, 64, cfg.scale)
+                got = scores[b, h].cpu().numpy()
+                assert np.all(np.abs(got[:nc] - sigma[:nc]) <= SIGMA_TOL), (name, b, h)
+                assert np.all(np.isneginf(got[nc:])), (name, b, h)
+                if s > 0:
+                    check_selection(sel[b, h, :s].cpu().numpy(), sigma, nc, s)
+            ref = M.branch_attention(qg, Kg, f64(v[b, h]), T, 64, w, sel_e[b, h].cpu().numpy(), cfg.scale)
+            check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16")
+            check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16")
