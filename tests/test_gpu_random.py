@@ -4,9 +4,10 @@ ragged lengths including T < L and T <= w), each checked end to end against the
 oracle: the selector on the GPU's own records, the attention on the GPU's
 selection, and the decode step against the three entry points.  A second draw
 takes contexts of up to 64k tokens (many selector chunks and decode workgroups
-per unit), and a third checks the exact-mass and Quest selectors and the
-two-branch decode.  COBS_RANDOM_SEEDS sets the number of seeds of each draw
-(default 24, 6 and 8) for a longer sweep."""
+per unit), a third checks the exact-mass and Quest selectors and the two-branch
+decode, and a fourth checks that a paged cache is bitwise the contiguous one.
+COBS_RANDOM_SEEDS sets the number of seeds of each draw (default 24, 6, 8 and 6)
+for a longer sweep."""
 
 import os
 
@@ -168,3 +169,72 @@ def test_random_diagnostic_entry_points(seed):
             ref = M.branch_attention(qg, Kg, f64(v[b, h]), T, 64, w, sel_e[b, h].cpu().numpy(), cfg.scale)
             check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16")
             check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16")
+
+
+@pytest.mark.parametrize("seed", list(range(int(_N) if _N else 6)))
+def test_random_paged_cache_is_bitwise_contiguous(seed):
+    """The same cache stored as pages of one block in a shuffled pool (with
+    unused pages) gives bitwise the contiguous results: block statistics,
+    attention, the decode step and, for bf16 caches, the exact-mass selector and
+    the two-branch decode."""
+    c = _draw(7000 + seed)
+    G, d, Hkv, B, tmax, s, w = c["G"], c["d"], c["Hkv"], c["B"], c["tmax"], c["s"], c["w"]
+    say(f"random paged config {seed}: {c}")
+    prob = synth.make_problem("c2", seed=8000 + seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"])
+    cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
+                      rank=c["r"], budget=s, window=w, kv_dtype=c["kv"], mean_dtype=c["md"],
+                      factor_dtype=c["fd"])
+    q, k, v = prob["q"].to(DEV), prob["k"].to(DEV), prob["v"].to(DEV)
+    nbm = tmax // 64
+    pages = B * nbm + 3
+    perm = torch.randperm(pages, generator=torch.Generator().manual_seed(9000 + seed))[:B * nbm]
+    table = perm.view(B, nbm).to(torch.int32)
+    kp = torch.zeros((pages, Hkv, 64, d), dtype=k.dtype, device=DEV)
+    vp = torch.zeros_like(kp)
+    for b in range(B):
+        for j in range(nbm):
+            kp[table[b, j]] = k[b, :, j * 64:(j + 1) * 64]
+            vp[table[b, j]] = v[b, :, j * 64:(j + 1) * 64]
+    tab = table.to(DEV)
+    seq_d = torch.from_numpy(c["seq"]).to(DEV)
+
+    def run(paged):
+        kw = dict(block_table=tab, num_pages=pages) if paged else {}
+        kk, vv = (kp, vp) if paged else (k, v)
+        res = {}
+        rec = cobs.new_summaries(cfg, DEV)
+        cobs.cobs_build_block_stats(cfg, kk, vv, seq_d, rec, **kw)
+        res["rec"] = rec
+        sel = synth.make_selection(B, Hkv, c["seq"], 64, w, max(s, 1), seed=seed, fill="random")[:, :, :s]
+        sel = sel.contiguous().to(DEV)
+        res["out"] = torch.empty((B, G * Hkv, d), dtype=torch.float32, device=DEV)
+        res["lse"] = torch.empty((B, G * Hkv), dtype=torch.float32, device=DEV)
+        cobs.cobs_sparse_decode(cfg, q, kk, vv, seq_d, sel, res["out"], cobs.new_workspace(cfg, cobs.OP_DECODE, DEV),
+                                lse=res["lse"], **kw)
+        res["rec1"] = rec.clone()
+        res["out1"], res["lse1"] = torch.empty_like(res["out"]), torch.empty_like(res["lse"])
+        res["sel1"] = torch.empty((B, Hkv, max(s, 1)), dtype=torch.int32, device=DEV)
+        cobs.cobs_decode_step(cfg, q, kk, vv, seq_d, res["rec1"], res["out1"],
+                              cobs.new_workspace(cfg, cobs.OP_STEP, DEV), sel=res["sel1"] if s > 0 else None,
+                              lse=res["lse1"], **kw)
+        if c["kv"] == "bf16":
+            res["sx"] = torch.full((B, Hkv, max(s, 1)), -7, dtype=torch.int32, device=DEV)
+            res["scx"] = torch.empty((B, Hkv, cfg.num_blocks), dtype=torch.float32, device=DEV)
+            cobs.cobs_select_exact(cfg, q, kk, vv, seq_d, res["sx"], cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, DEV),
+                                   scores=res["scx"], **kw)
+            for nm in ("os", "ow"):
+                res[nm] = torch.empty_like(res["out"])
+            for nm in ("ls", "lw"):
+                res[nm] = torch.empty_like(res["lse"])
+            cobs.cobs_sparse_decode_branches(cfg, q, kk, vv, seq_d, sel, res["os"], res["ow"],
+                                             cobs.new_workspace(cfg, cobs.OP_DECODE, DEV), lse_sel=res["ls"],
+                                             lse_win=res["lw"], **kw)
+        sync()
+        return res
+
+    a, b_ = run(False), run(True)
+    assert sorted(a) == sorted(b_)
+    for key in a:
+        if key == "sel1" and s == 0:
+            continue
+        assert torch.equal(a[key], b_[key]), key
