@@ -40,7 +40,10 @@ def f64(t):
 
 
 def oracle_select(rec_unit, q_unit, T, cfg):
-    """Oracle sigma, candidate count and selection of one unit from record bytes."""
+    """Oracle sigma, candidate count and selection of one unit from record bytes.
+    A row with no tokens has no blocks, no candidates and no selection."""
+    if T <= 0:
+        return np.zeros(0), 0, []
     counts, means, factors = R.decode(rec_unit, cfg.head_dim, cfg.rank, cfg.mean_dtype, cfg.factor_dtype)
     nb = M.num_blocks(T, cfg.block_size)
     ell = M.log_mass_estimate(q_unit, counts[:nb], means[:nb], factors[:nb], cfg.scale)

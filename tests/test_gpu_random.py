@@ -6,8 +6,8 @@ selection, and the decode step against the three entry points.  A second draw
 takes contexts of up to 64k tokens (many selector chunks and decode workgroups
 per unit), a third checks the exact-mass and Quest selectors and the two-branch
 decode, and a fourth checks that a paged cache is bitwise the contiguous one.
-COBS_RANDOM_SEEDS sets the number of seeds of each draw (default 24, 6, 8 and 6)
-for a longer sweep."""
+A fifth puts rows of length 0 beside the others.  COBS_RANDOM_SEEDS sets the
+number of seeds of each draw (default 24, 6, 8, 6 and 6) for a longer sweep."""
 
 import os
 
@@ -72,6 +72,20 @@ def test_random_long_context_end_to_end(seed):
     _check(_draw_long(3000 + seed), 4000 + seed, f"random long-context config {seed}")
 
 
+@pytest.mark.parametrize("seed", list(range(int(_N) if _N else 6)))
+def test_random_configuration_with_empty_rows(seed):
+    """Rows of length 0 beside full and ragged ones: no candidates, all -1
+    selections, scores -inf, out 0 and lse -inf for the empty rows, no record
+    written for them, and the other rows unaffected."""
+    c = _draw(11000 + seed)
+    rng = np.random.default_rng(12000 + seed)
+    B = max(c["B"], 3)
+    seq = rng.integers(0, c["tmax"] + 1, size=B).astype(np.int32)
+    seq[0], seq[1] = c["tmax"], 0
+    c.update(B=B, seq=seq)
+    _check(c, 13000 + seed, f"random config with empty rows {seed}")
+
+
 def _check(c, data_seed, tag):
     G, d, Hkv, B, tmax = c["G"], c["d"], c["Hkv"], c["B"], c["tmax"]
     say(f"{tag}: {c}")
@@ -96,7 +110,8 @@ def _check(c, data_seed, tag):
     # the step on a copy whose newest-block records are stale
     rec1 = rec.clone()
     for b in range(B):
-        rec1[b, :, (int(c["seq"][b]) - 1) // 64] = 0
+        if int(c["seq"][b]) > 0:
+            rec1[b, :, (int(c["seq"][b]) - 1) // 64] = 0
     sel1 = torch.empty_like(sel_c)
     out1, lse1 = torch.empty_like(out), torch.empty_like(lse)
     cobs.cobs_decode_step(cfg, qd, kd, vd, seq_d, rec1, out1, cobs.new_workspace(cfg, cobs.OP_STEP, DEV),
