@@ -76,12 +76,15 @@ def test_random_long_context_end_to_end(seed):
 def test_random_configuration_with_empty_rows(seed):
     """Rows of length 0 beside full and ragged ones: no candidates, all -1
     selections, scores -inf, out 0 and lse -inf for the empty rows, no record
-    written for them, and the other rows unaffected."""
+    written for them, and the other rows unaffected.  A length above T_max
+    counts as T_max and a negative one as 0."""
     c = _draw(11000 + seed)
     rng = np.random.default_rng(12000 + seed)
-    B = max(c["B"], 3)
+    B = max(c["B"], 4)
     seq = rng.integers(0, c["tmax"] + 1, size=B).astype(np.int32)
     seq[0], seq[1] = c["tmax"], 0
+    seq[2] = c["tmax"] + int(rng.integers(1, 500))
+    seq[3] = -int(rng.integers(1, 100))
     c.update(B=B, seq=seq)
     _check(c, 13000 + seed, f"random config with empty rows {seed}")
 
@@ -109,9 +112,10 @@ def _check(c, data_seed, tag):
                             lse=lse)
     # the step on a copy whose newest-block records are stale
     rec1 = rec.clone()
+    seq_c = np.clip(c["seq"], 0, tmax)                 # lengths as the library reads them
     for b in range(B):
-        if int(c["seq"][b]) > 0:
-            rec1[b, :, (int(c["seq"][b]) - 1) // 64] = 0
+        if int(seq_c[b]) > 0:
+            rec1[b, :, (int(seq_c[b]) - 1) // 64] = 0
     sel1 = torch.empty_like(sel_c)
     out1, lse1 = torch.empty_like(out), torch.empty_like(lse)
     cobs.cobs_decode_step(cfg, qd, kd, vd, seq_d, rec1, out1, cobs.new_workspace(cfg, cobs.OP_STEP, DEV),
@@ -120,7 +124,7 @@ def _check(c, data_seed, tag):
     rec_h, sc_h = rec.cpu().numpy(), scores.cpu().numpy()
     sel_h, out_h, lse_h = sel_c.cpu().numpy(), out.cpu().numpy(), lse.cpu().numpy()
     for b in range(B):
-        T = int(c["seq"][b])
+        T = int(seq_c[b])
         for h in range(Hkv):
             gs = slice(h * G, (h + 1) * G)
             sigma, nc, _ = oracle_select(rec_h[b, h], q[b, gs].double().numpy(), T, cfg)
