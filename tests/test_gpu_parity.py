@@ -655,3 +655,65 @@ def test_decode_step_in_a_graph_matches_eager_on_every_replay():
         # eager work between replays, on the same workspace
         cobs.cobs_decode_step(cfg, q, k, v, seq, rec, out_e, ws, sel=sel_e)
         sync()
+
+
+def test_every_entry_point_in_a_graph_matches_eager_on_every_replay():
+    """Build, select, the exact-mass and Quest selectors, attention and the
+    two-branch attention enqueue kernels only on the stream they are given: one
+    graph holding all six replays them bitwise, with eager calls on the same
+    workspaces and synchronisations between the replays."""
+    d, G, Hkv, Tmax, s, w = 128, 4, 2, 2048, 6, 200
+    seq = np.array([2048, 1500, 70], np.int32)
+    B = len(seq)
+    prob = _decode_problem(d, G, "bf16", seq, Hkv, Tmax, seed=33)
+    q, k, v = prob["q"].to(DEV), prob["k"].to(DEV), prob["v"].to(DEV)
+    cfg = _cfg(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, max_seq_len=Tmax, budget=s, window=w,
+               mean_dtype="bf16", factor_dtype="e2m1")
+    seq_d = torch.from_numpy(seq).to(DEV)
+    ws = {op: cobs.new_workspace(cfg, op, DEV)
+          for op in (cobs.OP_BUILD, cobs.OP_SELECT, cobs.OP_SELECT_EXACT, cobs.OP_DECODE)}
+    shp = (B, G * Hkv, d)
+
+    def buffers():
+        o = dict(rec=cobs.new_summaries(cfg, DEV))
+        for nm in ("sel", "selx", "selq"):
+            o[nm] = torch.empty((B, Hkv, s), dtype=torch.int32, device=DEV)
+        for nm in ("sc", "scx", "scq"):
+            o[nm] = torch.empty((B, Hkv, cfg.num_blocks), dtype=torch.float32, device=DEV)
+        for nm in ("out", "os", "ow"):
+            o[nm] = torch.empty(shp, dtype=torch.float32, device=DEV)
+        for nm in ("lse", "ls", "lw"):
+            o[nm] = torch.empty(shp[:2], dtype=torch.float32, device=DEV)
+        return o
+
+    def run(o, stream=None):
+        cobs.cobs_build_block_stats(cfg, k, v, seq_d, o["rec"], ws=ws[cobs.OP_BUILD], stream=stream)
+        cobs.cobs_select(cfg, q, o["rec"], seq_d, o["sel"], ws[cobs.OP_SELECT], scores=o["sc"], stream=stream)
+        cobs.cobs_select_exact(cfg, q, k, v, seq_d, o["selx"], ws[cobs.OP_SELECT_EXACT], scores=o["scx"],
+                               stream=stream)
+        cobs.cobs_select_quest(cfg, q, k, v, seq_d, o["selq"], ws[cobs.OP_SELECT_EXACT], scores=o["scq"],
+                               stream=stream)
+        cobs.cobs_sparse_decode(cfg, q, k, v, seq_d, o["sel"], o["out"], ws[cobs.OP_DECODE], lse=o["lse"],
+                                stream=stream)
+        cobs.cobs_sparse_decode_branches(cfg, q, k, v, seq_d, o["selx"], o["os"], o["ow"], ws[cobs.OP_DECODE],
+                                         lse_sel=o["ls"], lse_win=o["lw"], stream=stream)
+
+    eager = buffers()
+    say("graph of every entry point: eager")
+    run(eager)
+    sync()
+    g_out = buffers()
+    stream = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        run(g_out, stream=stream)
+    for rep in range(3):
+        for nm, t in g_out.items():
+            t.zero_() if nm == "rec" else t.fill_(-5)
+        graph.replay()
+        sync()
+        say(f"graph of every entry point: replay {rep}")
+        for nm in eager:
+            assert torch.equal(g_out[nm], eager[nm]), (rep, nm)
+        run(buffers())            # eager work on the same workspaces between replays
+        sync()
