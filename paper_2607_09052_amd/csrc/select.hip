@@ -27,8 +27,15 @@ hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st
   if (!k) return hipErrorInvalidValue;
   const int base = select_min_bpw(p.mdt, p.fdt);
   const int64_t units = (int64_t)batch * p.hkv;
-  const int64_t slots = (int64_t)resident_workgroups(reinterpret_cast<const void*>(k), 256) * device_cus();
-  // blocks per workgroup: a multiple of `base`, enough that units * chunks fits the slots
+  // The grid is sized for the smaller resident count of the plain and the
+  // refreshing selector, so the decode step and a standalone selection chunk
+  // the blocks alike and their scores agree bitwise.
+  const SelectKernel kp = mfma ? select_mfma_kernel_for(p, d, g) : select_valu_kernel_for(p, d, g);
+  const SelectKernel kr = select_refresh_kernel_for(p, d, g);
+  if (!kp) return hipErrorInvalidValue;
+  int resident = resident_workgroups(reinterpret_cast<const void*>(kp), 256);
+  if (kr) resident = std::min(resident, resident_workgroups(reinterpret_cast<const void*>(kr), 256));
+  const int64_t slots = (int64_t)resident * device_cus();
   // blocks per workgroup: a multiple of `base`, one round of the resident slots
   int64_t bpw = (units * p.nbmax + slots - 1) / slots;
   bpw = std::max<int64_t>(base, (bpw + base - 1) / base * base);
