@@ -717,3 +717,54 @@ def test_every_entry_point_in_a_graph_matches_eager_on_every_replay():
             assert torch.equal(g_out[nm], eager[nm]), (rep, nm)
         run(buffers())            # eager work on the same workspaces between replays
         sync()
+
+
+def test_concurrent_steps_on_two_streams_match_sequential():
+    """Calls with their own workspaces and outputs share no state: two decode
+    steps on two streams, interleaved and overlapping, give bitwise the results
+    of the same calls made one after the other."""
+    cfgs, data = [], []
+    for i, (B, T) in enumerate(((2, 4096), (3, 2048))):
+        prob = synth.make_problem("c2", seed=51 + i, B=B, Hq=8, Hkv=2, T=T)
+        cfg = cobs.Config(batch=B, num_q_heads=8, num_kv_heads=2, head_dim=128, max_seq_len=T, rank=4,
+                          budget=8 + 4 * i, window=256)
+        q, k, v = prob["q"].to(DEV), prob["k"].to(DEV), prob["v"].to(DEV)
+        seq = torch.tensor([T - 17 * j for j in range(B)], dtype=torch.int32, device=DEV)
+        rec = cobs.new_summaries(cfg, DEV)
+        cobs.cobs_build_block_stats(cfg, k, v, seq, rec)
+        cfgs.append(cfg)
+        data.append((q, k, v, seq, rec))
+    sync()
+
+    def step(i, stream=None):
+        cfg, (q, k, v, seq, rec) = cfgs[i], data[i]
+        out = torch.empty((cfg.batch, 8, 128), dtype=torch.float32, device=DEV)
+        lse = torch.empty((cfg.batch, 8), dtype=torch.float32, device=DEV)
+        sel = torch.empty((cfg.batch, 2, cfg.budget), dtype=torch.int32, device=DEV)
+        ws = cobs.new_workspace(cfg, cobs.OP_STEP, DEV)
+        r = rec.clone()
+        return (out, lse, sel, r), lambda: cobs.cobs_decode_step(cfg, q, k, v, seq, r, out, ws, sel=sel, lse=lse,
+                                                                 stream=stream)
+
+    ref = []
+    for i in range(2):
+        bufs, call = step(i)
+        call()
+        sync()
+        ref.append(bufs)
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    runs = [[], []]
+    for i in range(2):
+        for _ in range(4):
+            runs[i].append(step(i, stream=streams[i]))
+    sync()                        # buffers are zeroed and copied on the default stream
+    say("two streams: interleaved steps")
+    for rep in range(4):
+        for i in range(2):
+            with torch.cuda.stream(streams[i]):
+                runs[i][rep][1]()
+    sync()
+    for i in range(2):
+        for bufs, _ in runs[i]:
+            for got, want in zip(bufs, ref[i]):
+                assert torch.equal(got, want), i
