@@ -103,8 +103,9 @@ typedef struct {
  *   elements, so (b, h, t, i) lives at
  *   k + ((block_table[b*(T_max/L) + t/L]*Hkv + h)*L + t%L)*d + i.
  *   Strides are ignored; page ids must lie in [0, num_pages) (an id outside it is
- *   never dereferenced: the decode leaves that page's tokens out and the
- *   statistics build reads them as zero keys).
+ *   never dereferenced: the decode leaves that page's tokens out, the
+ *   statistics build reads them as zero keys, and the exact-mass and Quest
+ *   selectors score such a block -inf for every head).
  * k, v: 16-byte aligned.                                                          */
 typedef struct {
   const void* k;

@@ -331,15 +331,3 @@ def drop_error(P, cent, kept):
     o_star = (P[:, None] * cent).sum(axis=0)
     tau = P[~kept].sum()
     return ((P[~kept][:, None] * (cent[~kept] - o_star)).sum(axis=0)) / (1.0 - tau)
-
-
-# -------------------------------------------------------- whole tensors --
-
-def gqa_group(h, G):
-    """Query heads sharing KV head h: contiguous, query head j -> KV head j // G (Sec. 2)."""
-    return slice(h * G, (h + 1) * G)
-
-
-def tail_block(T, L):
-    """Index of the block holding the newest token (position T - 1)."""
-    return (int(T) - 1) // int(L)

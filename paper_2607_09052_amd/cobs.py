@@ -124,14 +124,81 @@ def _check(status):
         raise CobsError(msg)
 
 
-def _kv(k, v, block_table=None, num_pages=0):
+_TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def _need(name, t, dtype, numel):
+    """Reject a tensor the kernels would misread: wrong dtype, not contiguous,
+    or fewer elements than the call reads or writes.  Returns it."""
+    if t is None:
+        raise CobsError(f"{name} is required")
+    if t.dtype != dtype:
+        raise CobsError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise CobsError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise CobsError(f"{name} holds {t.numel()} elements, the call needs {numel}")
+    return t
+
+
+def _opt(name, t, dtype, numel):
+    return None if t is None else _need(name, t, dtype, numel)
+
+
+def _same_gpu(**tensors):
+    """Every given tensor on one GPU (checked after the shapes and types)."""
+    dev = None
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise CobsError(f"{name} must be on a GPU")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise CobsError(f"{name} is on {t.device}, the call runs on {dev}")
+
+
+def _kv(cfg, k, v, block_table=None, num_pages=0):
+    """Validated K/V view (contiguous [>=B, >=Hkv, >=T_max, d] with the head
+    dimension dense, or pages [num_pages, Hkv, L, d] with a [B, T_max/L] table)."""
+    want = _TORCH_DTYPE[cfg.kv_dtype]
+    for name, t in (("k", k), ("v", v)):
+        if t is None or t.dtype != want:
+            raise CobsError(f"{name} must be {want} (kv_dtype {cfg.kv_dtype})")
+        if t.dim() != 4 or t.shape[-1] != cfg.head_dim or t.stride(-1) != 1:
+            raise CobsError(f"{name} must be 4-D with a dense head dimension of {cfg.head_dim}")
     if block_table is not None:
+        for name, t in (("k", k), ("v", v)):
+            if tuple(t.shape[1:]) != (cfg.num_kv_heads, cfg.block_size, cfg.head_dim) or not t.is_contiguous():
+                raise CobsError(f"paged {name} must be a contiguous [pages, Hkv, L, d] pool")
+            if not 1 <= int(num_pages) <= t.shape[0]:
+                raise CobsError(f"num_pages must lie in [1, {t.shape[0]}]")
+        _need("block_table", block_table, torch.int32, cfg.batch * cfg.num_blocks)
         return _KV(k.data_ptr(), v.data_ptr(), 0, 0, 0, block_table.data_ptr(), int(num_pages))
-    if k.stride() != v.stride():
-        raise CobsError("K and V must share strides")
-    if k.stride(-1) != 1:
-        raise CobsError("the head dimension of K/V must be contiguous")
+    if k.stride() != v.stride() or k.shape != v.shape:
+        raise CobsError("K and V must share shape and strides")
+    if k.shape[0] < cfg.batch or k.shape[1] < cfg.num_kv_heads or k.shape[2] < cfg.max_seq_len:
+        raise CobsError(f"K/V of shape {tuple(k.shape)} is smaller than "
+                        f"[{cfg.batch}, {cfg.num_kv_heads}, {cfg.max_seq_len}, {cfg.head_dim}]")
     return _KV(k.data_ptr(), v.data_ptr(), k.stride(0), k.stride(1), k.stride(2), None, 0)
+
+
+def _units(cfg):
+    return cfg.batch * cfg.num_kv_heads
+
+
+def _ws(ws):
+    """Workspace tensor (any element type, contiguous) and its size in bytes."""
+    if ws is None:
+        raise CobsError("ws is required")
+    if not ws.is_contiguous():
+        raise CobsError("ws must be contiguous")
+    return ws.numel() * ws.element_size()
+
+
+def _summaries(cfg, summaries):
+    return _need("summaries", summaries, torch.uint8, _units(cfg) * cfg.num_blocks * record_bytes(cfg))
 
 
 def record_bytes(cfg):
@@ -157,7 +224,10 @@ def cobs_build_block_stats(cfg, k, v, seq_lens, summaries, first_block=0, num_bl
                            ws=None, block_table=None, num_pages=0, stream=None):
     if num_blocks is None:
         num_blocks = cfg.num_blocks - first_block
-    kv = _kv(k, v, block_table, num_pages)
+    _need("seq_lens", seq_lens, torch.int32, cfg.batch)
+    _summaries(cfg, summaries)
+    kv = _kv(cfg, k, v, block_table, num_pages)
+    _same_gpu(seq_lens=seq_lens, summaries=summaries, k=k, v=v, block_table=block_table)
     _check(lib().cobs_build_block_stats(ctypes.byref(cfg.c_struct()), ctypes.byref(kv),
                                         _ptr(seq_lens), int(first_block), int(num_blocks),
                                         _ptr(summaries), _ptr(ws),
@@ -165,54 +235,97 @@ def cobs_build_block_stats(cfg, k, v, seq_lens, summaries, first_block=0, num_bl
                                         _stream(stream, summaries)))
 
 
+def _select_io(cfg, q, seq_lens, sel, scores):
+    _need("q", q, torch.float32, cfg.batch * cfg.num_q_heads * cfg.head_dim)
+    _need("seq_lens", seq_lens, torch.int32, cfg.batch)
+    _need("sel", sel, torch.int32, _units(cfg) * cfg.budget)
+    _opt("scores", scores, torch.float32, _units(cfg) * cfg.num_blocks)
+
+
 def cobs_select(cfg, q, summaries, seq_lens, sel, ws, scores=None, stream=None):
+    _select_io(cfg, q, seq_lens, sel, scores)
+    _summaries(cfg, summaries)
+    nws = _ws(ws)
+    _same_gpu(q=q, summaries=summaries, seq_lens=seq_lens, sel=sel, scores=scores, ws=ws)
     _check(lib().cobs_select(ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(summaries),
-                             _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws),
-                             ws.numel() * ws.element_size(), _stream(stream, q)))
+                             _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws), nws, _stream(stream, q)))
+
+
+def _dense_key_select(fn, cfg, q, k, v, seq_lens, sel, ws, scores, block_table, num_pages, stream):
+    _select_io(cfg, q, seq_lens, sel, scores)
+    kv = _kv(cfg, k, v, block_table, num_pages)
+    nws = _ws(ws)
+    _same_gpu(q=q, k=k, v=v, seq_lens=seq_lens, sel=sel, scores=scores, ws=ws, block_table=block_table)
+    _check(fn(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv), _ptr(seq_lens), _ptr(sel), _ptr(scores),
+              _ptr(ws), nws, _stream(stream, q)))
 
 
 def cobs_select_exact(cfg, q, k, v, seq_lens, sel, ws, scores=None, block_table=None, num_pages=0,
                       stream=None):
-    kv = _kv(k, v, block_table, num_pages)
-    _check(lib().cobs_select_exact(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
-                                   _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws),
-                                   ws.numel() * ws.element_size(), _stream(stream, q)))
+    _dense_key_select(lib().cobs_select_exact, cfg, q, k, v, seq_lens, sel, ws, scores, block_table, num_pages,
+                      stream)
 
 
 def cobs_select_quest(cfg, q, k, v, seq_lens, sel, ws, scores=None, block_table=None, num_pages=0,
                       stream=None):
-    kv = _kv(k, v, block_table, num_pages)
-    _check(lib().cobs_select_quest(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
-                                   _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws),
-                                   ws.numel() * ws.element_size(), _stream(stream, q)))
+    _dense_key_select(lib().cobs_select_quest, cfg, q, k, v, seq_lens, sel, ws, scores, block_table, num_pages,
+                      stream)
+
+
+def _decode_io(cfg, q, seq_lens, sel, outs, lses, sel_required=True):
+    _need("q", q, torch.float32, cfg.batch * cfg.num_q_heads * cfg.head_dim)
+    _need("seq_lens", seq_lens, torch.int32, cfg.batch)
+    if (sel_required and cfg.budget > 0) or sel is not None:
+        _need("sel", sel, torch.int32, _units(cfg) * cfg.budget)
+    for name, o in outs.items():
+        _need(name, o, torch.float32, cfg.batch * cfg.num_q_heads * cfg.head_dim)
+    for name, l in lses.items():
+        _opt(name, l, torch.float32, cfg.batch * cfg.num_q_heads)
 
 
 def cobs_sparse_decode(cfg, q, k, v, seq_lens, sel, out, ws, lse=None, block_table=None,
                        num_pages=0, stream=None):
-    kv = _kv(k, v, block_table, num_pages)
+    _decode_io(cfg, q, seq_lens, sel, dict(out=out), dict(lse=lse))
+    kv = _kv(cfg, k, v, block_table, num_pages)
+    nws = _ws(ws)
+    _same_gpu(q=q, k=k, v=v, seq_lens=seq_lens, sel=sel, out=out, lse=lse, ws=ws, block_table=block_table)
     _check(lib().cobs_sparse_decode(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
-                                    _ptr(seq_lens), _ptr(sel), _ptr(out), _ptr(lse), _ptr(ws),
-                                    ws.numel() * ws.element_size(), _stream(stream, q)))
+                                    _ptr(seq_lens), _ptr(sel), _ptr(out), _ptr(lse), _ptr(ws), nws,
+                                    _stream(stream, q)))
 
 
 def cobs_sparse_decode_branches(cfg, q, k, v, seq_lens, sel, out_sel, out_win, ws, lse_sel=None, lse_win=None,
                                 block_table=None, num_pages=0, stream=None):
-    kv = _kv(k, v, block_table, num_pages)
+    _decode_io(cfg, q, seq_lens, sel, dict(out_sel=out_sel, out_win=out_win), dict(lse_sel=lse_sel, lse_win=lse_win))
+    kv = _kv(cfg, k, v, block_table, num_pages)
+    nws = _ws(ws)
+    _same_gpu(q=q, k=k, v=v, seq_lens=seq_lens, sel=sel, out_sel=out_sel, out_win=out_win, lse_sel=lse_sel,
+              lse_win=lse_win, ws=ws, block_table=block_table)
     _check(lib().cobs_sparse_decode_branches(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
                                              _ptr(seq_lens), _ptr(sel), _ptr(out_sel), _ptr(lse_sel),
-                                             _ptr(out_win), _ptr(lse_win), _ptr(ws),
-                                             ws.numel() * ws.element_size(), _stream(stream, q)))
+                                             _ptr(out_win), _ptr(lse_win), _ptr(ws), nws, _stream(stream, q)))
 
 
 def cobs_decode_step(cfg, q, k, v, seq_lens, summaries, out, ws, sel=None, lse=None,
                      block_table=None, num_pages=0, stream=None):
-    kv = _kv(k, v, block_table, num_pages)
+    _decode_io(cfg, q, seq_lens, sel, dict(out=out), dict(lse=lse), sel_required=False)
+    _summaries(cfg, summaries)
+    kv = _kv(cfg, k, v, block_table, num_pages)
+    nws = _ws(ws)
+    _same_gpu(q=q, k=k, v=v, seq_lens=seq_lens, summaries=summaries, sel=sel, out=out, lse=lse, ws=ws,
+              block_table=block_table)
     _check(lib().cobs_decode_step(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
                                   _ptr(seq_lens), _ptr(summaries), _ptr(sel), _ptr(out), _ptr(lse),
-                                  _ptr(ws), ws.numel() * ws.element_size(), _stream(stream, q)))
+                                  _ptr(ws), nws, _stream(stream, q)))
 
 
 def cobs_pack_e2m1(x, codes, scales, stream=None):
+    if x is None or x.dim() != 2:
+        raise CobsError("x must be a 2-D [num_vectors, dim] tensor")
     n, dim = x.shape
+    _need("x", x, torch.float32, n * dim)
+    _need("codes", codes, torch.uint8, n * (dim // 2))
+    _need("scales", scales, torch.float32, n)
+    _same_gpu(x=x, codes=codes, scales=scales)
     _check(lib().cobs_pack_e2m1(_ptr(x), int(n), int(dim), _ptr(codes), _ptr(scales),
                                 _stream(stream, x)))

@@ -222,13 +222,18 @@ __device__ __forceinline__ void finish_select(const SelectParams& p, int unit, i
     for (int u = 0; u < UB; ++u) {
       if (u0 + u >= U) continue;
       const int blk = (u0 + u) * kSelThreads + tid;
+      // a block scored -inf for a head (an out-of-range page in the dense-key
+      // selectors) contributes nothing to it; -inf for every head gives -inf
       float mx = -INFINITY;
 #pragma unroll
-      for (int g = 0; g < G; ++g) { v[u][g] -= lz[g]; mx = fmaxf(mx, v[u][g]); }
+      for (int g = 0; g < G; ++g) {
+        v[u][g] = (v[u][g] == -INFINITY) ? -INFINITY : v[u][g] - lz[g];
+        mx = fmaxf(mx, v[u][g]);
+      }
       float acc = 0.0f;
 #pragma unroll
       for (int g = 0; g < G; ++g) acc += __expf(v[u][g] - mx);
-      const float sig = mx + __logf(acc);
+      const float sig = (mx == -INFINITY) ? -INFINITY : mx + __logf(acc);
       key[u0 + u] = order_key(sig);
       if (p.scores && blk < nc) p.scores[(int64_t)unit * p.nbmax + blk] = sig;
     }

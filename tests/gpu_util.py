@@ -128,6 +128,66 @@ def unit_slices(cfg, b, h):
     return b, slice(h * G, (h + 1) * G)
 
 
+def ky_fan_checks(xi, K, n, r):
+    """Block statistics of the GPU (fp32 factors xi [r, d] of the n keys K) against
+    the oracle: Ky-Fan energy, orthogonality and, where the eigengap allows,
+    closeness of the rank-r covariance."""
+    Sig = M.block_covariance(K)
+    lam = np.sort(np.clip(np.linalg.eigvalsh(Sig), 0, None))[::-1]
+    etop = lam[:r].sum()
+    e = float((xi ** 2).sum())
+    if etop <= 1e-12:
+        assert np.all(xi == 0), "zero-variance block must store exact zeros"
+        return
+    assert (1 - 1e-3) * etop <= e <= (1 + 1e-5) * etop + 1e-6, (e, etop)
+    nrm = np.linalg.norm(xi, axis=1)
+    for i in range(r):
+        for j in range(i + 1, r):
+            if nrm[i] > 0 and nrm[j] > 0:
+                assert abs(xi[i] @ xi[j]) <= 1e-4 * nrm[i] * nrm[j] + 1e-7
+    if lam[r - 1] > 0 and (lam[r - 1] - lam[r]) / lam[r - 1] >= 0.05:
+        ref = M.scaled_eigenvectors(Sig, r)
+        A, Bm = xi.T @ xi, ref.T @ ref
+        assert np.linalg.norm(A - Bm) <= 1e-3 * np.linalg.norm(Bm), np.linalg.norm(A - Bm) / np.linalg.norm(Bm)
+
+
+def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None):
+    """GPU block records of one unit against the oracle.
+
+    rec32_unit: the unit's records built with fp32 mean and factors from the
+    same keys; rec_unit: the configured storage.  Counts exact, means within
+    fp32 rounding of the oracle's, zero factors for a partial block, Ky-Fan
+    energy / orthogonality / rank-r subspace for full blocks, and the configured
+    record byte-identical to the oracle's encoding of the fp32 statistics (the
+    storage rounding of Sec. 5.5).  `blocks`: block indices to check (default all)."""
+    L, d, r = cfg.block_size, cfg.head_dim, cfg.rank
+    nb = M.num_blocks(T, L)
+    if nb == 0:
+        return
+    counts, means, factors = R.decode(rec32_unit[:nb], d, r, "f32", "f32")
+    K = np.asarray(K_unit, dtype=np.float64)
+    blocks = range(nb) if blocks is None else [j for j in blocks if j < nb]
+    for j in blocks:
+        n = M.block_count(T, L, j)
+        Kb = K[j * L:j * L + n]
+        assert counts[j] == n, (j, counts[j], n)
+        np.testing.assert_allclose(means[j], M.block_mean(Kb), rtol=0, atol=1e-6 * max(np.abs(Kb).max(), 1e-30))
+        if n < L or r == 0:
+            assert np.all(factors[j] == 0), j
+        else:
+            ky_fan_checks(factors[j], Kb, n, r)
+    want = R.encode(counts, means, factors, cfg.mean_dtype, cfg.factor_dtype)
+    got = np.asarray(rec_unit[:nb])
+    for j in blocks:
+        np.testing.assert_array_equal(got[j], want[j], err_msg=f"block {j}")
+
+
+def f32_config(cfg):
+    """The same problem with fp32 mean and factor storage."""
+    import dataclasses
+    return dataclasses.replace(cfg, mean_dtype="f32", factor_dtype="f32")
+
+
 def block_statistics_gpu(cfg, k, v, seq_lens):
     rec = cobs.new_summaries(cfg, DEV)
     cobs.cobs_build_block_stats(cfg, k, v, seq_lens, rec)

@@ -122,3 +122,43 @@ def test_null_and_workspace_errors_on_host():
     assert lib.cobs_sparse_decode_branches(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, fake, fake, None,
                                            None, None, fake, 1 << 30, None) == 1
     assert lib.cobs_status_string(3).startswith(b"COBS_ERR_WORKSPACE")
+
+
+def test_binding_rejects_tensors_the_kernels_would_misread():
+    """The Python binding checks dtype, contiguity, size and device of every
+    tensor before calling the library (CPU tensors: the device check fires last)."""
+    import torch
+    cfg = _cfg(batch=2, num_q_heads=8, num_kv_heads=2, head_dim=128, max_seq_len=1024, budget=4)
+    B, Hq, Hkv, d, T = 2, 8, 2, 128, 1024
+    q = torch.zeros((B, Hq, d), dtype=torch.float32)
+    k = torch.zeros((B, Hkv, T, d), dtype=torch.bfloat16)
+    seq = torch.zeros(B, dtype=torch.int32)
+    sel = torch.zeros((B, Hkv, 4), dtype=torch.int32)
+    out = torch.zeros((B, Hq, d), dtype=torch.float32)
+    ws = torch.zeros(1 << 20, dtype=torch.uint8)
+
+    def rejects(fn, *a, match, **kw):
+        with pytest.raises(cobs.CobsError, match=match):
+            fn(*a, **kw)
+
+    dec = cobs.cobs_sparse_decode
+    rejects(dec, cfg, q.to(torch.bfloat16), k, k, seq, sel, out, ws, match="q must be")
+    rejects(dec, cfg, q[:, :4].contiguous(), k, k, seq, sel, out, ws, match="q holds")
+    rejects(dec, cfg, q.transpose(0, 1), k, k, seq, sel, out, ws, match="contiguous")
+    rejects(dec, cfg, q, k, k, seq.to(torch.int64), sel, out, ws, match="seq_lens must be")
+    rejects(dec, cfg, q, k, k, seq, sel.to(torch.int64), out, ws, match="sel must be")
+    rejects(dec, cfg, q, k, k, seq, None, out, ws, match="sel is required")
+    rejects(dec, cfg, q, k, k, seq, sel, out.to(torch.bfloat16), ws, match="out must be")
+    rejects(dec, cfg, q, k, k, seq, sel, out, ws, lse=torch.zeros(B * Hq, dtype=torch.float64),
+            match="lse must be")
+    rejects(dec, cfg, q, k, k, seq, sel, out, ws, match="q must be on a GPU")
+    rejects(cobs.cobs_select, cfg, q, torch.zeros(8, dtype=torch.uint8), seq, sel, ws, match="summaries holds")
+    rejects(cobs.cobs_decode_step, cfg, q, k, k, seq, torch.zeros(8, dtype=torch.uint8), out, ws,
+            match="summaries holds")
+    rejects(cobs.cobs_pack_e2m1, torch.zeros((4, 8), dtype=torch.float64), torch.zeros((4, 4), dtype=torch.uint8),
+            torch.zeros(4), match="x must be")
+    rejects(dec, cfg, q, k.to(torch.float32), k.to(torch.float32), seq, sel, out, ws, match="kv_dtype")
+    rejects(dec, cfg, q, k[..., :64], k[..., :64], seq, sel, out, ws, match="dense head dimension")
+    rejects(dec, cfg, q, k[:, :, :512], k[:, :, :512], seq, sel, out, ws, match="smaller than")
+    rejects(dec, cfg, q, k, k, seq, sel, out, ws, block_table=torch.zeros((B, 16), dtype=torch.int32),
+            num_pages=4, match="paged k must be")

@@ -14,7 +14,7 @@ from oracle import numerics as nx
 from oracle import records as R
 from paper_2607_09052_amd import cobs
 from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_selection, f64, oracle_decode,
-                            oracle_select, rel_l2, say, sync, valid_prefix)
+                            ky_fan_checks, oracle_select, rel_l2, say, sync, valid_prefix)
 
 pytestmark = pytest.mark.gpu
 
@@ -466,27 +466,6 @@ def _stats_cache(law, d, nblk, tail, seed):
     return K, T
 
 
-def _ky_fan_checks(xi, K, n, r):
-    """Energy, orthogonality and (where the eigengap allows) subspace closeness."""
-    Sig = M.block_covariance(K)
-    lam = np.sort(np.clip(np.linalg.eigvalsh(Sig), 0, None))[::-1]
-    etop = lam[:r].sum()
-    e = float((xi ** 2).sum())
-    if etop <= 1e-12:
-        assert np.all(xi == 0), "zero-variance block must store exact zeros"
-        return
-    assert (1 - 1e-3) * etop <= e <= (1 + 1e-5) * etop + 1e-6, (e, etop)
-    nrm = np.linalg.norm(xi, axis=1)
-    for i in range(r):
-        for j in range(i + 1, r):
-            if nrm[i] > 0 and nrm[j] > 0:
-                assert abs(xi[i] @ xi[j]) <= 1e-4 * nrm[i] * nrm[j] + 1e-7
-    if lam[r - 1] > 0 and (lam[r - 1] - lam[r]) / lam[r - 1] >= 0.05:
-        ref = M.scaled_eigenvectors(Sig, r)
-        A, Bm = xi.T @ xi, ref.T @ ref
-        assert np.linalg.norm(A - Bm) <= 1e-3 * np.linalg.norm(Bm), np.linalg.norm(A - Bm) / np.linalg.norm(Bm)
-
-
 @pytest.mark.parametrize("law,d,r", [("gauss", 128, 4), ("spiked", 128, 4), ("mixed", 128, 8),
                                      ("gauss", 64, 2), ("spiked", 128, 12), ("lowrank", 64, 6)])
 def test_build_stats_matches_oracle(law, d, r):
@@ -510,7 +489,7 @@ def test_build_stats_matches_oracle(law, d, r):
         if n < 64:
             assert np.all(factors[blk] == 0)
             continue
-        _ky_fan_checks(factors[blk], K[blk * 64:blk * 64 + 64].astype(np.float64), n, r)
+        ky_fan_checks(factors[blk], K[blk * 64:blk * 64 + 64].astype(np.float64), n, r)
         # sign convention: the largest-magnitude entry of each stored vector is positive
         for i in range(r):
             if np.any(factors[blk, i] != 0):
@@ -549,7 +528,7 @@ def test_build_bf16_keys_and_storage_dtypes_consistent():
             np.testing.assert_allclose(m32, om, rtol=0, atol=2e-6 * np.abs(Kh).max())
             for blk in range(nb):
                 if oc[blk] == 64:
-                    _ky_fan_checks(x32[blk], Kh[blk * 64:(blk + 1) * 64], 64, r)
+                    ky_fan_checks(x32[blk], Kh[blk * 64:(blk + 1) * 64], 64, r)
             # bf16 storage = RNE of the fp32 statistics
             _, mb, xb = R.decode(recs[("bf16", "bf16")][b, h, :nb], d, r, "bf16", "bf16")
             t = lambda a: torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16).double().numpy()

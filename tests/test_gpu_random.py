@@ -18,8 +18,8 @@ import torch
 import synth
 from oracle import method as M
 from paper_2607_09052_amd import cobs
-from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_selection, f64, oracle_decode, oracle_select,
-                            say, sync)
+from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_records, check_selection, f32_config, f64,
+                            oracle_decode, oracle_select, say, sync)
 
 pytestmark = pytest.mark.gpu
 
@@ -101,6 +101,9 @@ def _check(c, data_seed, tag):
     seq_d = torch.from_numpy(c["seq"]).to(DEV)
     rec = cobs.new_summaries(cfg, DEV)
     cobs.cobs_build_block_stats(cfg, kd, vd, seq_d, rec)
+    cfg32 = f32_config(cfg)
+    rec32 = cobs.new_summaries(cfg32, DEV)
+    cobs.cobs_build_block_stats(cfg32, kd, vd, seq_d, rec32)
     s_alloc = max(c["s"], 1)
     sel = torch.full((B, Hkv, s_alloc), -7, dtype=torch.int32, device=DEV)
     scores = torch.empty((B, Hkv, cfg.num_blocks), dtype=torch.float32, device=DEV)
@@ -121,12 +124,17 @@ def _check(c, data_seed, tag):
     cobs.cobs_decode_step(cfg, qd, kd, vd, seq_d, rec1, out1, cobs.new_workspace(cfg, cobs.OP_STEP, DEV),
                           sel=sel1 if c["s"] > 0 else None, lse=lse1)
     sync()
-    rec_h, sc_h = rec.cpu().numpy(), scores.cpu().numpy()
+    rec_h, sc_h, rec32_h = rec.cpu().numpy(), scores.cpu().numpy(), rec32.cpu().numpy()
     sel_h, out_h, lse_h = sel_c.cpu().numpy(), out.cpu().numpy(), lse.cpu().numpy()
     for b in range(B):
         T = int(seq_c[b])
+        nb = -(-T // 64)
+        # block statistics of this row: every block of short contexts, else a
+        # stride of them plus the last two
+        blocks = None if nb <= 64 else sorted(set(range(0, nb, nb // 32)) | {nb - 2, nb - 1})
         for h in range(Hkv):
             gs = slice(h * G, (h + 1) * G)
+            check_records(cfg, rec_h[b, h], rec32_h[b, h], f64(k[b, h]), T, blocks)
             sigma, nc, _ = oracle_select(rec_h[b, h], q[b, gs].double().numpy(), T, cfg)
             assert np.all(np.abs(sc_h[b, h, :nc] - sigma[:nc]) <= SIGMA_TOL)
             assert np.all(np.isneginf(sc_h[b, h, nc:]))

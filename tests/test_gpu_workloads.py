@@ -1,16 +1,22 @@
 """End-to-end decode steps of the five workloads against the fp64 oracle.
 
-The GPU builds its own descriptors from K (fixed-count block power iteration,
-fp32) while the oracle builds its own (exact fp64 eigendecomposition); both
-then score, select and attend.  Descriptors built independently differ within
-the block-statistics tolerances, so scores are compared with a band `delta`
-per factor storage type (see DECISION_BAND) and the selection is checked with
-the set rule at band 2*delta.  Attention itself is compared on the same block
-set (the oracle's selection fed to the GPU's sparse decode), and the fused
-step's output is compared directly whenever both sides selected the same set.
-"""
+Two comparisons per checked (batch row, KV head) unit:
 
-import math
+* Shared record bytes (the decode-step rule): the oracle scores the records the
+  GPU built, so |sigma_gpu - sigma_oracle| <= 2e-5 on every candidate, the
+  selection is bit-exact unless the oracle's gap at the s-th boundary is below
+  1e-4 (then the set rule), and the step's output matches the oracle's
+  attention on the GPU's selection (relative L2 2e-3 for bf16 K/V, 1e-5 for
+  fp32).  The GPU's records themselves are checked against the oracle's block
+  statistics (counts, means, Ky-Fan energy, orthogonality, rank-r covariance)
+  and byte for byte against the oracle's storage encoding of the GPU's fp32
+  statistics.
+* Independent descriptors (build quality): the oracle also builds its own
+  descriptors from K by exact fp64 eigendecomposition.  Scores then agree
+  within a band per factor storage type (DECISION_BAND), selections follow the
+  set rule at twice that band, the share of selected block ids that differ is
+  bounded, and attention on the oracle's selection matches the oracle.
+"""
 
 import numpy as np
 import pytest
@@ -19,8 +25,8 @@ import torch
 import synth
 from oracle import method as M
 from paper_2607_09052_amd import cobs
-from tests.gpu_util import (DEV, check_out, check_selection, config_from, f64, oracle_decode,
-                            say, sync)
+from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_records, check_selection, config_from, f32_config,
+                            f64, oracle_decode, oracle_select, say, sync)
 
 pytestmark = pytest.mark.gpu
 
@@ -32,10 +38,36 @@ pytestmark = pytest.mark.gpu
 # move an element across an E2M1 rounding boundary, changing it by one code
 # step (up to max|xi|/3) and sigma by up to ~1e-2.
 DECISION_BAND = {"f32": 2e-3, "bf16": 4e-3, "e2m1": 2e-2}
+# Largest share of selected block ids allowed to differ between the GPU's and
+# the oracle's independently built descriptors (boundary blocks whose scores
+# lie within the band above).
+ID_DIFF_BOUND = {"f32": 0.05, "bf16": 0.05, "e2m1": 0.15}
 
 
 def _oracle_stats(K, T, cfg):
     return M.stored_statistics(*M.block_statistics(K, T, 64, cfg.rank), cfg.mean_dtype, cfg.factor_dtype)
+
+
+def _id_diff(a, b):
+    a = {x for x in np.asarray(a).tolist() if x >= 0}
+    b = {x for x in np.asarray(b).tolist() if x >= 0}
+    return len(a - b), max(len(a), 1)
+
+
+def _shared_bytes_check(cfg, rec_u, q_u, K_u, V_u, T, sel_u, out_u, lse_u, scores_u=None):
+    """The decode-step rule on the GPU's own records: oracle scores of the same
+    bytes, the set rule at 1e-4, attention on the GPU's selection."""
+    sigma, nc, _ = oracle_select(rec_u, q_u, T, cfg)
+    if scores_u is not None:
+        assert np.all(np.abs(scores_u[:nc] - sigma[:nc]) <= SIGMA_TOL), float(np.max(np.abs(scores_u[:nc] - sigma[:nc])))
+    exact = check_selection(sel_u, sigma, nc, cfg.budget)
+    o, l = oracle_decode(q_u, K_u, V_u, T, sel_u, cfg)
+    check_out(out_u, lse_u, o, l, cfg.kv_dtype)
+    return exact
+
+
+def _sample_blocks(nb, want=48):
+    return sorted(set(range(0, nb, max(1, nb // want))) | {nb - 1})
 
 
 def _run_case(name, seed, units=None, **over):
@@ -47,6 +79,12 @@ def _run_case(name, seed, units=None, **over):
     rec = cobs.new_summaries(cfg, DEV)
     say(f"{name}: build {B}x{Hkv}x{cfg.num_blocks} blocks")
     cobs.cobs_build_block_stats(cfg, k, v, seq, rec)
+    cfg32 = f32_config(cfg)
+    if (cfg.mean_dtype, cfg.factor_dtype) == ("f32", "f32"):
+        rec32 = rec
+    else:
+        rec32 = cobs.new_summaries(cfg32, DEV)
+        cobs.cobs_build_block_stats(cfg32, k, v, seq, rec32)
     out = torch.empty((B, c["Hq"], d), dtype=torch.float32, device=DEV)
     lse = torch.empty((B, c["Hq"]), dtype=torch.float32, device=DEV)
     sel = torch.empty((B, Hkv, c["s"]), dtype=torch.int32, device=DEV)
@@ -65,11 +103,19 @@ def _run_case(name, seed, units=None, **over):
     ora = {}
     sel_o = torch.full_like(sel, -1)
     worst = 0.0
-    same = 0
+    same = shared_exact = 0
+    ndiff = ntot = 0
+    T = int(c["T"])
+    nb = -(-T // 64)
     for (b, h) in units:
-        T = int(c["T"])
         K, V = f64(k[b, h, :T]), f64(v[b, h, :T])
         qu = f64(q[b, h * G:(h + 1) * G])
+        sl = slice(h * G, (h + 1) * G)
+        rec_u = rec[b, h].cpu().numpy()
+        check_records(cfg, rec_u, rec32[b, h].cpu().numpy(), K, T, _sample_blocks(nb))
+        shared_exact += _shared_bytes_check(cfg, rec_u, qu, K, V, T, sel[b, h].cpu().numpy(),
+                                            out[b, sl].cpu().numpy(), lse[b, sl].cpu().numpy(),
+                                            scores[b, h].cpu().numpy())
         res = M.decode_unit(qu, K, V, T, 64, cfg.rank, cfg.budget, cfg.window, cfg.scale,
                             cfg.mean_dtype, cfg.factor_dtype, stats=_oracle_stats(K, T, cfg))
         ora[(b, h)] = res
@@ -79,8 +125,13 @@ def _run_case(name, seed, units=None, **over):
         worst = max(worst, dev_)
         assert dev_ <= band, (b, h, dev_)
         same += check_selection(sel[b, h].cpu().numpy(), res["sigma"], nc, cfg.budget, band=2 * band)
+        nd, nt = _id_diff(sel[b, h].cpu().numpy(), res["sel"])
+        ndiff, ntot = ndiff + nd, ntot + nt
         sel_o[b, h] = torch.from_numpy(res["sel"].astype(np.int32))
-    say(f"{name}: max |sigma_gpu - sigma_oracle| = {worst:.2e}; identical selections {same}/{len(units)}")
+    say(f"{name}: shared bytes: exact selections {shared_exact}/{len(units)}; independent descriptors: "
+        f"max |sigma_gpu - sigma_oracle| = {worst:.2e}, identical selections {same}/{len(units)}, "
+        f"differing block ids {ndiff}/{ntot}")
+    assert ndiff <= ID_DIFF_BOUND[cfg.factor_dtype] * ntot, (ndiff, ntot)
     out_o = torch.empty_like(out)
     lse_o = torch.empty_like(lse)
     cobs.cobs_sparse_decode(cfg, q, k, v, seq, sel_o, out_o, cobs.new_workspace(cfg, cobs.OP_DECODE, DEV), lse=lse_o)
@@ -88,8 +139,6 @@ def _run_case(name, seed, units=None, **over):
     for (b, h), res in ora.items():
         sl = slice(h * G, (h + 1) * G)
         check_out(out_o[b, sl].cpu().numpy(), lse_o[b, sl].cpu().numpy(), res["out"], res["lse"], cfg.kv_dtype)
-        if np.array_equal(sel[b, h].cpu().numpy(), res["sel"]):
-            check_out(out[b, sl].cpu().numpy(), lse[b, sl].cpu().numpy(), res["out"], res["lse"], cfg.kv_dtype)
     return prob, sel, ora
 
 
@@ -124,14 +173,23 @@ def test_full_size_sampled_units(name, units):
 
 
 def test_c5_build_then_256_appending_steps():
-    """Prefill build, then 256 decode steps that each append one token (c5 shapes)."""
+    """Prefill build, then 256 decode steps that each append one token (c5 shapes).
+
+    Every 8th step, every block-fill step and the last: on two units, the step's
+    selection and output against the oracle on the step's own records (the
+    decode-step rule), and against the oracle's independently maintained
+    records (band rule; the differing selected ids are counted and bounded).
+    On block-fill steps the newly filled block's record is also checked against
+    the oracle's statistics of its keys."""
     prob = synth.make_problem("c5", device=DEV)
     c = prob["cfg"]
     cfg = config_from(c)
+    cfg32 = f32_config(cfg)
     B, Hkv, G, d, T0 = c["B"], c["Hkv"], c["Hq"] // c["Hkv"], c["d"], c["T"]
     k, v = prob["k"], prob["v"]
     seq = torch.full((B,), T0, dtype=torch.int32, device=DEV)
     rec = cobs.new_summaries(cfg, DEV)
+    rec32 = cobs.new_summaries(cfg32, DEV)
     say("c5: prefill build")
     cobs.cobs_build_block_stats(cfg, k, v, seq, rec)
     ws = cobs.new_workspace(cfg, cobs.OP_STEP, DEV)
@@ -143,19 +201,33 @@ def test_c5_build_then_256_appending_steps():
     Vf = {u: f64(v[u[0], u[1]]) for u in units}
     stats = {u: [np.array(x) for x in _oracle_stats(Kf[u], T0, cfg)] for u in units}
     band = DECISION_BAND[cfg.factor_dtype]
-    worst = 0.0
+    checked = shared_exact = indep_same = ndiff = ntot = fills = 0
     for step in range(c["steps"]):
         T = T0 + step + 1
         seq.fill_(T)
         q = prob["q_steps"][step].contiguous()
         cobs.cobs_decode_step(cfg, q, k, v, seq, rec, out, ws, sel=sel, lse=lse)
-        if step % 32 == 0 or step == c["steps"] - 1 or T % 64 == 0:
+        fill = T % 64 == 0
+        if step % 8 == 0 or step == c["steps"] - 1 or fill:
+            j = (T - 1) // 64
+            if fill:
+                # the filled block once more with fp32 storage, for its statistics
+                cobs.cobs_build_block_stats(cfg32, k, v, seq, rec32, first_block=j, num_blocks=1)
             sync()
             say(f"c5: step {step} T={T}")
             for (b, h) in units:
+                qu = f64(q[b, h * G:(h + 1) * G])
+                sl = slice(h * G, (h + 1) * G)
+                rec_u = rec[b, h].cpu().numpy()
+                if fill:
+                    check_records(cfg, rec_u, rec32[b, h].cpu().numpy(), Kf[(b, h)][:T], T, [j])
+                    fills += 1
+                shared_exact += _shared_bytes_check(cfg, rec_u, qu, Kf[(b, h)], Vf[(b, h)], T,
+                                                    sel[b, h].cpu().numpy(), out[b, sl].cpu().numpy(),
+                                                    lse[b, sl].cpu().numpy())
                 # oracle tail update (the block holding token T-1), then the step
+                # on the oracle's own records
                 cnt, mns, fac = stats[(b, h)]
-                j = (T - 1) // 64
                 tail = M.stored_statistics(*M.block_statistics(Kf[(b, h)][j * 64:T], T - j * 64, 64, cfg.rank),
                                            cfg.mean_dtype, cfg.factor_dtype)
                 if j >= len(cnt):
@@ -165,13 +237,15 @@ def test_c5_build_then_256_appending_steps():
                 else:
                     cnt[j], mns[j], fac[j] = tail[0][0], tail[1][0], tail[2][0]
                 stats[(b, h)] = [cnt, mns, fac]
-                qu = f64(q[b, h * G:(h + 1) * G])
                 res = M.decode_unit(qu, Kf[(b, h)], Vf[(b, h)], T, 64, cfg.rank, cfg.budget, cfg.window,
                                     cfg.scale, cfg.mean_dtype, cfg.factor_dtype, stats=(cnt, mns, fac))
-                check_selection(sel[b, h].cpu().numpy(), res["sigma"], res["nc"], cfg.budget, band=2 * band)
-                sl = slice(h * G, (h + 1) * G)
-                if np.array_equal(sel[b, h].cpu().numpy(), res["sel"]):
-                    check_out(out[b, sl].cpu().numpy(), lse[b, sl].cpu().numpy(), res["out"], res["lse"], "bf16")
-                else:
-                    worst += 1
-    say(f"c5: steps with a boundary-band selection difference: {int(worst)}")
+                indep_same += check_selection(sel[b, h].cpu().numpy(), res["sigma"], res["nc"], cfg.budget,
+                                              band=2 * band)
+                nd, nt = _id_diff(sel[b, h].cpu().numpy(), res["sel"])
+                ndiff, ntot = ndiff + nd, ntot + nt
+                checked += 1
+    say(f"c5: {checked} unit-steps checked ({fills} on block fills); shared bytes: exact selections "
+        f"{shared_exact}/{checked}; independent descriptors: identical selections {indep_same}/{checked}, "
+        f"differing block ids {ndiff}/{ntot}")
+    assert fills >= 2 * 4
+    assert ndiff <= ID_DIFF_BOUND[cfg.factor_dtype] * ntot, (ndiff, ntot)

@@ -90,6 +90,54 @@ def test_low_rank_factors_are_best_rank_r():
     np.testing.assert_allclose(xi.T @ xi, best, rtol=0, atol=1e-11)
 
 
+def test_sign_rule_on_hand_worked_vectors():
+    """Reading of the stored eigenvector's sign (the paper leaves it open; the score
+    q^T xi xi^T q does not depend on it): each vector is flipped so that its
+    largest-magnitude entry is positive, the lowest index winning a tie."""
+    xi = np.array([[0.1, -0.5, 0.3],        # largest |.| at index 1, negative: flip
+                   [0.2, 0.7, -0.1],        # largest positive already: keep
+                   [-0.5, 0.5, 0.0],        # tie between 0 and 1: index 0 decides, flip
+                   [0.5, -0.5, 0.25],       # tie, index 0 positive: keep
+                   [0.0, 0.0, 0.0]])        # zero vector stays zero
+    want = np.array([[-0.1, 0.5, -0.3],
+                     [0.2, 0.7, -0.1],
+                     [0.5, -0.5, -0.0],
+                     [0.5, -0.5, 0.25],
+                     [0.0, 0.0, 0.0]])
+    np.testing.assert_array_equal(M.canonical_sign(xi), want)
+    # every stored factor of a real block obeys the rule (checked entry by entry)
+    Kb = synth.make_keys_block(64, 128, "gauss", 41).astype(np.float64)
+    for fac in (M.scaled_eigenvectors(M.block_covariance(Kb), 6), M.scaled_eigenvectors_gram(Kb, 6)):
+        for row in fac:
+            mags = np.abs(row)
+            first = int(np.nonzero(mags == mags.max())[0][0])
+            assert row[first] > 0
+
+
+def test_partial_tail_block_stores_zero_factors_until_it_fills():
+    """Sec. 5.6 rebuilds a block's factors as the block fills; the reading here: a
+    partial block (n_b < L) stores its exact count and mean and zero factors, and
+    the same block gets the top-r eigen-factors of its population covariance once
+    it holds L keys."""
+    L, d, r = 64, 32, 3
+    K = synth.make_keys_block(4 * L, d, "gauss", 77).astype(np.float64)
+    for m in (1, 17, 63):
+        T = 3 * L + m
+        counts, means, factors = M.block_statistics(K, T, L, r)
+        assert counts.tolist() == [L, L, L, m]
+        np.testing.assert_allclose(means[3], np.mean(K[3 * L:T], axis=0), rtol=0, atol=1e-14)
+        assert np.all(factors[3] == 0.0)
+        for b in range(3):
+            assert np.all(np.linalg.norm(factors[b], axis=1) > 0.1)
+    counts, means, factors = M.block_statistics(K, 4 * L, L, r)
+    assert counts.tolist() == [L] * 4
+    # the filled block: top-r eigenpairs of the library's 1/n covariance (up to sign)
+    lam, U = np.linalg.eigh(np.cov(K[3 * L:].T, bias=True))
+    ref = (np.sqrt(lam[::-1][:r])[:, None] * U[:, ::-1][:, :r].T)
+    for i in range(r):
+        assert min(np.abs(factors[3, i] - ref[i]).max(), np.abs(factors[3, i] + ref[i]).max()) < 1e-10
+
+
 def test_gaussian_cgf_has_no_higher_cumulants():
     """eq. (cgf-expansion): for Gaussian keys ln E[exp(c q.x)] = c q.mu + c^2/2 q^T Sigma q.
 
