@@ -5,8 +5,10 @@
 // Executed by all 256 threads of a workgroup.  The block's keys are staged
 // transposed in LDS in their stored type and centred on the block mean as they
 // are read (fp32), and the 64 x 64 Gram matrix Gamma = Kc Kc^T / n is formed.
-// Its top-r eigenvectors come from a fixed-count block power iteration on
-// P = 16 (r <= 4) or 32 columns, re-orthonormalised by Cholesky-QR every step,
+// Its top-r eigenvectors come from a fixed-count block power iteration with
+// P = 16 (r <= 4) or 32 columns, re-orthonormalised by Cholesky-QR after one
+// product by Gamma in the first two steps and after two (Gamma^2) in the ten
+// that follow,
 // followed by a Rayleigh-Ritz step whose P x P eigenproblem is solved by
 // parallel cyclic Jacobi.  The scaled eigenvectors are xi_i = Kc^T w_i / sqrt(n)
 // (their squared norms are the Ritz values), with the sign that makes the
@@ -23,7 +25,8 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 namespace cobs {
 
 constexpr int kBuildThreads = 256;
-constexpr int kPowerIters = 16;
+constexpr int kPowerIters = 12;        // orthonormalisations
+constexpr int kSinglePowerIters = 2;   // the first ones after one product, the others after two
 constexpr int kJacobiSweeps = 4;
 
 // What the statistics of a block read and write.
@@ -234,10 +237,17 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
           acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, kc(e, 16 * ct + lr), acc[ct], 0, 0, 0);
       }
       const float inv_n = 1.0f / (float)n;
+      float diag = 0.0f;                 // this wave's part of the trace
 #pragma unroll
       for (int ct = 0; ct < kL / 16; ++ct)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) Gm[(16 * wave + 4 * lk + v) * kL + 16 * ct + lr] = acc[ct][v] * inv_n;
+        for (int v = 0; v < 4; ++v) {
+          const float g = acc[ct][v] * inv_n;
+          Gm[(16 * wave + 4 * lk + v) * kL + 16 * ct + lr] = g;
+          if (ct == wave && 4 * lk + v == lr) diag += g;
+        }
+      diag = wave_sum(diag);
+      if (lane == 0) red[wave] = diag;
     }
     for (int idx = tid; idx < kL * P; idx += NT) Wm[idx] = init_sign(idx / P, idx % P);
     __syncthreads();
@@ -245,11 +255,21 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     // Matrix products of the iteration on the fp32 matrix cores
     // (v_mfma_f32_16x16x4_f32: lane l holds A[l%16][l/16] and B[l/16][l%16] and
     // gets D[4(l/16)+v][l%16]).  Wave w owns rows [16w, 16w+16) of the 64 x P
-    // products.
+    // products.  After the first kSinglePowerIters steps each iteration applies
+    // Gamma twice before re-orthonormalising (power iteration on Gamma^2): the
+    // basis converges twice as fast per orthonormalisation.  The first steps
+    // use one product, so that from the random start the columns do not lose a
+    // direction whose eigenvalue is below a few percent of the largest (its
+    // pivot would scale with the fourth power).  Rayleigh-Ritz uses Gamma.
     const int lane = tid & 63, wave = tid >> 6;
     const int lr = lane & 15, lk = lane >> 4;
-    for (int it = 0; it <= kPowerIters; ++it) {
-      // ---- Y = Gamma W (Gamma symmetric: read by column, conflict free)
+    // The products use Gamma / trace(Gamma), eigenvalues in [0, 1], so that the
+    // fourth powers in Y^T Y stay far from the fp32 range at any key scale; the
+    // Ritz values are only compared with each other.
+    const float trace = red[0] + red[1] + red[2] + red[3];
+    const float gsc = trace > 0.0f ? 1.0f / trace : 0.0f;
+    // dst = (Gamma / trace) src (Gamma symmetric: read by column, conflict free)
+    auto gamma_times = [&](const float* src, float* dst) {
       if (lw) {
         f32x4_t acc[P / 16];
 #pragma unroll
@@ -259,15 +279,24 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
           const float a = Gm[(k0 + lk) * kL + 16 * wave + lr];
 #pragma unroll
           for (int ct = 0; ct < P / 16; ++ct)
-            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Wm[(k0 + lk) * P + 16 * ct + lr], acc[ct], 0, 0, 0);
+            acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, src[(k0 + lk) * P + 16 * ct + lr], acc[ct], 0, 0, 0);
         }
 #pragma unroll
         for (int ct = 0; ct < P / 16; ++ct)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) Ym[(16 * wave + 4 * lk + v) * P + 16 * ct + lr] = acc[ct][v];
+          for (int v = 0; v < 4; ++v) dst[(16 * wave + 4 * lk + v) * P + 16 * ct + lr] = acc[ct][v] * gsc;
       }
       __syncthreads();
+    };
+    float* Wp = Wm;                      // the current basis
+    float* Yp = Ym;                      // its image
+    for (int it = 0; it <= kPowerIters; ++it) {
+      gamma_times(Wp, Yp);
       if (it == kPowerIters) break;      // last product feeds the Rayleigh-Ritz step
+      if (it >= kSinglePowerIters) {
+        gamma_times(Yp, Wp);             // Gamma^2 W, into the basis buffer
+        float* t = Wp; Wp = Yp; Yp = t;
+      }
 
       // ---- S = Y^T Y, 16 x 16 tiles spread over the four waves
       for (int tl = wave; lw && tl < (P / 16) * (P / 16); tl += kBuildThreads / 64) {
@@ -275,24 +304,31 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
         f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll 4
         for (int k0 = 0; k0 < kL; k0 += 4)
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Ym[(k0 + lk) * P + 16 * ta + lr],
-                                                     Ym[(k0 + lk) * P + 16 * tc + lr], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Yp[(k0 + lk) * P + 16 * ta + lr],
+                                                     Yp[(k0 + lk) * P + 16 * tc + lr], acc, 0, 0, 0);
 #pragma unroll
         for (int v = 0; v < 4; ++v) Sm[(16 * ta + 4 * lk + v) * (P + 1) + 16 * tc + lr] = acc[v];
       }
       __syncthreads();
-      // ---- S = L L^T (Cholesky) and X = L^-1, in wave 0: lane k < P holds row k
-      // of L, then column k of X; a pivot below 1e-6 trace (rank deficit) gives a
-      // zero column
+      // ---- Cholesky of the column-normalised S' = N S N (N = diag(S)^-1/2),
+      // S' = L L^T, and X = L^-1, in wave 0: lane k < P holds row k of L, then
+      // column k of X.  A pivot of S' below 1e-6 (column k nearly inside the
+      // span of the earlier ones, whatever its length) gives a zero column, so
+      // a direction of small eigenvalue is kept as long as it is independent.
       if (wave == 0) {
-        float row[P];
+        float row[P], rn[P];
         const int li = lane < P ? lane : 0;
 #pragma unroll
-        for (int c = 0; c < P; ++c) row[c] = Sm[li * (P + 1) + c];
-        float trace = 0.0f;
+        for (int c = 0; c < P; ++c) {
+          const float dc = Sm[c * (P + 1) + c];
+          rn[c] = dc > 0.0f ? 1.0f / sqrtf(dc) : 0.0f;
+        }
+        float rnl = rn[0];
 #pragma unroll
-        for (int c = 0; c < P; ++c) trace += Sm[c * (P + 1) + c];
-        const float thr = 1e-6f * trace;
+        for (int c = 1; c < P; ++c) rnl = (c == li) ? rn[c] : rnl;
+#pragma unroll
+        for (int c = 0; c < P; ++c) row[c] = Sm[li * (P + 1) + c] * rnl * rn[c];
+        const float thr = 1e-6f;
         float rd[P];
 #pragma unroll
         for (int k = 0; k < P; ++k) {
@@ -319,9 +355,10 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
             acc -= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[m]), k)) * x[m];
           x[k] = acc * rd[k];
         }
+        // W = Y N X^T: lane c stores X[k][c] N_cc at Lm[c][k]
         if (lane < P) {
 #pragma unroll
-          for (int k = 0; k < P; ++k) Lm[lane * (P + 1) + k] = x[k];     // Lm[c][k] = X[k][c]
+          for (int k = 0; k < P; ++k) Lm[lane * (P + 1) + k] = x[k] * rnl;
         }
       }
       __syncthreads();
@@ -332,7 +369,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
         for (int ct = 0; ct < P / 16; ++ct) acc[ct] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int k0 = 0; k0 < P; k0 += 4) {
-          const float a = Ym[(16 * wave + lr) * P + k0 + lk];
+          const float a = Yp[(16 * wave + lr) * P + k0 + lk];
 #pragma unroll
           for (int ct = 0; ct < P / 16; ++ct)
             acc[ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, Lm[(k0 + lk) * (P + 1) + 16 * ct + lr], acc[ct], 0, 0, 0);
@@ -340,7 +377,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
 #pragma unroll
         for (int ct = 0; ct < P / 16; ++ct)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) Wm[(16 * wave + 4 * lk + v) * P + 16 * ct + lr] = acc[ct][v];
+          for (int v = 0; v < 4; ++v) Wp[(16 * wave + 4 * lk + v) * P + 16 * ct + lr] = acc[ct][v];
       }
       __syncthreads();
     }
@@ -350,8 +387,8 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       const int a = idx / P, c = idx % P;
       float s1 = 0.0f, s2 = 0.0f;
       for (int i = 0; i < kL; ++i) {
-        s1 += Wm[i * P + a] * Ym[i * P + c];
-        s2 += Wm[i * P + c] * Ym[i * P + a];
+        s1 += Wp[i * P + a] * Yp[i * P + c];
+        s2 += Wp[i * P + c] * Yp[i * P + a];
       }
       Hm[0][a * (P + 1) + c] = 0.5f * (s1 + s2);
       Vm[0][a * (P + 1) + c] = (a == c) ? 1.0f : 0.0f;
@@ -412,8 +449,8 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       const int i = idx / kL, row = idx % kL;
       const int col = order[i];
       float s = 0.0f;
-      for (int a = 0; a < P; ++a) s += Wm[row * P + a] * Vm[cur][a * (P + 1) + col];
-      Ym[i * kL + row] = s;
+      for (int a = 0; a < P; ++a) s += Wp[row * P + a] * Vm[cur][a * (P + 1) + col];
+      Yp[i * kL + row] = s;
     }
     __syncthreads();
     const float rs = 1.0f / sqrtf((float)n);
@@ -422,7 +459,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       const int i = idx / D, e = idx % D;
       float s = 0.0f;
       if (ritzval[i] > 1e-6f * top && top > 0.0f) {
-        for (int row = 0; row < kL; ++row) s += kc(e, row) * Ym[i * kL + row];
+        for (int row = 0; row < kL; ++row) s += kc(e, row) * Yp[i * kL + row];
         s *= rs;
       }
       Xi[i * D + e] = s;
