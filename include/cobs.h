@@ -219,6 +219,27 @@ cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const c
                                const int32_t* seq_lens, void* summaries, int32_t* sel,
                                float* out, float* lse, void* ws, size_t ws_bytes, void* stream);
 
+/* Size of the library's own workspace for cobs_decode_step_noalloc, per GPU. */
+#define COBS_NOALLOC_SCRATCH_BYTES (32u << 20)
+
+/* cobs_decode_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The workspace is a static device array
+ * of the library, COBS_NOALLOC_SCRATCH_BYTES on every GPU the library runs on,
+ * held until the process ends; the call itself allocates nothing.
+ *   Arguments and results: as for cobs_decode_step.
+ *   Errors: COBS_ERR_WORKSPACE if cobs_workspace_bytes(cfg, COBS_OP_STEP)
+ *   exceeds COBS_NOALLOC_SCRATCH_BYTES (32 MiB holds e.g. B = 32, Hq = 32,
+ *   Hkv = 8, T_max = 32768, budget 85; B = 8, Hq = 64, Hkv = 8, T_max = 131072);
+ *   COBS_ERR_HIP if the array's address cannot be obtained.
+ *   Each call first clears its arrival counters in the array (one extra small
+ *   launch), so a call needs no state from the previous one.  Every call on one
+ *   GPU uses the same array: calls that overlap in time on one GPU (different
+ *   streams, or host threads) race and must be serialised by the caller.      */
+cobs_status_t cobs_decode_step_noalloc(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                       const int32_t* seq_lens, void* summaries, int32_t* sel,
+                                       float* out, float* lse, void* stream);
+
 /* FP4 E2M1 encoder used for descriptor storage (Sec. 5.5), exposed so the
  * rounding rule can be checked on its own.
  *   x:      device fp32 [num_vectors, dim], dim even, 2 <= dim <= 4096.

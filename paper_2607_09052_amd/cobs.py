@@ -53,6 +53,7 @@ _SIGS = {
     "cobs_sparse_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_sparse_decode_branches": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_decode_step": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
+    "cobs_decode_step_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "cobs_pack_e2m1": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P]),
     "cobs_status_string": (ctypes.c_char_p, [ctypes.c_int]),
 }
@@ -317,6 +318,19 @@ def cobs_decode_step(cfg, q, k, v, seq_lens, summaries, out, ws, sel=None, lse=N
     _check(lib().cobs_decode_step(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
                                   _ptr(seq_lens), _ptr(summaries), _ptr(sel), _ptr(out), _ptr(lse),
                                   _ptr(ws), nws, _stream(stream, q)))
+
+
+def cobs_decode_step_noalloc(cfg, q, k, v, seq_lens, summaries, out, sel=None, lse=None,
+                             block_table=None, num_pages=0, stream=None):
+    """cobs_decode_step on the library's own per-GPU workspace (no ws argument)."""
+    _decode_io(cfg, q, seq_lens, sel, dict(out=out), dict(lse=lse), sel_required=False)
+    _summaries(cfg, summaries)
+    kv = _kv(cfg, k, v, block_table, num_pages)
+    _same_gpu(q=q, k=k, v=v, seq_lens=seq_lens, summaries=summaries, sel=sel, out=out, lse=lse,
+              block_table=block_table)
+    _check(lib().cobs_decode_step_noalloc(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
+                                          _ptr(seq_lens), _ptr(summaries), _ptr(sel), _ptr(out), _ptr(lse),
+                                          _stream(stream, q)))
 
 
 def cobs_pack_e2m1(x, codes, scales, stream=None):

@@ -249,6 +249,65 @@ cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
   return hip_status(launch_decode(p, v.d, v.G, v.kv_f32 != 0, v.B, v.nbmax, st));
 }
 
+cobs_status_t check_step(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                         const int32_t* seq_lens, void* summaries, float* out) {
+  cobs_status_t s = check_config(cfg);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if ((s = check_kv(kv, v)) != COBS_OK) return s;
+  if (!q || !seq_lens || !summaries || !out || !aligned(summaries, 16)) return COBS_ERR_INVALID_ARG;
+  return COBS_OK;
+}
+
+// One decode step on the workspace `wsb` (selector region, then decode
+// region, then the selection when the caller passes none).
+cobs_status_t run_step(const Derived& v, const float* q, const cobs_kv_t* kv, const int32_t* seq_lens,
+                       void* summaries, int32_t* sel, float* out, float* lse, uint8_t* wsb, hipStream_t st) {
+  cobs_status_t s;
+  int32_t* selp = sel ? sel : reinterpret_cast<int32_t*>(wsb + v.step_sel);
+  if (select_refreshes(v.r, v.kv_f32 != 0)) {
+    // the selector's launch recomputes the newest block's record before scoring
+    if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st, kv)) != COBS_OK) return s;
+    return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
+  }
+  if ((s = run_build(v, kv, seq_lens, 0, 0, true, summaries, st)) != COBS_OK) return s;
+  if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st)) != COBS_OK) return s;
+  return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
+}
+
+// Zero two arrays of arrival counters (one workgroup).
+__global__ void zero_counters_kernel(unsigned* a, int na, unsigned* b, int nb) {
+  for (int i = threadIdx.x; i < na; i += blockDim.x) a[i] = 0u;
+  for (int i = threadIdx.x; i < nb; i += blockDim.x) b[i] = 0u;
+}
+
+}  // namespace
+
+// Workspace of cobs_decode_step_noalloc: device memory of the library itself,
+// one copy per GPU, held until the process ends.  Host code never uses this
+// name as an address (on the host it is only a handle for the symbol lookup):
+// the device address of each GPU's copy comes from hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[COBS_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+// Device address of the current GPU's scratch, looked up once per device.
+cobs_status_t scratch_address(uint8_t** out) {
+  static std::mutex mu;
+  static std::map<int, uint8_t*> addr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return COBS_ERR_HIP;
+  std::lock_guard<std::mutex> lock(mu);
+  auto it = addr.find(dev);
+  if (it == addr.end()) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return COBS_ERR_HIP;
+    it = addr.emplace(dev, static_cast<uint8_t*>(ptr)).first;
+  }
+  *out = it->second;
+  return COBS_OK;
+}
+
 }  // namespace
 
 namespace cobs {
@@ -391,24 +450,31 @@ cobs_status_t cobs_sparse_decode_branches(const cobs_config_t* cfg, const float*
 cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
                                const int32_t* seq_lens, void* summaries, int32_t* sel, float* out,
                                float* lse, void* ws, size_t ws_bytes, void* stream) {
-  cobs_status_t s = check_config(cfg);
+  cobs_status_t s = check_step(cfg, q, kv, seq_lens, summaries, out);
   if (s != COBS_OK) return s;
   const Derived v = derive(cfg);
-  if ((s = check_kv(kv, v)) != COBS_OK) return s;
-  if (!q || !seq_lens || !summaries || !out || !aligned(summaries, 16)) return COBS_ERR_INVALID_ARG;
   if ((s = check_ws(ws, ws_bytes, v.step_bytes)) != COBS_OK) return s;
-  uint8_t* wsb = static_cast<uint8_t*>(ws);
-  // the selection goes to the caller's buffer if given, else to the workspace
-  int32_t* selp = sel ? sel : reinterpret_cast<int32_t*>(wsb + v.step_sel);
+  return run_step(v, q, kv, seq_lens, summaries, sel, out, lse, static_cast<uint8_t*>(ws),
+                  static_cast<hipStream_t>(stream));
+}
+
+cobs_status_t cobs_decode_step_noalloc(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
+                                       const int32_t* seq_lens, void* summaries, int32_t* sel, float* out,
+                                       float* lse, void* stream) {
+  cobs_status_t s = check_step(cfg, q, kv, seq_lens, summaries, out);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if (v.step_bytes > (size_t)COBS_NOALLOC_SCRATCH_BYTES) return COBS_ERR_WORKSPACE;
+  uint8_t* wsb = nullptr;
+  if ((s = scratch_address(&wsb)) != COBS_OK) return s;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (select_refreshes(v.r, v.kv_f32 != 0)) {
-    // the selector's launch recomputes the newest block's record before scoring
-    if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st, kv)) != COBS_OK) return s;
-    return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
-  }
-  if ((s = run_build(v, kv, seq_lens, 0, 0, true, summaries, st)) != COBS_OK) return s;
-  if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st)) != COBS_OK) return s;
-  return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
+  // the scratch keeps whatever the last call on this GPU left there: clear the
+  // arrival counters of this call's layout first
+  hipLaunchKernelGGL(zero_counters_kernel, dim3(1), dim3(256), 0, st,
+                     reinterpret_cast<unsigned*>(wsb + v.sel_cnt), v.units,
+                     reinterpret_cast<unsigned*>(wsb + v.sel_bytes + v.dec_cnt), v.units);
+  if ((s = hip_status(hipGetLastError())) != COBS_OK) return s;
+  return run_step(v, q, kv, seq_lens, summaries, sel, out, lse, wsb, st);
 }
 
 cobs_status_t cobs_pack_e2m1(const float* x, int64_t num_vectors, int32_t dim, uint8_t* codes,

@@ -24,7 +24,7 @@ def _declared_functions():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared_functions()
-    assert len(declared) == 11, declared
+    assert len(declared) == 12, declared
     lib = cobs.lib()
     for name in declared:
         assert hasattr(lib, name), name
@@ -162,3 +162,18 @@ def test_binding_rejects_tensors_the_kernels_would_misread():
     rejects(dec, cfg, q, k[:, :, :512], k[:, :, :512], seq, sel, out, ws, match="smaller than")
     rejects(dec, cfg, q, k, k, seq, sel, out, ws, block_table=torch.zeros((B, 16), dtype=torch.int32),
             num_pages=4, match="paged k must be")
+
+
+def test_noalloc_step_rejects_problems_beyond_its_scratch():
+    """cobs_decode_step_noalloc refuses, on the host, a problem whose step
+    workspace exceeds the library's per-GPU array."""
+    lib = cobs.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    kv = cobs._KV(fake.value, fake.value, 1 << 24, 1 << 21, 128, None, 0)
+    big = _cfg(batch=64, num_q_heads=64, num_kv_heads=8, max_seq_len=131072, budget=85, window=1024,
+               mean_dtype="e2m1", factor_dtype="e2m1")
+    assert cobs.workspace_bytes(big, cobs.OP_STEP) > 32 << 20
+    assert lib.cobs_decode_step_noalloc(ctypes.byref(big.c_struct()), fake, ctypes.byref(kv), fake, fake, None,
+                                        fake, None, None) == 3
+    assert lib.cobs_decode_step_noalloc(ctypes.byref(_cfg().c_struct()), None, ctypes.byref(kv), fake, fake,
+                                        None, fake, None, None) == 1
