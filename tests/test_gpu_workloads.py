@@ -41,7 +41,7 @@ DECISION_BAND = {"f32": 2e-3, "bf16": 4e-3, "e2m1": 2e-2}
 # Largest share of selected block ids allowed to differ between the GPU's and
 # the oracle's independently built descriptors (boundary blocks whose scores
 # lie within the band above).
-ID_DIFF_BOUND = {"f32": 0.05, "bf16": 0.05, "e2m1": 0.15}
+ID_DIFF_BOUND = {"f32": 0.01, "bf16": 0.01, "e2m1": 0.02}
 
 
 def _oracle_stats(K, T, cfg):
