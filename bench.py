@@ -1,6 +1,6 @@
 """Decode-step benchmark of the COBS path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload c2] [--copies M]
+    python bench.py [--steps K] [--warmup W] [--workloads c3,c2,c4,c5] [--copies M]
                     [--no-cpu-baseline] [--traffic FILE] [--calibrate-copy MIB]
 
 One step = one cobs_decode_step call on one layer: refresh of the record of the
@@ -8,23 +8,29 @@ block holding the newest token, block scoring + top-s selection, and sparse
 attention over the selected blocks plus the window, for every batch row and
 KV head.  Inputs are seeded synthetic tensors resident in HBM before timing.
 
+The first workload (default c3: B=32, 32k context, the largest single-GPU
+configuration at 32k) gives the headline line; the others (c2, c4, c5) are
+reported under "workloads" with the same fields.  For each workload:
+
 The timed loop is a decode loop: every step appends one token, so the context
 of each layer copy advances by one per step through T_hi-63 .. T_hi (one full
 fill of the newest block, T_hi the workload's context) and wraps; the copies
-start at staggered phases, so over any window of steps one in 64 is the step
-that fills a block and recomputes its covariance factors (the other steps
-refresh the partial block's mean).  To measure HBM rather than the 256 MB
-last-level cache the steps rotate over M independent copies of the layer (K/V
-cache, descriptors, queries) that together read >= 2 GB per sweep.  A sweep
-(one step per copy plus the context advance) is captured once as a HIP graph
-and replayed, so host launch overhead is not in the measurement.
+start at staggered phases, so one step in 64 is the step that fills a block
+and recomputes its covariance factors (the other steps refresh the partial
+block's mean).  To measure HBM rather than the 256 MB last-level cache the
+steps rotate over M independent copies of the layer (K/V cache, descriptors,
+queries) that together read >= 2 GB per sweep.  Steps are replayed from HIP
+graphs (a whole sweep, and a partial sweep for the remainder), so exactly W
+untimed and then exactly K timed steps run, without host launch overhead;
+fill_cycle_us is the mean over all 64 phases from a longer replay.
 
-Prints one JSON line: the metric (us per decode step per layer), achieved GB/s
-on the step's algorithmic bytes, the roofline of the dominant kernel (timed on
-its own the same way, HIP events on the launch stream) and the fp64 oracle's
-time on the host cores as a baseline.  config.eager_call_us adds per-call
-median / p10 / p90 of eager (not graph) steps, launch included: steady, over
-the rotating copies, and cold, after a 1 GiB read that evicts the caches.
+Each workload reports the metric (us per decode step per layer), GB/s on the
+step's algorithmic bytes, the roofline of its dominant kernel (timed on its own
+the same way, HIP events on the launch stream) and the fp64 oracle's time on
+the host cores as a baseline (all cores and one thread).  config.eager_call_us
+adds per-call median / p10 / p90 of eager (not graph) steps, launch included:
+steady, over the rotating copies, and cold, after a 1 GiB read that evicts the
+caches; read_ceiling_gbps is the rate of that 1 GiB read itself.
 """
 
 import argparse
@@ -131,21 +137,25 @@ def measured_traffic(path, workload, kernel):
 def prefill_summary(cfg, B, T, ms):
     """Block-statistics build of a whole cache of T tokens: time, bytes and flops.
 
-    Flops are those of the method as built here, per full block: the centred
-    Gram matrix (2 L^2 d), the subspace iteration on it (kPowerIters + 1
-    products Gamma W of 2 L^2 P flops, and per re-orthonormalisation Y^T Y and
-    Y X^T, 2 L P^2 each), the Rayleigh-Ritz product (2 L P^2) and the factors
-    xi = Kc^T w (2 L d r); P = 16 columns for r <= 4, 32 beyond.
+    Flops are the method's own work per full block (Sec. 5.6): the centred Gram
+    matrix, 2 L^2 d; the small symmetric eigenproblem, counted as the (4/3) L^3
+    of reducing an L x L matrix to tridiagonal form; and the factors
+    xi = Kc^T w, 2 L d r.  The fixed-count subspace iteration that stands in for
+    the eigensolver here executes more (see executed_mflop_per_block).
     """
     L, d, r = 64, cfg.head_dim, cfg.rank
     P = 16 if r <= 4 else 32
-    iters = 16
     full = B * cfg.num_kv_heads * (T // L)
     blocks = B * cfg.num_kv_heads * (-(-T // L))
-    per_block = 2 * L * L * d + (iters + 1) * 2 * L * L * P + iters * 4 * L * P * P + 2 * L * P * P + 2 * L * d * r
+    method = 2 * L * L * d + 4 * L ** 3 / 3 + 2 * L * d * r
+    # as built: Gram, 2 single + 10 double products Gamma W (23 with the last),
+    # 12 re-orthonormalisations (Y^T Y and Y X^T), Rayleigh-Ritz, factors
+    executed = 2 * L * L * d + 23 * 2 * L * L * P + 12 * 4 * L * P * P + 2 * L * P * P + 2 * L * d * r
     kbytes = B * cfg.num_kv_heads * T * d * ESZ[cfg.kv_dtype] + blocks * cobs.record_bytes(cfg)
     return {"us": round(ms * 1e3, 1), "blocks": blocks, "full_blocks": full,
-            "gflops": round(full * per_block / (ms * 1e-3) / 1e9, 1), "gbps": round(kbytes / (ms * 1e-3) / 1e9, 1)}
+            "gflops": round(full * method / (ms * 1e-3) / 1e9, 1), "method_mflop_per_block": round(method / 1e6, 3),
+            "executed_mflop_per_block": round(executed / 1e6, 3),
+            "gbps": round(kbytes / (ms * 1e-3) / 1e9, 1)}
 
 
 def replay_time(graph, reps, stream):
@@ -205,15 +215,28 @@ def needle_recall(prob, cfg, seq, dev):
     return out
 
 
-def cpu_baseline(prob, cfg, t_lo, budget_s=12.0):
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(prob, cfg, t_lo, budget_s=8.0, budget_1t_s=4.0):
     """The fp64 oracle's decode step on the host cores, on a bounded sample.
 
     Untimed: the oracle builds its own descriptors for two (batch row, KV head)
     units.  Timed per unit-step, cycling the context through the same block-fill
     cycle as the GPU loop: refresh of the tail block's statistics (factors
     when it is full), scoring, top-s and sparse attention.  Scaled to one step
-    of the whole layer (all units).
+    of the whole layer (all units).  Run with numpy/BLAS on every host core the
+    process may use, then on one thread.
     """
+    from threadpoolctl import threadpool_limits
     from oracle import method as M
     c = prob["cfg"]
     G = c["Hq"] // c["Hkv"]
@@ -228,60 +251,58 @@ def cpu_baseline(prob, cfg, t_lo, budget_s=12.0):
         stats = M.stored_statistics(*M.block_statistics(K, T_hi, L, r), cfg.mean_dtype, cfg.factor_dtype)
         prepared.append((q, K, V, [np.array(x) for x in stats]))
     prep_s = time.time() - t_prep
-    n = 0
-    t0 = time.time()
-    while time.time() - t0 < budget_s:
-        q, K, V, stats = prepared[n % len(prepared)]
-        T = t_lo + (n // len(prepared)) % CYCLE
-        j = (T - 1) // L
-        tail = M.stored_statistics(*M.block_statistics(K[j * L:T], T - j * L, L, r),
-                                   cfg.mean_dtype, cfg.factor_dtype)
-        for arr, x in zip(stats, tail):
-            arr[j] = x[0]
-        nb = -(-T // L)
-        M.decode_unit(q, K, V, T, L, r, cfg.budget, cfg.window, cfg.scale, cfg.mean_dtype,
-                      cfg.factor_dtype, stats=tuple(a[:nb] for a in stats))
-        n += 1
-    per_unit = (time.time() - t0) / n
+
+    def run(budget):
+        n = 0
+        t0 = time.time()
+        while time.time() - t0 < budget:
+            q, K, V, stats = prepared[n % len(prepared)]
+            T = t_lo + (n // len(prepared)) % CYCLE
+            j = (T - 1) // L
+            tail = M.stored_statistics(*M.block_statistics(K[j * L:T], T - j * L, L, r),
+                                       cfg.mean_dtype, cfg.factor_dtype)
+            for arr, x in zip(stats, tail):
+                arr[j] = x[0]
+            nb = -(-T // L)
+            M.decode_unit(q, K, V, T, L, r, cfg.budget, cfg.window, cfg.scale, cfg.mean_dtype,
+                          cfg.factor_dtype, stats=tuple(a[:nb] for a in stats))
+            n += 1
+        return (time.time() - t0) / n, n
+
+    per_unit, n = run(budget_s)
+    with threadpool_limits(limits=1):
+        per_unit_1t, n1 = run(budget_1t_s)
     cores = len(os.sched_getaffinity(0))
     return {"value": round(per_unit * len(units) * 1e6, 1), "unit": "us/step/layer", "cores": cores,
-            "kind": "oracle",
-            "sample": f"{n} unit-steps of 2 of the {len(units)} (batch row, KV head) units, T cycling "
-                      f"{t_lo}..{t_lo + CYCLE - 1}, in {per_unit * n:.1f} s, scaled x{len(units)}; "
-                      f"descriptor prefill ({prep_s:.1f} s) untimed; numpy/BLAS on {cores} host cores"}
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "value_1_thread": round(per_unit_1t * len(units) * 1e6, 1),
+            "sample": f"{n} unit-steps ({n1} on one thread) of 2 of the {len(units)} (batch row, KV head) "
+                      f"units, T cycling {t_lo}..{t_lo + CYCLE - 1}, {per_unit * n:.1f} s "
+                      f"({per_unit_1t * n1:.1f} s on one thread), scaled x{len(units)}; descriptor prefill "
+                      f"({prep_s:.1f} s) untimed; numpy/BLAS on {cores} host cores, then on 1"}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=200)
-    ap.add_argument("--workload", default="c2", choices=sorted(synth.CONFIGS))
-    ap.add_argument("--copies", type=int, default=0, help="layer copies to rotate (0: >= 2 GB per sweep)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic.txt"),
-                    help="rocprofv3 HBM traffic summary ('traffic <workload> <kernel> <read> <written>' lines)")
-    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
-                    help="only run a plain device copy of MIB MiB ten times (HBM counter calibration)")
-    args = ap.parse_args()
-    if args.calibrate_copy:
-        n = args.calibrate_copy * (1 << 20) // 4
-        src = torch.randn(n, device="cuda:0")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        for _ in range(10):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "copies": 10}), flush=True)
-        return
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported here (the decode step "
-              "shards by KV head or batch row with no communication)", file=sys.stderr)
-        sys.exit(2)
+def timed_steps(g_full, g_part, copies, k, stream):
+    """Run exactly k decode steps from the sweep graphs (k // copies whole
+    sweeps, then a partial sweep of k % copies steps); microseconds in total
+    from HIP events on `stream`, or None for k = 0."""
+    if k <= 0:
+        return None
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(k // copies):
+        g_full.replay()
+    if k % copies:
+        g_part[k % copies].replay()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) * 1e3
 
-    dev = "cuda:0"
-    torch.cuda.set_device(0)
-    name = args.workload
+
+def run_workload(name, args, dev, with_cpu):
+    """Every measurement of one workload; returns its result fields."""
     prob = synth.make_problem(name, device=dev, steps=0)
     c = prob["cfg"]
     cfg = cobs.Config(batch=c["B"], num_q_heads=c["Hq"], num_kv_heads=c["Hkv"], head_dim=c["d"],
@@ -317,6 +338,7 @@ def main():
     wss = [cobs.new_workspace(cfg, cobs.OP_STEP, dev) for _ in layers]
     sel_ws = [cobs.new_workspace(cfg, cobs.OP_SELECT, dev) for _ in layers]
     dec_ws = [cobs.new_workspace(cfg, cobs.OP_DECODE, dev) for _ in layers]
+    osa_ws = [cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, dev) for _ in layers]
     torch.cuda.synchronize()
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
@@ -324,9 +346,13 @@ def main():
     def advance():
         seqs.sub_(t_lo - 1).remainder_(CYCLE).add_(t_lo)
 
+    def one_step(i):
+        q, k, v, r_ = layers[i]
+        cobs.cobs_decode_step(cfg, q, k, v, seqs[i], r_, out, wss[i], sel=sels[i], lse=lse, stream=stream)
+
     def sweep_step():
-        for i, (q, k, v, r_) in enumerate(layers):
-            cobs.cobs_decode_step(cfg, q, k, v, seqs[i], r_, out, wss[i], sel=sels[i], lse=lse, stream=stream)
+        for i in range(copies):
+            one_step(i)
         advance()
 
     def sweep_select():
@@ -342,8 +368,6 @@ def main():
             cobs.cobs_build_block_stats(cfg, k, v, seqs[i], r_, first_block=cfg.num_blocks - 1, num_blocks=1,
                                         stream=stream)
 
-    osa_ws = [cobs.new_workspace(cfg, cobs.OP_SELECT_EXACT, dev) for _ in layers]
-
     def sweep_osa():
         for i, (q, k, v, r_) in enumerate(layers):
             cobs.cobs_select_exact(cfg, q, k, v, seqs[i], sels[i], osa_ws[i], stream=stream)
@@ -356,28 +380,34 @@ def main():
         fn()
     torch.cuda.synchronize()
     g_step = capture(sweep_step, stream)
-    reps_w = max(1, math.ceil(args.warmup / copies))
-    reps = max(1, math.ceil(args.steps / copies))
-    for _ in range(reps_w):
-        g_step.replay()
-    us_sweep = replay_time(g_step, reps, stream)
-    steps = reps * copies
-    us_step = us_sweep / copies
+    # partial sweeps: the first j steps of a sweep (no context advance)
+    parts = sorted({args.steps % copies, args.warmup % copies} - {0})
+    g_part = {j: capture(lambda j=j: [one_step(i) for i in range(j)], stream) for j in parts}
+    torch.cuda.synchronize()
+    timed_steps(g_step, g_part, copies, args.warmup, stream)            # exactly W untimed steps
+    us_total = timed_steps(g_step, g_part, copies, args.steps, stream)  # exactly K timed steps
+    us_step = us_total / args.steps
+    # the mean over the whole fill cycle (every copy through all 64 phases)
+    cyc_reps = max(2, math.ceil(CYCLE * 2 / copies))
+    fill_cycle_us = replay_time(g_step, cyc_reps, stream) / copies
+    reps = max(4, math.ceil(400 / copies))
     # per-kernel averages and the fixed-context fill step, same protocol
     kern_us = {}
     for key, fn in (("select_kernel", sweep_select), ("decode_kernel", sweep_decode),
                     ("build_stats_kernel", sweep_tail)):
         g = capture(fn, stream)
         g.replay()
-        kern_us[key] = replay_time(g, max(2, reps // 2), stream) / copies
+        kern_us[key] = replay_time(g, reps, stream) / copies
+        del g
     g_fill = capture(sweep_fill, stream)
     g_fill.replay()
-    fill_us = replay_time(g_fill, max(2, reps // 4), stream) / copies
+    fill_us = replay_time(g_fill, max(2, reps // 2), stream) / copies
     # the exact-mass (OSA) selector, same protocol: it reads every key once
     g_osa = capture(sweep_osa, stream)
     g_osa.replay()
-    osa_us = replay_time(g_osa, max(2, reps // 4), stream) / copies
+    osa_us = replay_time(g_osa, max(2, reps // 2), stream) / copies
     osa_bytes = ab["keys"]
+    del g_fill, g_osa
     # prefill: statistics of every block of the cache (one layer copy), eager launches
     r_pre = torch.empty_like(rec)
     pre_ms = []
@@ -390,14 +420,10 @@ def main():
         if it > 0:
             pre_ms.append(e0.elapsed_time(e1))
     del r_pre
+
     # per-call distributions, eager launches timed one by one with HIP events on
     # the launch stream: steady (rotating layer copies, as in the timed loop) and
-    # cold (a 1 GiB write between calls evicts the caches)
-    def one_call(i):
-        q, k, v, r_ = layers[i % copies]
-        cobs.cobs_decode_step(cfg, q, k, v, seqs[i % copies], r_, out, wss[i % copies], sel=sels[i % copies],
-                              lse=lse, stream=stream)
-
+    # cold (a 1 GiB read between calls evicts the caches)
     def per_call(n, before=None):
         xs = []
         for i in range(n):
@@ -405,7 +431,7 @@ def main():
                 before(i)
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
-            one_call(i)
+            one_step(i % copies)
             e1.record(stream)
             e1.synchronize()
             xs.append(e0.elapsed_time(e1) * 1e3)
@@ -415,10 +441,20 @@ def main():
     n_calls = max(64, min(400, 4 * copies))
     steady = per_call(n_calls)
     # the eviction reads 1 GiB (a write would leave the caches full of dirty
-    # lines whose write-back would then land in the timed call)
+    # lines whose write-back would then land in the timed call); its own rate
+    # is the streaming-read ceiling reported beside the results
     flush = torch.ones(256 * 1024 * 1024, dtype=torch.float32, device=dev)
     sink = torch.empty((), dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
+    read_us = []
+    for _ in range(6):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        torch.amax(flush, dim=0, out=sink)
+        e1.record(stream)
+        e1.synchronize()
+        read_us.append(e0.elapsed_time(e1) * 1e3)
+    read_gbps = flush.numel() * 4 / (float(np.median(read_us[1:])) * 1e-6) / 1e9
     cold = per_call(min(n_calls, 100), before=lambda i: torch.amax(flush, dim=0, out=sink))
     del flush, sink
     torch.cuda.set_stream(torch.cuda.default_stream())
@@ -429,18 +465,10 @@ def main():
     traffic = measured_traffic(args.traffic, name, dom)
     gbps = ab["step"] / (us_step * 1e-6) / 1e9
     res = {
-        "metric": METRIC,
         "value": round(us_step, 3),
-        "unit": "us/step/layer",
-        "n_gpus": 1,
-        "steps": steps,
-        "warmup": reps_w * copies,
+        "steps": args.steps,
+        "warmup": args.warmup,
         "ms_per_step": round(us_step / 1e3, 6),
-        "higher_is_better": False,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
         "achieved_gbps": round(gbps, 1),
         "hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
         "config": {
@@ -450,9 +478,12 @@ def main():
                         f"{c['factor_dtype']} factors",
             "bytes_per_step": round(ab["step"]),
             "layer_copies_rotated": copies,
+            "fill_cycle_us": round(fill_cycle_us, 3),
+            "fill_cycle_gbps": round(ab["step"] / (fill_cycle_us * 1e-6) / 1e9, 1),
             "kernels_us": {k_: round(v_, 3) for k_, v_ in kern_us.items()},
             "fill_step_us": round(fill_us, 3),
             "eager_call_us": {"steady": steady, "cold": cold},
+            "read_ceiling_gbps": round(read_gbps, 1),
             "osa_select": {"us": round(osa_us, 3), "key_bytes": round(osa_bytes),
                            "gbps": round(osa_bytes / (osa_us * 1e-6) / 1e9, 1),
                            "frac": round(osa_bytes / (osa_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)},
@@ -466,9 +497,80 @@ def main():
     }
     if "needles" in prob and prob["needles"]:
         res["config"]["needle_recall"] = needle_recall(prob, cfg, seq_hi, dev)
-    if not args.no_cpu_baseline:
+    if with_cpu:
         res["cpu_baseline"] = cpu_baseline(prob, cfg, t_lo)
-    print(json.dumps(res), flush=True)
+    del layers, prob, rec, wss, sel_ws, dec_ws, osa_ws, g_step, g_part
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--workloads", default="c3,c2,c4,c5",
+                    help="comma-separated workloads; the first is the headline line")
+    ap.add_argument("--copies", type=int, default=0, help="layer copies to rotate (0: >= 2 GB per sweep)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic.txt"),
+                    help="rocprofv3 HBM traffic summary ('traffic <workload> <kernel> <read> <written>' lines)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB ten times (HBM counter calibration)")
+    args = ap.parse_args()
+    if args.calibrate_copy:
+        n = args.calibrate_copy * (1 << 20) // 4
+        src = torch.randn(n, device="cuda:0")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "copies": 10}), flush=True)
+        return
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported here (the decode step "
+              "shards by KV head or batch row with no communication)", file=sys.stderr)
+        sys.exit(2)
+    if args.steps < 1 or args.warmup < 0:
+        print("--steps must be >= 1 and --warmup >= 0", file=sys.stderr)
+        sys.exit(2)
+    names = [w.strip() for w in args.workloads.split(",") if w.strip()]
+    for w in names:
+        if w not in synth.CONFIGS:
+            print(f"unknown workload {w}; choose from {sorted(synth.CONFIGS)}", file=sys.stderr)
+            sys.exit(2)
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    results = {}
+    for w in names:
+        print(f"bench: workload {w}", file=sys.stderr, flush=True)
+        results[w] = run_workload(w, args, dev, with_cpu=not args.no_cpu_baseline)
+    head = results[names[0]]
+    line = {
+        "metric": METRIC,
+        "value": head["value"],
+        "unit": "us/step/layer",
+        "n_gpus": 1,
+        "steps": head["steps"],
+        "warmup": head["warmup"],
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "achieved_gbps": head["achieved_gbps"],
+        "hbm_frac": head["hbm_frac"],
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "cpu_baseline": head["cpu_baseline"],
+    }
+    if len(names) > 1:
+        line["workloads"] = {w: results[w] for w in names[1:]}
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":

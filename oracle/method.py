@@ -22,6 +22,8 @@ Readings of passages the paper leaves open (kept identical in the HIP path):
 This module is test infrastructure (see the package docstring).
 """
 
+import math
+
 import numpy as np
 
 from . import records as rec
@@ -121,21 +123,66 @@ def block_statistics(K, T, L, r):
     return counts, means, factors
 
 
-def stored_statistics(counts, means, factors, mean_dtype, factor_dtype):
-    """Round-trip through the descriptor storage format (bf16 / fp32 / E2M1)."""
+def skew_coefficients(Kb, xi):
+    """Diagonal third cumulant along each stored direction (Sec. 7.7), per factor.
+
+    With u_i = xi_i / |xi_i| and lambda_i = |xi_i|^2, the paper's scalar is
+    g_i = (1/n) sum_t (u_i . (k_t - kbar))^3 and its cubic score term is
+    (1/6) (u_i . q)^3 g_i.  Stored here: gamma_i = g_i / lambda_i^(3/2) (the
+    standardised skewness of the block along u_i), so that the same term is
+    (1/6) gamma_i (xi_i . q)^3 from the stored xi_i.  A zero factor gives 0.
+    Kb [n, d] keys, xi [r, d] factors  ->  [r].
+    """
+    Kb = np.asarray(Kb, dtype=np.float64)
+    xi = np.asarray(xi, dtype=np.float64)
+    Kc = Kb - block_mean(Kb)
+    out = np.zeros(xi.shape[0])
+    for i in range(xi.shape[0]):
+        lam = float(xi[i] @ xi[i])
+        if lam > 0.0:
+            u = xi[i] / math.sqrt(lam)
+            g = float(np.mean((Kc @ u) ** 3))
+            out[i] = g / lam ** 1.5
+    return out
+
+
+def block_extras(K, V, T, L, factors, skew, value_mean):
+    """Optional record parts of every block: skew coefficients [NB, r] of its
+    factors (zero for a partial block, whose factors are zero) and the mean
+    value [NB, d] of its tokens (the pooled value of the compression branch).
+    Either is None when not asked for."""
+    K = np.asarray(K, dtype=np.float64)
+    nb, r = factors.shape[0], factors.shape[1]
+    skews = np.zeros((nb, r)) if skew else None
+    vmeans = np.zeros((nb, K.shape[1])) if value_mean else None
+    for b in range(nb):
+        n = block_count(T, L, b)
+        if skew:
+            skews[b] = skew_coefficients(K[b * L:b * L + n], factors[b])
+        if value_mean:
+            vmeans[b] = block_mean(np.asarray(V, dtype=np.float64)[b * L:b * L + n])
+    return skews, vmeans
+
+
+def stored_statistics(counts, means, factors, mean_dtype, factor_dtype, skews=None, vmeans=None):
+    """Round-trip through the descriptor storage format (bf16 / fp32 / E2M1).
+    With skew coefficients or value means, returns them too (5-tuple)."""
     d = means.shape[1]
     r = factors.shape[1]
-    buf = rec.encode(counts, means, factors, mean_dtype, factor_dtype)
-    return rec.decode(buf, d, r, mean_dtype, factor_dtype)
+    buf = rec.encode(counts, means, factors, mean_dtype, factor_dtype, skews, vmeans)
+    return rec.decode(buf, d, r, mean_dtype, factor_dtype, skews is not None, vmeans is not None)
 
 
 # ---------------------------------------------------------------- scoring --
 
-def log_mass_estimate(q, counts, means, factors, c):
+def log_mass_estimate(q, counts, means, factors, c, skews=None):
     """Second-order log-mass estimate of every block for every query head.
 
     eq. (trunc) with q <- c q and L <- n_b, curvature through eq. (gram):
         l_b^g = ln n_b + c q_g . kbar_b + (c^2 / 2) sum_i (xi_{b,i} . q_g)^2
+    With skew coefficients gamma (Sec. 7.7, see skew_coefficients) the
+    diagonal third-order term (c^3 / 6) sum_i gamma_{b,i} (xi_{b,i} . q_g)^3
+    is added.
     q [G, d], counts [NB], means [NB, d], factors [NB, r, d]  ->  [NB, G].
     """
     q = np.asarray(q, dtype=np.float64)
@@ -144,8 +191,13 @@ def log_mass_estimate(q, counts, means, factors, c):
         proj = np.einsum("brd,gd->bgr", factors, q)     # [NB, G, r]
         quad = (proj ** 2).sum(axis=2)
     else:
+        proj = None
         quad = np.zeros_like(lin)
-    return np.log(np.asarray(counts, dtype=np.float64))[:, None] + c * lin + 0.5 * c * c * quad
+    ell = np.log(np.asarray(counts, dtype=np.float64))[:, None] + c * lin + 0.5 * c * c * quad
+    if skews is not None and proj is not None:
+        cub = (np.asarray(skews, dtype=np.float64)[:, None, :] * proj ** 3).sum(axis=2)
+        ell = ell + (c ** 3 / 6.0) * cub
+    return ell
 
 
 def logsumexp(x, axis):
@@ -234,17 +286,33 @@ def branch_attention(q, K, V, T, L, w, sel, c):
     return o_s, l_s, o_w, l_w
 
 
-def decode_unit(q, K, V, T, L, r, s, w, c, mean_dtype, factor_dtype, stats=None):
+def compression_attention(q, counts, key_means, value_means, c):
+    """The mean-pool compression branch (Sec. 2 branch (i); Sec. 5.2 keeps it
+    beside the covariance selector): softmax attention of each query head over
+    the pooled blocks, block b entering as one key kbar_b (its mean key) with
+    one value vbar_b (its mean value), for every block holding a token.
+    Returns out [G, d] and lse [G] = ln sum_b exp(c q_g . kbar_b); no blocks
+    give 0 and -inf."""
+    live = np.asarray(counts) > 0
+    return sparse_attention(q, np.asarray(key_means)[live], np.asarray(value_means)[live],
+                            np.arange(int(live.sum())), c)
+
+
+def decode_unit(q, K, V, T, L, r, s, w, c, mean_dtype, factor_dtype, stats=None, skew=False):
     """One decode step of one (batch, KV head) unit, every stage in order.
 
-    stats: optional (counts, means, factors) already in storage precision;
-    otherwise they are built from K and round-tripped through storage.
+    stats: optional (counts, means, factors[, skews, vmeans]) already in
+    storage precision; otherwise they are built from K (with skew coefficients
+    when `skew`) and round-tripped through storage.
     Returns dict(ell, sigma, nc, sel, out, lse, stats).
     """
     if stats is None:
-        stats = stored_statistics(*block_statistics(K, T, L, r), mean_dtype, factor_dtype)
-    counts, means, factors = stats
-    ell = log_mass_estimate(q, counts, means, factors, c)
+        counts, means, factors = block_statistics(K, T, L, r)
+        skews, _ = block_extras(K, V, T, L, factors, skew, False)
+        stats = stored_statistics(counts, means, factors, mean_dtype, factor_dtype, skews)
+    counts, means, factors = stats[:3]
+    skews = stats[3] if len(stats) > 3 else None
+    ell = log_mass_estimate(q, counts, means, factors, c, skews)
     sigma = group_scores(ell)
     nc = candidate_count(T, L, w)
     sel = select_top(sigma, nc, s)

@@ -88,3 +88,16 @@ def test_bench_refuses_several_gpus():
     assert r.returncode == 2, r.stderr[-500:]
     assert "measures one GPU" in r.stderr
     assert r.stdout.strip() == ""
+
+
+def test_prefill_flops_count_the_method_not_the_iteration():
+    """Sec. 5.6: Gram matrix 2 L^2 d, a dense symmetric eigenproblem (its
+    tridiagonal reduction, 4 L^3 / 3) and the factors 2 L d r per full block."""
+    c = _cfg(rank=4)
+    ms = 1.0
+    out = bench.prefill_summary(c, 1, 64 * 10, ms)
+    per = 2 * 64 * 64 * 128 + 4 * 64 ** 3 / 3 + 2 * 64 * 128 * 4
+    assert out["full_blocks"] == 10 and out["blocks"] == 10
+    assert abs(out["method_mflop_per_block"] - per / 1e6) < 1e-3
+    assert abs(out["gflops"] - 10 * per / 1e-3 / 1e9) < 0.1
+    assert out["executed_mflop_per_block"] > out["method_mflop_per_block"]

@@ -447,3 +447,131 @@ def test_quest_box_score_bounds_and_forms():
     corners = np.array([[lo[0] if a else hi[0], lo[1] if b_ else hi[1], lo[2] if c_ else hi[2]]
                         for a in (0, 1) for b_ in (0, 1) for c_ in (0, 1)])
     np.testing.assert_allclose(M.quest_block_scores(qt, Kt, 5, 8)[0, 0], (corners @ qt[0]).max(), atol=1e-12)
+
+
+# ------------------------------------------------- diagonal skew (Sec. 7.7) --
+
+def _rank1_skewed_block(n, d, seed):
+    """Keys varying along one unit direction u with exponential (skewed) weights."""
+    rng = np.random.default_rng(seed)
+    u = rng.standard_normal(d)
+    u /= np.linalg.norm(u)
+    m = rng.standard_normal(d)
+    a = rng.exponential(1.0, n)
+    return m[None, :] + a[:, None] * u[None, :], u
+
+
+def test_skew_term_is_the_exact_third_cumulant_for_a_rank_one_block():
+    """For keys along one direction the third cumulant tensor is g u (x) u (x) u,
+    so the diagonal term equals (c^3 / 6) (1/n) sum_t (q . (k_t - kbar))^3,
+    computed here from the keys by brute force."""
+    Kb, u = _rank1_skewed_block(64, 32, 5)
+    counts, means, factors = M.block_statistics(Kb, 64, 64, 2)
+    skews, _ = M.block_extras(Kb, None, 64, 64, factors, True, False)
+    q = np.random.default_rng(6).standard_normal((3, 32))
+    c = 0.2
+    l2 = M.log_mass_estimate(q, counts, means, factors, c)
+    l3 = M.log_mass_estimate(q, counts, means, factors, c, skews)
+    Kc = Kb - Kb.mean(axis=0)
+    brute = c ** 3 / 6.0 * np.mean((Kc @ q.T) ** 3, axis=0)
+    np.testing.assert_allclose((l3 - l2)[0], brute, rtol=1e-10, atol=1e-13)
+    assert abs(skews[0, 0]) > 0.5                 # an exponential law is strongly skewed
+    assert np.max(np.abs(brute)) > 1e-3
+
+
+def test_skew_term_vanishes_for_symmetric_blocks_and_ignores_the_sign():
+    """A block symmetric about its mean has no third cumulant; flipping a stored
+    vector's sign flips its coefficient, leaving the score unchanged."""
+    rng = np.random.default_rng(8)
+    half = rng.standard_normal((32, 48)) * np.linspace(3, 0.2, 48)
+    Kb = np.concatenate([1.0 + half, 1.0 - half])
+    counts, means, factors = M.block_statistics(Kb, 64, 64, 4)
+    skews, _ = M.block_extras(Kb, None, 64, 64, factors, True, False)
+    np.testing.assert_allclose(skews, 0.0, atol=1e-12)
+    Ks, _ = _rank1_skewed_block(64, 48, 9)
+    Ks = Ks + 0.3 * rng.standard_normal(Ks.shape)
+    xi = M.scaled_eigenvectors(M.block_covariance(Ks), 3)
+    q = rng.standard_normal((2, 48))
+    g = M.skew_coefficients(Ks, xi)
+    gf = M.skew_coefficients(Ks, -xi)
+    np.testing.assert_allclose(gf, -g, rtol=1e-12)
+    a = M.log_mass_estimate(q, [64], Ks.mean(0)[None], xi[None], 0.3, g[None])
+    b = M.log_mass_estimate(q, [64], Ks.mean(0)[None], -xi[None], 0.3, gf[None])
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
+
+def test_third_order_estimate_has_a_fourth_order_remainder():
+    """eq. (cgf-expansion) truncated after kappa_3: on a rank-one block the error
+    of the third-order estimate against the exact ln m_b shrinks 16-fold when q
+    halves, that of the second-order estimate 8-fold."""
+    Kb, u = _rank1_skewed_block(64, 16, 12)
+    counts, means, factors = M.block_statistics(Kb, 64, 64, 1)
+    skews, _ = M.block_extras(Kb, None, 64, 64, factors, True, False)
+    errs = []
+    for scale in (0.08, 0.04):
+        q = (scale * u)[None, :]
+        exact = M.exact_block_log_mass(q, Kb, 64, 64, 1.0)[0, 0]
+        l2 = M.log_mass_estimate(q, counts, means, factors, 1.0)[0, 0]
+        l3 = M.log_mass_estimate(q, counts, means, factors, 1.0, skews)[0, 0]
+        errs.append((abs(l2 - exact), abs(l3 - exact)))
+    (e2a, e3a), (e2b, e3b) = errs
+    assert e3a < e2a and e3b < e2b
+    assert 6.5 < e2a / e2b < 9.5, e2a / e2b
+    assert 13.0 < e3a / e3b < 19.0, e3a / e3b
+
+
+# ---------------------------------------- compression branch (Sec. 2, 5.2) --
+
+def test_compression_branch_of_one_token_blocks_is_dense_attention():
+    """With one token per block the pooled keys and values are the tokens
+    themselves: the branch is softmax attention over every token, written out
+    here directly."""
+    rng = np.random.default_rng(21)
+    K, V, q = rng.standard_normal((40, 16)), rng.standard_normal((40, 16)), rng.standard_normal((3, 16))
+    counts, means, factors = M.block_statistics(K, 40, 1, 0)
+    _, vmeans = M.block_extras(K, V, 40, 1, factors, False, True)
+    out, lse = M.compression_attention(q, counts, means, vmeans, 0.25)
+    s = 0.25 * q @ K.T
+    p = np.exp(s - s.max(axis=1, keepdims=True))
+    np.testing.assert_allclose(out, (p @ V) / p.sum(axis=1, keepdims=True), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, np.log(np.exp(s).sum(axis=1)), rtol=0, atol=1e-12)
+
+
+def test_compression_branch_pools_blocks_by_their_means():
+    """Blocks of L copies of one (key, value) pool to that pair; a partial tail
+    block pools its own tokens; no blocks give 0 and -inf."""
+    rng = np.random.default_rng(22)
+    reps_k, reps_v = rng.standard_normal((5, 8)), rng.standard_normal((5, 8))
+    K = np.repeat(reps_k, 4, axis=0)[:19]
+    V = np.repeat(reps_v, 4, axis=0)[:19]
+    q = rng.standard_normal((2, 8))
+    counts, means, factors = M.block_statistics(K, 19, 4, 0)
+    _, vmeans = M.block_extras(K, V, 19, 4, factors, False, True)
+    assert counts.tolist() == [4, 4, 4, 4, 3]
+    out, lse = M.compression_attention(q, counts, means, vmeans, 0.5)
+    s = 0.5 * q @ reps_k.T
+    p = np.exp(s)
+    np.testing.assert_allclose(out, (p @ reps_v) / p.sum(axis=1, keepdims=True), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, np.log(p.sum(axis=1)), rtol=0, atol=1e-12)
+    o0, l0 = M.compression_attention(q, np.zeros(3, int), np.zeros((3, 8)), np.zeros((3, 8)), 0.5)
+    assert np.all(o0 == 0) and np.all(np.isneginf(l0))
+
+
+def test_records_with_skew_and_value_means_round_trip():
+    """fp32 storage of every part is exact; the optional parts sit where the
+    layout says, the rest of the record is unchanged."""
+    rng = np.random.default_rng(23)
+    nb, d, r = 5, 64, 3
+    counts = np.array([64, 64, 64, 64, 9])
+    means, vmeans = rng.standard_normal((nb, d)), rng.standard_normal((nb, d))
+    factors, skews = rng.standard_normal((nb, r, d)), rng.standard_normal((nb, r))
+    f32 = lambda x: np.asarray(x).astype(np.float32).astype(np.float64)
+    buf = R.encode(counts, means, factors, "f32", "f32", skews, vmeans)
+    c2, m2, x2, s2, v2 = R.decode(buf, d, r, "f32", "f32", True, True)
+    assert c2.tolist() == counts.tolist()
+    for a, b in ((m2, means), (x2, factors), (s2, skews), (v2, vmeans)):
+        np.testing.assert_array_equal(a, f32(b))
+    plain = R.encode(counts, means, factors, "f32", "f32")
+    lay, lay0 = R.layout(d, r, "f32", "f32", True, True), R.layout(d, r, "f32", "f32")
+    np.testing.assert_array_equal(buf[:, lay["mean_off"]:lay["vmean_off"]], plain[:, lay0["mean_off"]:lay0["total"]])
+    assert lay["total"] == lay0["total"] + 16 + 4 * d
