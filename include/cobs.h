@@ -75,6 +75,18 @@ typedef enum {
   COBS_OP_SELECT_EXACT = 4 /* cobs_select_exact, cobs_select_quest */
 } cobs_op_t;
 
+/* Optional record parts (cobs_config_t.options).
+ *   COBS_OPT_SKEW: the diagonal third-cumulant term of Sec. 7.7.  Per factor the
+ *     record stores gamma_i = g_i / lambda_i^(3/2), where lambda_i = |xi_i|^2,
+ *     u_i = xi_i / |xi_i| and g_i = (1/n) sum_t (u_i . (k_t - kbar))^3 (the
+ *     paper's scalar), computed from the fp32 factors before storage rounding;
+ *     the selector adds (c^3/6) sum_i gamma_i (xi_i . q)^3, the paper's
+ *     (1/6) sum_i (u_i . q)^3 g_i, to l_b^g.  A diagnostic selector variant.
+ *   COBS_OPT_VALUE_MEAN: the record also stores the block's mean value (in the
+ *     mean dtype), the pooled value of the mean-pool compression branch
+ *     (Sec. 2 branch (i), kept by Sec. 5.2); needed by cobs_compression_branch. */
+typedef enum { COBS_OPT_SKEW = 1, COBS_OPT_VALUE_MEAN = 2 } cobs_option_t;
+
 /* Problem description shared by every call (host struct, passed by pointer). */
 typedef struct {
   int32_t batch;         /* B >= 1                                                  */
@@ -90,6 +102,7 @@ typedef struct {
   cobs_dtype_t mean_dtype;   /* stored block mean: F32, BF16 or E2M1                  */
   cobs_dtype_t factor_dtype; /* stored scaled eigenvectors: F32, BF16 or E2M1         */
   float softmax_scale;   /* c; 0 selects 1/sqrt(d)                                  */
+  int32_t options;       /* bitwise OR of cobs_option_t; 0 for the plain method    */
 } cobs_config_t;
 
 /* KV cache of one layer.
@@ -118,16 +131,20 @@ typedef struct {
 /* Descriptor record of one block (Sec. 5.3 / 5.5), little-endian, 16-byte aligned:
  *   0        int32   n_b
  *   4        float   scale of the E2M1 mean (0 for F32/BF16 means)
- *   8        8 zero bytes
+ *   8        float   scale of the E2M1 value mean (COBS_OPT_VALUE_MEAN, else 0)
+ *   12       4 zero bytes
  *   16       float   scale of factor i, i < r (E2M1 factors only), zero padded to 16 B
+ *   S        float   skew coefficient gamma_i, i < r (COBS_OPT_SKEW only), zero padded to 16 B
  *   M        mean: d elements of mean_dtype
  *   M+|mean| factors: r vectors of d elements of factor_dtype, vector-major
+ *   V        value mean: d elements of mean_dtype (COBS_OPT_VALUE_MEAN only)
  *   size     rounded up to 16 B
  * Element sizes: F32 4 B, BF16 2 B, E2M1 one nibble (element 2j in the low nibble
  * of byte j).  E2M1 vectors use scale = fp32(max|x|)/6, y = x/scale in fp32,
  * round to nearest of {0,.5,1,1.5,2,3,4,6} with ties to the even code, |y| <= 6,
  * no negative zero, scale 0 for an all-zero vector.  A block with n_b < L stores
- * zero factors.  Summaries of one layer: [B, Hkv, T_max/L] records.
+ * zero factors (and zero skew coefficients).  Summaries of one layer:
+ * [B, Hkv, T_max/L] records.
  * Returns 0 if cfg is invalid.                                                     */
 size_t cobs_record_bytes(const cobs_config_t* cfg);
 
@@ -239,6 +256,21 @@ cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const c
 cobs_status_t cobs_decode_step_noalloc(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
                                        const int32_t* seq_lens, void* summaries, int32_t* sel,
                                        float* out, float* lse, void* stream);
+
+/* The mean-pool compression branch (Sec. 2 branch (i), kept by COBS beside its
+ * covariance selector, Sec. 5.2), for a caller-side gate with the selection and
+ * window branches: per query head, softmax attention over the pooled blocks,
+ * block b entering as one key (its stored mean key) with one value (its stored
+ * mean value), for every block b < ceil(T/L):
+ *   out_g = sum_b exp(c q_g . kbar_b) vbar_b / sum_b exp(c q_g . kbar_b),
+ *   lse_g = ln sum_b exp(c q_g . kbar_b).
+ * Needs records built with COBS_OPT_VALUE_MEAN (COBS_ERR_INVALID_ARG otherwise).
+ *   q:    device fp32 [B, Hq, d].   summaries: records (read only).
+ *   out:  device fp32 [B, Hq, d], written; a row with T = 0 gives 0.
+ *   lse:  optional device fp32 [B, Hq], written (-inf for T = 0).
+ * One workgroup per (batch row, KV head); no workspace.                         */
+cobs_status_t cobs_compression_branch(const cobs_config_t* cfg, const float* q, const void* summaries,
+                                      const int32_t* seq_lens, float* out, float* lse, void* stream);
 
 /* FP4 E2M1 encoder used for descriptor storage (Sec. 5.5), exposed so the
  * rounding rule can be checked on its own.

@@ -16,7 +16,7 @@ not fix the scale rule or the rounding; the reading used throughout is:
     5. the sign is kept in bit 3 unless the magnitude code is 0 (no -0),
     6. max|x| == 0 gives scale 0 and all codes 0,
     7. element 2j sits in the low nibble of byte j, element 2j+1 in the high.
-  Decoding is code value times scale, exact in fp32.
+  Decoding is code value times scale, computed in float64 (exact).
 
 This module is test infrastructure (see the package docstring).
 """
@@ -91,7 +91,7 @@ def e2m1_encode(x):
 
 
 def e2m1_decode(codes, scales):
-    """float64 values code_value * scale (exact in fp32)."""
+    """float64 values code_value * scale (exact in float64)."""
     codes = np.asarray(codes, dtype=np.uint8)
     mag = E2M1_GRID[codes & 7]
     sign = np.where(codes & 8, -1.0, 1.0)

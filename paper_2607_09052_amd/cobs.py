@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcobs.so"
 F32, BF16, E2M1 = 0, 1, 2
 DTYPES = {"f32": F32, "bf16": BF16, "e2m1": E2M1}
 OP_BUILD, OP_SELECT, OP_DECODE, OP_STEP, OP_SELECT_EXACT = 0, 1, 2, 3, 4
+OPT_SKEW, OPT_VALUE_MEAN = 1, 2
 BLOCK = 64
 
 
@@ -32,7 +33,8 @@ class _Config(ctypes.Structure):
                 ("max_seq_len", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("rank", ctypes.c_int32), ("budget", ctypes.c_int32), ("window", ctypes.c_int32),
                 ("kv_dtype", ctypes.c_int), ("mean_dtype", ctypes.c_int),
-                ("factor_dtype", ctypes.c_int), ("softmax_scale", ctypes.c_float)]
+                ("factor_dtype", ctypes.c_int), ("softmax_scale", ctypes.c_float),
+                ("options", ctypes.c_int32)]
 
 
 class _KV(ctypes.Structure):
@@ -54,6 +56,7 @@ _SIGS = {
     "cobs_sparse_decode_branches": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_decode_step": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P]),
     "cobs_decode_step_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "cobs_compression_branch": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "cobs_pack_e2m1": (ctypes.c_int, [_P, ctypes.c_int64, ctypes.c_int32, _P, _P, _P]),
     "cobs_status_string": (ctypes.c_char_p, [ctypes.c_int]),
 }
@@ -93,12 +96,18 @@ class Config:
     factor_dtype: str = "f32"
     softmax_scale: float = 0.0
     block_size: int = BLOCK
+    skew: bool = False           # records carry the diagonal third-cumulant coefficients
+    value_mean: bool = False     # records carry the block's mean value (compression branch)
+
+    @property
+    def options(self):
+        return (OPT_SKEW if self.skew else 0) | (OPT_VALUE_MEAN if self.value_mean else 0)
 
     def c_struct(self):
         return _Config(self.batch, self.num_q_heads, self.num_kv_heads, self.head_dim,
                        self.max_seq_len, self.block_size, self.rank, self.budget, self.window,
                        DTYPES[self.kv_dtype], DTYPES[self.mean_dtype], DTYPES[self.factor_dtype],
-                       float(self.softmax_scale))
+                       float(self.softmax_scale), self.options)
 
     @property
     def num_blocks(self):
@@ -331,6 +340,18 @@ def cobs_decode_step_noalloc(cfg, q, k, v, seq_lens, summaries, out, sel=None, l
     _check(lib().cobs_decode_step_noalloc(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
                                           _ptr(seq_lens), _ptr(summaries), _ptr(sel), _ptr(out), _ptr(lse),
                                           _stream(stream, q)))
+
+
+def cobs_compression_branch(cfg, q, summaries, seq_lens, out, lse=None, stream=None):
+    """The mean-pool compression branch over value-mean records (cfg.value_mean)."""
+    _need("q", q, torch.float32, cfg.batch * cfg.num_q_heads * cfg.head_dim)
+    _need("seq_lens", seq_lens, torch.int32, cfg.batch)
+    _summaries(cfg, summaries)
+    _need("out", out, torch.float32, cfg.batch * cfg.num_q_heads * cfg.head_dim)
+    _opt("lse", lse, torch.float32, cfg.batch * cfg.num_q_heads)
+    _same_gpu(q=q, summaries=summaries, seq_lens=seq_lens, out=out, lse=lse)
+    _check(lib().cobs_compression_branch(ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(summaries), _ptr(seq_lens),
+                                         _ptr(out), _ptr(lse), _stream(stream, q)))
 
 
 def cobs_pack_e2m1(x, codes, scales, stream=None):

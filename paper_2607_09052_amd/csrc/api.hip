@@ -40,12 +40,14 @@ cobs_status_t check_config(const cobs_config_t* c) {
   if (c->block_size != kL) return COBS_ERR_UNSUPPORTED;
   if (c->rank > kMaxRank) return COBS_ERR_UNSUPPORTED;
   if (c->max_seq_len / c->block_size > kMaxBlocksPerSeq) return COBS_ERR_UNSUPPORTED;
+  if (c->options & ~(COBS_OPT_SKEW | COBS_OPT_VALUE_MEAN)) return COBS_ERR_INVALID_ARG;
   return COBS_OK;
 }
 
 struct Derived {
   int B, hq, hkv, G, d, tmax, nbmax, r, s, w, units;
   int mdt, fdt, kv_f32;
+  int skew, vmean;      // optional record parts
   float c;
   RecLayout lay;
   int nch_max;          // selector: workgroups (chunks) per unit, upper bound
@@ -74,7 +76,9 @@ Derived derive(const cobs_config_t* c) {
   v.fdt = dtype_code(c->factor_dtype);
   v.kv_f32 = c->kv_dtype == COBS_F32;
   v.c = c->softmax_scale > 0.0f ? c->softmax_scale : 1.0f / sqrtf((float)v.d);
-  v.lay = rec_layout(v.d, v.r, v.mdt, v.fdt);
+  v.skew = (c->options & COBS_OPT_SKEW) ? 1 : 0;
+  v.vmean = (c->options & COBS_OPT_VALUE_MEAN) ? 1 : 0;
+  v.lay = rec_layout(v.d, v.r, v.mdt, v.fdt, v.skew != 0, v.vmean != 0);
 
   // grid bounds for the workspace; the launchers pick the actual grids within them
   v.nch_max = (v.nbmax + select_min_bpw(v.mdt, v.fdt) - 1) / select_min_bpw(v.mdt, v.fdt);
@@ -152,6 +156,8 @@ cobs_status_t run_build(const Derived& v, const cobs_kv_t* kv, const int32_t* se
   p.first_block = first;
   p.tail_mode = tail ? 1 : 0;
   p.kv_f32 = v.kv_f32;
+  p.skew = v.skew;
+  p.vmean = v.vmean;
   p.lay = v.lay;
   if (!tail && count == 0) return COBS_OK;
   dim3 grid(tail ? 1 : count, v.hkv, v.B);
@@ -185,6 +191,8 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
   p.fdt = v.fdt;
   p.nch = v.nch_max;
   p.bpw = 0;
+  p.skew = v.skew;
+  p.vmean = v.vmean;
   p.c = v.c;
   p.lay = v.lay;
   return hip_status(launch_select(p, v.d, v.G, v.B, st));
@@ -215,6 +223,8 @@ cobs_status_t run_select_exact(const Derived& v, const float* q, const cobs_kv_t
   p.fdt = v.fdt;
   p.nch = v.nchx_max;
   p.bpw = 0;
+  p.skew = 0;
+  p.vmean = 0;
   p.c = v.c;
   p.lay = v.lay;
   return hip_status(launch_select_exact(p, v.d, v.G, v.B, st, quest));
@@ -475,6 +485,29 @@ cobs_status_t cobs_decode_step_noalloc(const cobs_config_t* cfg, const float* q,
                      reinterpret_cast<unsigned*>(wsb + v.sel_bytes + v.dec_cnt), v.units);
   if ((s = hip_status(hipGetLastError())) != COBS_OK) return s;
   return run_step(v, q, kv, seq_lens, summaries, sel, out, lse, wsb, st);
+}
+
+cobs_status_t cobs_compression_branch(const cobs_config_t* cfg, const float* q, const void* summaries,
+                                      const int32_t* seq_lens, float* out, float* lse, void* stream) {
+  cobs_status_t s = check_config(cfg);
+  if (s != COBS_OK) return s;
+  const Derived v = derive(cfg);
+  if (!v.vmean) return COBS_ERR_INVALID_ARG;      // the records hold no value means
+  if (!q || !summaries || !seq_lens || !out || !aligned(summaries, 16)) return COBS_ERR_INVALID_ARG;
+  CompressParams p;
+  p.q = q;
+  p.rec = static_cast<const uint8_t*>(summaries);
+  p.seq_lens = seq_lens;
+  p.out = out;
+  p.lse = lse;
+  p.hkv = v.hkv;
+  p.hq = v.hq;
+  p.nbmax = v.nbmax;
+  p.tmax = v.tmax;
+  p.mdt = v.mdt;
+  p.c = v.c;
+  p.lay = v.lay;
+  return hip_status(launch_compress(p, v.d, v.G, v.B, static_cast<hipStream_t>(stream)));
 }
 
 cobs_status_t cobs_pack_e2m1(const float* x, int64_t num_vectors, int32_t dim, uint8_t* codes,

@@ -34,6 +34,7 @@ struct StatsArgs {
   KvView kv;
   uint8_t* rec;          // [B, Hkv, nbmax] records
   int hkv, nbmax, r, mdt, fdt;
+  int skew, vmean;       // optional record parts: skew coefficients, value mean
   RecLayout lay;
 };
 
@@ -86,6 +87,24 @@ __device__ void store_vector(const float* x, int dim, int dt, uint8_t* dst, floa
   }
 }
 
+// The part of a record after its factors (written last, after the factors
+// themselves): zero factors for a block without them, the value mean of a
+// value-mean record, and zero padding up to the record size.  Called by every
+// thread of the workgroup (store_vector holds barriers).
+template <int D, int NT = kBuildThreads>
+__device__ __forceinline__ void store_tail_impl(const StatsArgs& p, uint8_t* R, const float* vmean, int tid,
+                                                float* red, bool zero_factors) {
+  const RecLayout lay = p.lay;
+  if (zero_factors)
+    for (int idx = lay.fac_off / 4 + tid; idx < lay.vmean_off / 4; idx += NT) reinterpret_cast<uint32_t*>(R)[idx] = 0u;
+  int end = lay.vmean_off;
+  if (p.vmean) {
+    store_vector(vmean, D, p.mdt, R + lay.vmean_off, reinterpret_cast<float*>(R + 8), tid, kBuildThreads, red);
+    end += lay.mean_bytes;
+  }
+  for (int idx = end / 4 + tid; idx < lay.total / 4; idx += NT) reinterpret_cast<uint32_t*>(R)[idx] = 0u;
+}
+
 // LDS carve-out of the statistics pool (16-byte aligned pieces).
 template <int D, int P, bool KF32>
 struct StatsLds {
@@ -106,7 +125,9 @@ struct StatsLds {
   static constexpr size_t order = al(cpart + 4 * P);
   static constexpr size_t ritz = al(order + 4 * kMaxRank);
   static constexpr size_t red = al(ritz + 4 * kMaxRank);
-  static constexpr size_t bytes = al(red + 4 * kBuildThreads);
+  static constexpr size_t vmean = al(red + 4 * kBuildThreads);   // mean value (value-mean records)
+  static constexpr size_t skw = al(vmean + 4 * D);               // skew coefficients
+  static constexpr size_t bytes = al(skw + 4 * kMaxRank);
   static_assert(8 * (kBuildThreads / (D / 8)) * D <= 4 * kL * kL, "column sums fit the Gram buffer");
   static_assert(kMaxRank * D <= kL * kL, "xi fits the Gram buffer");
 };
@@ -138,6 +159,8 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   float* ritzval = reinterpret_cast<float*>(pool + Lay::ritz);
   float* Xi = Gm;                                  // after the power iteration
   float* red = reinterpret_cast<float*>(pool + Lay::red);
+  float* vmean = reinterpret_cast<float*>(pool + Lay::vmean);
+  float* skw = reinterpret_cast<float*>(pool + Lay::skw);
   // centred key e of row i, as the block's fp32 arithmetic sees it
   auto kc = [&](int e, int i) -> float {
     if constexpr (KF32) return KT[e * KS + i] - mean[e];
@@ -194,17 +217,52 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     mean[tid] = (float)(sum / (double)n);
   }
   __syncthreads();
+  if (p.vmean) {
+    // the block's mean value, the same way (value rows summed in fp64, one rounding)
+    double vs[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) vs[q] = 0.0;
+#pragma unroll
+    for (int ps = 0; ps < NPASS; ++ps) {
+      const int i = r0 + ps * RPP;
+      const int64_t off = (lw && i < n) ? kv_offset(p.kv, b, h, j * kL + i) : -1;
+      if (off >= 0) {
+        float x[8];
+        if constexpr (KF32) {
+          const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(p.kv.v) + off + e0);
+          const float4 a = src[0], c = src[1];
+          x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = c.x; x[5] = c.y; x[6] = c.z; x[7] = c.w;
+        } else {
+          const uint4 a = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.kv.v) + off + e0);
+          x[0] = bf16_lo(a.x); x[1] = bf16_hi(a.x); x[2] = bf16_lo(a.y); x[3] = bf16_hi(a.y);
+          x[4] = bf16_lo(a.z); x[5] = bf16_hi(a.z); x[6] = bf16_lo(a.w); x[7] = bf16_hi(a.w);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) vs[q] += (double)x[q];
+      }
+    }
+    if (lw) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) red64[r0 * D + e0 + q] = vs[q];
+    }
+    __syncthreads();
+    if (tid < D) {
+      double sum = 0.0;
+      for (int g = 0; g < RPP; ++g) sum += red64[g * D + tid];
+      vmean[tid] = (float)(sum / (double)n);
+    }
+    __syncthreads();
+  }
   const bool factors = (n == kL) && (r > 0);
   uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
   const RecLayout lay = p.lay;
   if (!factors) {
-    // partial block (or r = 0): count, mean, zero factors
+    // partial block (or r = 0): count, mean, zero factors and skew coefficients
     for (int idx = tid; idx < lay.mean_off / 4; idx += NT)
       reinterpret_cast<uint32_t*>(R)[idx] = (idx == 0) ? (uint32_t)n : 0u;
     __syncthreads();
     store_vector(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), tid, kBuildThreads, red);
-    for (int idx = lay.fac_off / 4 + tid; idx < lay.total / 4; idx += NT)
-      reinterpret_cast<uint32_t*>(R)[idx] = 0u;
+    store_tail_impl<D, NT>(p, R, vmean, tid, red, true);
     return;
   }
   // stage the keys transposed in their stored type: KT[e][i] = k_{jL+i}[e]
@@ -489,6 +547,23 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       }
     }
     __syncthreads();
+    if (p.skew) {
+      // skew coefficient of factor i (wave i % 4; lane t = token t):
+      // gamma_i = (1/n) sum_t z_t^3 with z_t = (xi_i . kc_t) / |xi_i|^2, the
+      // projection on u_i standardised by its deviation
+      for (int i = tid >> 6; lw && i < r; i += kBuildThreads / 64) {
+        const int t = tid & 63;
+        float nrm = 0.0f;
+        for (int e = t; e < D; e += 64) nrm += Xi[i * D + e] * Xi[i * D + e];
+        const float lam = wave_sum(nrm);
+        float pr = 0.0f;
+        for (int e = 0; e < D; ++e) pr += kc(e, t) * Xi[i * D + e];
+        const float z = (lam > 0.0f) ? pr / lam : 0.0f;
+        const float s3 = wave_sum(z * z * z);
+        if (t == 0) skw[i] = s3 / (float)n;
+      }
+      __syncthreads();
+    }
   }
 
   // ---- write the record
@@ -500,16 +575,14 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   __syncthreads();
   store_vector(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), tid,
                kBuildThreads, red);
+  if (p.skew && tid < r) reinterpret_cast<float*>(R + lay.skew_off)[tid] = skw[tid];
   __syncthreads();
   for (int i = 0; i < r; ++i) {
     store_vector(&Xi[i * D], D, p.fdt, R + lay.fac_off + i * lay.vec_bytes,
                  reinterpret_cast<float*>(R + 16) + i, tid, kBuildThreads, red);
     __syncthreads();
   }
-  // zero the tail padding of the record
-  const int used = lay.fac_off + r * lay.vec_bytes;
-  for (int idx = used / 4 + tid; idx < lay.total / 4; idx += NT)
-    reinterpret_cast<uint32_t*>(R)[idx] = 0u;
+  store_tail_impl<D, NT>(p, R, vmean, tid, red, false);
 }
 
 }  // namespace cobs

@@ -22,6 +22,8 @@ __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams 
   a.r = p.r;
   a.mdt = p.mdt;
   a.fdt = p.fdt;
+  a.skew = p.skew;
+  a.vmean = p.vmean;
   a.lay = p.lay;
   block_stats<D, P, KF32>(a, b, h, j, min(kL, T - j * kL), pool);
 }

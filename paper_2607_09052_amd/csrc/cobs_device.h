@@ -21,6 +21,8 @@ struct RecLayout {
   int mean_bytes;
   int fac_off;     // offset of factor 0
   int vec_bytes;   // bytes of one factor vector
+  int skew_off;    // offset of the skew coefficients (skew records)
+  int vmean_off;   // offset of the value mean (value-mean records)
   int total;       // record size, multiple of 16
 };
 
@@ -28,14 +30,17 @@ __host__ __device__ inline int vec_bytes(int d, int dt) {
   return dt == DT_F32 ? 4 * d : (dt == DT_BF16 ? 2 * d : d / 2);
 }
 
-__host__ __device__ inline RecLayout rec_layout(int d, int r, int mdt, int fdt) {
+__host__ __device__ inline RecLayout rec_layout(int d, int r, int mdt, int fdt, bool skew = false,
+                                                bool vmean = false) {
   RecLayout l;
-  int fscale = (fdt == DT_E2M1) ? ((4 * r + 15) / 16) * 16 : 0;
-  l.mean_off = 16 + fscale;
+  const int fscale = (fdt == DT_E2M1) ? ((4 * r + 15) / 16) * 16 : 0;
+  l.skew_off = 16 + fscale;
+  l.mean_off = l.skew_off + (skew ? ((4 * r + 15) / 16) * 16 : 0);
   l.mean_bytes = vec_bytes(d, mdt);
   l.fac_off = l.mean_off + l.mean_bytes;
   l.vec_bytes = vec_bytes(d, fdt);
-  l.total = ((l.fac_off + r * l.vec_bytes + 15) / 16) * 16;
+  l.vmean_off = l.fac_off + r * l.vec_bytes;
+  l.total = ((l.vmean_off + (vmean ? l.mean_bytes : 0) + 15) / 16) * 16;
   return l;
 }
 

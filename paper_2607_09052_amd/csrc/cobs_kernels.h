@@ -12,6 +12,7 @@ struct BuildParams {
   const int32_t* seq_lens;
   uint8_t* rec;
   int hkv, tmax, nbmax, r, mdt, fdt, first_block, tail_mode, kv_f32;
+  int skew, vmean;      // optional record parts (skew coefficients, value mean)
   RecLayout lay;
 };
 
@@ -25,6 +26,7 @@ struct SelectParams {
   float* part;      // [B*Hkv][nch][G][2]
   unsigned* cnt;    // [B*Hkv] arrival counters
   int hkv, hq, nbmax, tmax, r, s, w, mdt, fdt, nch, bpw;
+  int skew, vmean;  // records carry skew coefficients (scored) / a value mean (kept by the refresh)
   float c;
   RecLayout lay;
   // decode step (bf16 K/V, r <= 4): the workgroup whose chunk holds a row's
@@ -55,6 +57,19 @@ struct DecodeParams {
 };
 
 hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st);
+
+// The mean-pool compression branch over value-mean records.
+struct CompressParams {
+  const float* q;
+  const uint8_t* rec;
+  const int32_t* seq_lens;
+  float* out;
+  float* lse;
+  int hkv, hq, nbmax, tmax, mdt;
+  float c;
+  RecLayout lay;
+};
+hipError_t launch_compress(const CompressParams& p, int d, int g, int batch, hipStream_t st);
 hipError_t launch_pack_e2m1(const float* x, int64_t nvec, int dim, uint8_t* codes, float* scales,
                             hipStream_t st);
 // Launchers choose the grid (chunks / work items per workgroup) from the

@@ -372,6 +372,7 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
   constexpr int EPL = D / 16;
   constexpr int MW = slice_words<MDT, EPL>(), FW = slice_words<FDT, EPL>();
   constexpr int SW = (FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0;    // 16-byte words of factor scales
+  constexpr int KW = (RMAX + 3) / 4;                             // 16-byte words of skew coefficients
   float (*gm)[G] = reinterpret_cast<float (*)[G]>(pool);
   float (*gs)[G] = reinterpret_cast<float (*)[G]>(pool + 16 * G * 4);
   __shared__ int s_last;
@@ -394,6 +395,7 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
   struct Slice {
     uint4 hdr;
     uint4 fsw[SW > 0 ? SW : 1];
+    uint4 ksw[KW];
     uint32_t mw[MW], fw[RMAX][FW];
   };
   auto load = [&](int base, Slice& S) {
@@ -402,6 +404,10 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
     S.hdr = *reinterpret_cast<const uint4*>(R);
 #pragma unroll
     for (int j = 0; j < SW; ++j) S.fsw[j] = reinterpret_cast<const uint4*>(R + 16)[j];
+    // skew coefficients (read unconditionally: without them these bytes are
+    // the start of the mean and factors, inside the record; discarded)
+#pragma unroll
+    for (int j = 0; j < KW; ++j) S.ksw[j] = reinterpret_cast<const uint4*>(R + p.lay.skew_off)[j];
     load_slice<MDT, EPL>(R + p.lay.mean_off, ln, S.mw);
     const uint8_t* F0 = (r > 0) ? R + p.lay.fac_off : qrow;
 #pragma unroll
@@ -436,7 +442,7 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
     const int blk = base + grp;
     const bool valid = blk < blk_hi;
     const float mscale = (MDT == DT_E2M1) ? __uint_as_float(cur.hdr.y) : 1.0f;
-    float lin[G], quad[G];
+    float lin[G], quad[G], cub[G];
     {
       float x[EPL];
       unpack_elems<MDT, EPL>(cur.mw, x);
@@ -447,6 +453,7 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
         for (int e = 0; e < EPL; ++e) a += x[e] * qv[g][e];
         lin[g] = row16_sum(a) * mscale;
         quad[g] = 0.0f;
+        cub[g] = 0.0f;
       }
     }
 #pragma unroll
@@ -457,6 +464,11 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
         const uint32_t c = (i % 4 == 0) ? wv.x : (i % 4 == 1) ? wv.y : (i % 4 == 2) ? wv.z : wv.w;
         fs = __uint_as_float(c);
       }
+      float gam = 0.0f;
+      if (p.skew) {
+        const uint4 kv = cur.ksw[i / 4];
+        gam = __uint_as_float((i % 4 == 0) ? kv.x : (i % 4 == 1) ? kv.y : (i % 4 == 2) ? kv.z : kv.w);
+      }
       float x[EPL];
       unpack_elems<FDT, EPL>(cur.fw[i], x);
 #pragma unroll
@@ -465,13 +477,17 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
 #pragma unroll
         for (int e = 0; e < EPL; ++e) a += x[e] * qv[g][e];
         a = row16_sum(a) * fs;
-        if (i < r) quad[g] += a * a;
+        if (i < r) {
+          quad[g] += a * a;
+          cub[g] += gam * (a * a * a);
+        }
       }
     }
     const float lnn = logf((float)(int)cur.hdr.x);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const float l = lnn + lin[g] + 0.5f * quad[g];
+      // second-order estimate, plus the diagonal third-order term of skew records
+      const float l = lnn + lin[g] + 0.5f * quad[g] + cub[g] * (1.0f / 6.0f);
       if (valid) {
         if (ln == 0) st_agent(&p.ell[((int64_t)unit * p.nbmax + blk) * G + g], l);
         lse_merge(run_m[g], run_s[g], l, 1.0f);
@@ -538,7 +554,8 @@ __device__ __forceinline__ sbf16x8_t tile_operand(const uint32_t* w, int kk) {
 
 template <int G, int RMAX, int FDT>
 constexpr size_t select_mfma_lds() {
-  return select_pool_bytes<4 * 16 * (1 + ((FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0)) * 16 + 2 * 4 * G * 4>();
+  return select_pool_bytes<4 * 16 * (1 + ((FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0)) * 16 + 2 * 4 * G * 4 +
+                           4 * 16 * ((RMAX + 3) / 4) * 16>();
 }
 
 // `pool`: select_mfma_lds<G, RMAX, FDT>() bytes of LDS.
@@ -548,9 +565,11 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
   constexpr int KST = D / 32;                                  // k-steps per lane group
   constexpr int MW = elem_bytes<MDT>(D / 4) / 4, FW = elem_bytes<FDT>(D / 4) / 4;
   constexpr int HU = 1 + ((FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0);   // 16-byte header words used
+  constexpr int KW = (RMAX + 3) / 4;                                 // 16-byte words of skew coefficients
   uint4 (*hdr_s)[16][HU] = reinterpret_cast<uint4 (*)[16][HU]>(pool);
   float (*gm)[G] = reinterpret_cast<float (*)[G]>(pool + 4 * 16 * HU * 16);
   float (*gs)[G] = reinterpret_cast<float (*)[G]>(pool + 4 * 16 * HU * 16 + 4 * G * 4);
+  uint4 (*ksk_s)[16][KW] = reinterpret_cast<uint4 (*)[16][KW]>(pool + 4 * 16 * HU * 16 + 2 * 4 * G * 4);
   __shared__ int s_last;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -571,6 +590,7 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
   struct Tile {
     uint32_t mw[MW], fw[RMAX][FW];
     uint4 hw[(HU + 3) / 4];
+    uint4 kw;            // skew word min(l / 16, KW - 1) (inside the record; used by skew records)
   };
   auto load = [&](int c0, Tile& S) {
     const int blk = max(min(c0 + hcol, blk_hi - 1), 0);
@@ -581,6 +601,7 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
     for (int i = 0; i < RMAX; ++i) load_words<FW>(F0 + min(i, rlast) * fstride + grp * (FW * 4), S.fw[i]);
 #pragma unroll
     for (int jj = 0; jj < (HU + 3) / 4; ++jj) S.hw[jj] = reinterpret_cast<const uint4*>(R)[min(grp + 4 * jj, HU - 1)];
+    S.kw = reinterpret_cast<const uint4*>(R + p.lay.skew_off)[min(grp, KW - 1)];
   };
   // the first tile is in flight while the queries load and split
   Tile cur;
@@ -616,6 +637,7 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
     load(c0 + 64, nxt);
 #pragma unroll
     for (int jj = 0; jj < (HU + 3) / 4; ++jj) hdr_s[wave][hcol][min(grp + 4 * jj, HU - 1)] = cur.hw[jj];
+    if (p.skew && grp < KW) ksk_s[wave][hcol][grp] = cur.kw;
     __builtin_amdgcn_sched_barrier(0);
     const uint32_t* mw = cur.mw;
     const uint32_t (*fw)[FW] = cur.fw;
@@ -646,7 +668,7 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
       const int ob = c0 + 4 * grp + i;
       const uint4 h0 = hdr_s[wave][4 * grp + i][0];
       const float msc = (MDT == DT_E2M1) ? __uint_as_float(h0.y) : 1.0f;
-      float quad = 0.0f;
+      float quad = 0.0f, cub = 0.0f;
 #pragma unroll
       for (int f = 0; f < RMAX; ++f) {
         float fs = 1.0f;
@@ -654,11 +676,20 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
           const uint4 wv = hdr_s[wave][4 * grp + i][1 + f / 4];
           fs = __uint_as_float((f % 4 == 0) ? wv.x : (f % 4 == 1) ? wv.y : (f % 4 == 2) ? wv.z : wv.w);
         }
+        float gam = 0.0f;
+        if (p.skew) {
+          const uint4 kv = ksk_s[wave][4 * grp + i][f / 4];
+          gam = __uint_as_float((f % 4 == 0) ? kv.x : (f % 4 == 1) ? kv.y : (f % 4 == 2) ? kv.z : kv.w);
+        }
         const float t = af[f][i] * fs;
-        if (f < r) quad += t * t;
+        if (f < r) {
+          quad += t * t;
+          cub += gam * (t * t * t);
+        }
       }
       if (ob < blk_hi) {
-        const float l = logf((float)(int)h0.x) + acc[i] * msc + 0.5f * quad;
+        // second-order estimate, plus the diagonal third-order term of skew records
+        const float l = logf((float)(int)h0.x) + acc[i] * msc + 0.5f * quad + cub * (1.0f / 6.0f);
         if (hcol < G) st_agent(&p.ell[((int64_t)unit * p.nbmax + ob) * G + hcol], l);
         lse_merge(run_m, run_s, l, 1.0f);
       }
@@ -733,6 +764,8 @@ __device__ __forceinline__ void select_refresh_task(const SelectParams& p, char*
     a.r = p.r;
     a.mdt = p.mdt;
     a.fdt = p.fdt;
+    a.skew = p.skew;
+    a.vmean = p.vmean;
     a.lay = p.lay;
     block_stats<D, 16, false>(a, b, h, j, min(kL, T - j * kL), pool);
     __builtin_amdgcn_s_waitcnt(0);       // the record is written before it is scored

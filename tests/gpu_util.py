@@ -44,9 +44,12 @@ def oracle_select(rec_unit, q_unit, T, cfg):
     A row with no tokens has no blocks, no candidates and no selection."""
     if T <= 0:
         return np.zeros(0), 0, []
-    counts, means, factors = R.decode(rec_unit, cfg.head_dim, cfg.rank, cfg.mean_dtype, cfg.factor_dtype)
+    parts = R.decode(rec_unit, cfg.head_dim, cfg.rank, cfg.mean_dtype, cfg.factor_dtype, cfg.skew, cfg.value_mean)
+    counts, means, factors = parts[:3]
+    skews = parts[3] if cfg.skew else None
     nb = M.num_blocks(T, cfg.block_size)
-    ell = M.log_mass_estimate(q_unit, counts[:nb], means[:nb], factors[:nb], cfg.scale)
+    ell = M.log_mass_estimate(q_unit, counts[:nb], means[:nb], factors[:nb], cfg.scale,
+                              None if skews is None else skews[:nb])
     sigma = M.group_scores(ell)
     nc = M.candidate_count(T, cfg.block_size, cfg.window)
     return sigma, nc, M.select_top(sigma, nc, cfg.budget)
@@ -151,7 +154,7 @@ def ky_fan_checks(xi, K, n, r):
         assert np.linalg.norm(A - Bm) <= 1e-3 * np.linalg.norm(Bm), np.linalg.norm(A - Bm) / np.linalg.norm(Bm)
 
 
-def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None):
+def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None, V_unit=None):
     """GPU block records of one unit against the oracle.
 
     rec32_unit: the unit's records built with fp32 mean and factors from the
@@ -164,7 +167,9 @@ def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None):
     nb = M.num_blocks(T, L)
     if nb == 0:
         return
-    counts, means, factors = R.decode(rec32_unit[:nb], d, r, "f32", "f32")
+    parts = R.decode(rec32_unit[:nb], d, r, "f32", "f32", cfg.skew, cfg.value_mean)
+    counts, means, factors = parts[:3]
+    skews, vmeans = (parts[3], parts[4]) if (cfg.skew or cfg.value_mean) else (None, None)
     K = np.asarray(K_unit, dtype=np.float64)
     blocks = range(nb) if blocks is None else [j for j in blocks if j < nb]
     for j in blocks:
@@ -176,7 +181,12 @@ def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None):
             assert np.all(factors[j] == 0), j
         else:
             ky_fan_checks(factors[j], Kb, n, r)
-    want = R.encode(counts, means, factors, cfg.mean_dtype, cfg.factor_dtype)
+        if skews is not None:
+            np.testing.assert_allclose(skews[j], M.skew_coefficients(Kb, factors[j]), rtol=1e-4, atol=2e-4)
+        if vmeans is not None and V_unit is not None:
+            Vb = np.asarray(V_unit, dtype=np.float64)[j * L:j * L + n]
+            np.testing.assert_allclose(vmeans[j], M.block_mean(Vb), rtol=0, atol=1e-6 * max(np.abs(Vb).max(), 1e-30))
+    want = R.encode(counts, means, factors, cfg.mean_dtype, cfg.factor_dtype, skews, vmeans)
     got = np.asarray(rec_unit[:nb])
     for j in blocks:
         np.testing.assert_array_equal(got[j], want[j], err_msg=f"block {j}")

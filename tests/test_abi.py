@@ -24,7 +24,7 @@ def _declared_functions():
 
 def test_library_exports_every_declared_symbol():
     declared = _declared_functions()
-    assert len(declared) == 12, declared
+    assert len(declared) == 13, declared
     lib = cobs.lib()
     for name in declared:
         assert hasattr(lib, name), name
@@ -44,9 +44,22 @@ def _cfg(**over):
 @pytest.mark.parametrize("md", ["f32", "bf16", "e2m1"])
 @pytest.mark.parametrize("fd", ["f32", "bf16", "e2m1"])
 @pytest.mark.parametrize("d,r", [(64, 2), (128, 4), (128, 16), (64, 0)])
-def test_record_bytes_match_oracle_layout(md, fd, d, r):
-    assert cobs.record_bytes(_cfg(head_dim=d, rank=r, mean_dtype=md, factor_dtype=fd)) == \
-        R.layout(d, r, md, fd)["total"]
+@pytest.mark.parametrize("skew,vmean", [(False, False), (True, False), (False, True), (True, True)])
+def test_record_bytes_match_oracle_layout(md, fd, d, r, skew, vmean):
+    assert cobs.record_bytes(_cfg(head_dim=d, rank=r, mean_dtype=md, factor_dtype=fd, skew=skew,
+                                  value_mean=vmean)) == R.layout(d, r, md, fd, skew, vmean)["total"]
+
+
+def test_unknown_options_and_compression_without_value_means_are_rejected():
+    lib = cobs.lib()
+    cfg = _cfg().c_struct()
+    cfg.options = 4
+    assert lib.cobs_record_bytes(ctypes.byref(cfg)) == 0
+    fake = ctypes.c_void_p(1 << 20)
+    plain = _cfg().c_struct()
+    assert lib.cobs_compression_branch(ctypes.byref(plain), fake, fake, fake, fake, None, None) == 1
+    vm = _cfg(value_mean=True).c_struct()
+    assert lib.cobs_compression_branch(ctypes.byref(vm), None, fake, fake, fake, None, None) == 1
 
 
 def test_workspace_sizes_are_aligned_and_ordered():

@@ -17,6 +17,7 @@ import torch
 
 import synth
 from oracle import method as M
+from oracle import records as R
 from paper_2607_09052_amd import cobs
 from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_records, check_selection, f32_config, f64,
                             oracle_decode, oracle_select, say, sync)
@@ -42,7 +43,11 @@ def _draw(seed):
     seq[0] = tmax
     if B > 1:
         seq[1] = int(rng.integers(1, 64))           # a row shorter than one block
-    return dict(G=G, d=d, Hkv=Hkv, B=B, tmax=tmax, kv=kv, md=md, fd=fd, r=r, s=s, w=w, seq=seq)
+    # optional record parts (skew coefficients, value means), drawn last so the
+    # other draws of a seed are unchanged
+    skew, vmean = bool(rng.random() < 0.3), bool(rng.random() < 0.3)
+    return dict(G=G, d=d, Hkv=Hkv, B=B, tmax=tmax, kv=kv, md=md, fd=fd, r=r, s=s, w=w, seq=seq,
+                skew=skew, vmean=vmean)
 
 
 def _draw_long(seed):
@@ -95,7 +100,7 @@ def _check(c, data_seed, tag):
     prob = synth.make_problem("c2", seed=data_seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"])
     cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
                       rank=c["r"], budget=c["s"], window=c["w"], kv_dtype=c["kv"], mean_dtype=c["md"],
-                      factor_dtype=c["fd"])
+                      factor_dtype=c["fd"], skew=c.get("skew", False), value_mean=c.get("vmean", False))
     q, k, v = prob["q"], prob["k"], prob["v"]
     qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
     seq_d = torch.from_numpy(c["seq"]).to(DEV)
@@ -123,6 +128,9 @@ def _check(c, data_seed, tag):
     out1, lse1 = torch.empty_like(out), torch.empty_like(lse)
     cobs.cobs_decode_step(cfg, qd, kd, vd, seq_d, rec1, out1, cobs.new_workspace(cfg, cobs.OP_STEP, DEV),
                           sel=sel1 if c["s"] > 0 else None, lse=lse1)
+    if cfg.value_mean:
+        out_c, lse_c = torch.empty_like(out), torch.empty_like(lse)
+        cobs.cobs_compression_branch(cfg, qd, rec, seq_d, out_c, lse_c)
     sync()
     rec_h, sc_h, rec32_h = rec.cpu().numpy(), scores.cpu().numpy(), rec32.cpu().numpy()
     sel_h, out_h, lse_h = sel_c.cpu().numpy(), out.cpu().numpy(), lse.cpu().numpy()
@@ -134,7 +142,7 @@ def _check(c, data_seed, tag):
         blocks = None if nb <= 64 else sorted(set(range(0, nb, nb // 32)) | {nb - 2, nb - 1})
         for h in range(Hkv):
             gs = slice(h * G, (h + 1) * G)
-            check_records(cfg, rec_h[b, h], rec32_h[b, h], f64(k[b, h]), T, blocks)
+            check_records(cfg, rec_h[b, h], rec32_h[b, h], f64(k[b, h]), T, blocks, f64(v[b, h]))
             sigma, nc, _ = oracle_select(rec_h[b, h], q[b, gs].double().numpy(), T, cfg)
             assert np.all(np.abs(sc_h[b, h, :nc] - sigma[:nc]) <= SIGMA_TOL)
             assert np.all(np.isneginf(sc_h[b, h, nc:]))
@@ -142,6 +150,11 @@ def _check(c, data_seed, tag):
                 check_selection(sel_h[b, h], sigma, nc, c["s"])
             o, l = oracle_decode(q[b, gs].double().numpy(), f64(k[b, h]), f64(v[b, h]), T, sel_h[b, h], cfg)
             check_out(out_h[b, gs], lse_h[b, gs], o, l, c["kv"])
+            if cfg.value_mean:
+                nb = -(-T // 64)
+                parts = R.decode(rec_h[b, h, :nb], d, cfg.rank, c["md"], c["fd"], cfg.skew, True)
+                o, l = M.compression_attention(q[b, gs].double().numpy(), parts[0], parts[1], parts[4], cfg.scale)
+                check_out(out_c[b, gs].cpu().numpy(), lse_c[b, gs].cpu().numpy(), o, l, "f32")
     assert torch.equal(rec1, rec)
     if c["s"] > 0:
         assert torch.equal(sel1, sel_c)
@@ -210,7 +223,7 @@ def test_random_paged_cache_is_bitwise_contiguous(seed):
     prob = synth.make_problem("c2", seed=8000 + seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"])
     cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
                       rank=c["r"], budget=s, window=w, kv_dtype=c["kv"], mean_dtype=c["md"],
-                      factor_dtype=c["fd"])
+                      factor_dtype=c["fd"], skew=c["skew"], value_mean=c["vmean"])
     q, k, v = prob["q"].to(DEV), prob["k"].to(DEV), prob["v"].to(DEV)
     nbm = tmax // 64
     pages = B * nbm + 3
