@@ -37,7 +37,7 @@ cobs_status_t check_config(const cobs_config_t* c) {
   const int g = c->num_q_heads / c->num_kv_heads;
   if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return COBS_ERR_UNSUPPORTED;
   if (c->head_dim != 64 && c->head_dim != 128) return COBS_ERR_UNSUPPORTED;
-  if (c->block_size != kL) return COBS_ERR_UNSUPPORTED;
+  if (c->block_size != 32 && c->block_size != 64 && c->block_size != 128) return COBS_ERR_UNSUPPORTED;
   if (c->rank > kMaxRank) return COBS_ERR_UNSUPPORTED;
   if (c->max_seq_len / c->block_size > kMaxBlocksPerSeq) return COBS_ERR_UNSUPPORTED;
   if (c->options & ~(COBS_OPT_SKEW | COBS_OPT_VALUE_MEAN)) return COBS_ERR_INVALID_ARG;
@@ -46,6 +46,7 @@ cobs_status_t check_config(const cobs_config_t* c) {
 
 struct Derived {
   int B, hq, hkv, G, d, tmax, nbmax, r, s, w, units;
+  int L, lsh;           // block length and its log2
   int mdt, fdt, kv_f32;
   int skew, vmean;      // optional record parts
   float c;
@@ -67,7 +68,9 @@ Derived derive(const cobs_config_t* c) {
   v.G = v.hq / v.hkv;
   v.d = c->head_dim;
   v.tmax = c->max_seq_len;
-  v.nbmax = v.tmax / kL;
+  v.L = c->block_size;
+  v.lsh = v.L == 32 ? 5 : (v.L == 64 ? 6 : 7);
+  v.nbmax = v.tmax / v.L;
   v.r = c->rank;
   v.s = c->budget;
   v.w = c->window;
@@ -82,7 +85,7 @@ Derived derive(const cobs_config_t* c) {
 
   // grid bounds for the workspace; the launchers pick the actual grids within them
   v.nch_max = (v.nbmax + select_min_bpw(v.mdt, v.fdt) - 1) / select_min_bpw(v.mdt, v.fdt);
-  v.nwg_max = decode_max_wg(v.s, v.w, v.nbmax, v.kv_f32 != 0);
+  v.nwg_max = decode_max_wg(v.s, v.w, v.nbmax, v.kv_f32 != 0, v.L);
 
   size_t off = 0;
   v.sel_ell = off;  off = round_up(off + sizeof(float) * (size_t)v.units * v.G * v.nbmax, kAlign);
@@ -130,6 +133,7 @@ KvView make_view(const cobs_kv_t* kv, const Derived& v) {
   x.nbmax = v.nbmax;
   x.hkv = v.hkv;
   x.d = v.d;
+  x.lsh = v.lsh;
   return x;
 }
 
@@ -191,6 +195,7 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
   p.fdt = v.fdt;
   p.nch = v.nch_max;
   p.bpw = 0;
+  p.lsh = v.lsh;
   p.skew = v.skew;
   p.vmean = v.vmean;
   p.c = v.c;
@@ -223,6 +228,7 @@ cobs_status_t run_select_exact(const Derived& v, const float* q, const cobs_kv_t
   p.fdt = v.fdt;
   p.nch = v.nchx_max;
   p.bpw = 0;
+  p.lsh = v.lsh;
   p.skew = 0;
   p.vmean = 0;
   p.c = v.c;
@@ -255,6 +261,7 @@ cobs_status_t run_decode(const Derived& v, const float* q, const cobs_kv_t* kv,
   p.w = v.w;
   p.nwg = v.nwg_max;
   p.spw = 0;
+  p.lsh = v.lsh;
   p.c = v.c;
   return hip_status(launch_decode(p, v.d, v.G, v.kv_f32 != 0, v.B, v.nbmax, st));
 }
@@ -275,7 +282,7 @@ cobs_status_t run_step(const Derived& v, const float* q, const cobs_kv_t* kv, co
                        void* summaries, int32_t* sel, float* out, float* lse, uint8_t* wsb, hipStream_t st) {
   cobs_status_t s;
   int32_t* selp = sel ? sel : reinterpret_cast<int32_t*>(wsb + v.step_sel);
-  if (select_refreshes(v.r, v.kv_f32 != 0)) {
+  if (select_refreshes(v.r, v.kv_f32 != 0, v.L)) {
     // the selector's launch recomputes the newest block's record before scoring
     if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st, kv)) != COBS_OK) return s;
     return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
@@ -505,6 +512,7 @@ cobs_status_t cobs_compression_branch(const cobs_config_t* cfg, const float* q, 
   p.nbmax = v.nbmax;
   p.tmax = v.tmax;
   p.mdt = v.mdt;
+  p.lsh = v.lsh;
   p.c = v.c;
   p.lay = v.lay;
   return hip_status(launch_compress(p, v.d, v.G, v.B, static_cast<hipStream_t>(stream)));

@@ -4,15 +4,15 @@
 
 namespace cobs {
 
-// One 256-thread workgroup per (batch row, KV head, block).
-template <int D, int P, bool KF32>
+// One 256-thread workgroup per (batch row, KV head, block) of LB tokens.
+template <int D, int P, int LB, bool KF32>
 __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams p) {
-  __shared__ __align__(16) char pool[stats_lds_bytes<D, P, KF32>()];
+  __shared__ __align__(16) char pool[stats_lds_bytes<D, P, LB, KF32>()];
   const int b = blockIdx.z, h = blockIdx.y;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   if (T <= 0) return;
-  const int nb = (T + kL - 1) / kL;
-  const int j = p.tail_mode ? (T - 1) / kL : p.first_block + (int)blockIdx.x;
+  const int nb = (T + LB - 1) / LB;
+  const int j = p.tail_mode ? (T - 1) / LB : p.first_block + (int)blockIdx.x;
   if (j < 0 || j >= nb) return;
   StatsArgs a;
   a.kv = p.kv;
@@ -25,7 +25,7 @@ __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams 
   a.skew = p.skew;
   a.vmean = p.vmean;
   a.lay = p.lay;
-  block_stats<D, P, KF32>(a, b, h, j, min(kL, T - j * kL), pool);
+  block_stats<D, P, LB, KF32>(a, b, h, j, min(LB, T - j * LB), pool);
 }
 
 // E2M1 encoding of independent vectors, one workgroup per vector.
@@ -52,11 +52,20 @@ __global__ __launch_bounds__(256) void pack_e2m1_kernel(const float* x, int dim,
 }
 
 // ------------------------------------------------------------- launchers --
+template <int D, int P, int LB>
+static hipError_t launch_build_dpl(const BuildParams& p, dim3 grid, hipStream_t st) {
+  if (p.kv_f32) hipLaunchKernelGGL((build_stats_kernel<D, P, LB, true>), grid, dim3(kBuildThreads), 0, st, p);
+  else hipLaunchKernelGGL((build_stats_kernel<D, P, LB, false>), grid, dim3(kBuildThreads), 0, st, p);
+  return hipGetLastError();
+}
+
 template <int D, int P>
 static hipError_t launch_build_dp(const BuildParams& p, dim3 grid, hipStream_t st) {
-  if (p.kv_f32) hipLaunchKernelGGL((build_stats_kernel<D, P, true>), grid, dim3(kBuildThreads), 0, st, p);
-  else hipLaunchKernelGGL((build_stats_kernel<D, P, false>), grid, dim3(kBuildThreads), 0, st, p);
-  return hipGetLastError();
+  switch (p.kv.lsh) {
+    case 5: return launch_build_dpl<D, P, 32>(p, grid, st);
+    case 7: return launch_build_dpl<D, P, 128>(p, grid, st);
+    default: return launch_build_dpl<D, P, 64>(p, grid, st);
+  }
 }
 
 hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st) {

@@ -6,7 +6,8 @@
 
 namespace cobs {
 
-constexpr int kL = 64;          // tokens per block (one token per lane of a wave)
+constexpr int kL = 64;          // block length of the decode step's fused newest-block refresh
+constexpr int kMaxL = 128;      // block lengths: 32, 64 or 128 tokens
 constexpr int kMaxG = 16;       // query heads per KV head
 constexpr int kMaxRank = 16;
 constexpr int kMaxBlocksPerSeq = 8192;   // T_max / L bound for the in-LDS top-s
@@ -98,17 +99,21 @@ struct KvView {
   int nbmax;                     // T_max / L
   int hkv;
   int d;
+  int lsh;                       // log2 of the block length L
 };
 
 // Element offset of token t of (b, h); -1 when its page id is out of range.
 __device__ __forceinline__ int64_t kv_offset(const KvView& kv, int b, int h, int t) {
   if (kv.table == nullptr) return (int64_t)b * kv.sb + (int64_t)h * kv.sh + (int64_t)t * kv.st;
-  int page = kv.table[(int64_t)b * kv.nbmax + t / kL];
+  int page = kv.table[(int64_t)b * kv.nbmax + (t >> kv.lsh)];
   if (page < 0 || (int64_t)page >= kv.num_pages) return -1;
-  return (((int64_t)page * kv.hkv + h) * kL + (t % kL)) * (int64_t)kv.d;
+  return ((((int64_t)page * kv.hkv + h) << kv.lsh) + (t & ((1 << kv.lsh) - 1))) * (int64_t)kv.d;
 }
 
 __device__ __forceinline__ int clamp_len(int T, int tmax) { return T < 0 ? 0 : (T > tmax ? tmax : T); }
+
+// Blocks of 2^lsh tokens holding t tokens: ceil(t / L).
+__host__ __device__ __forceinline__ int blocks_of(int t, int lsh) { return (t + (1 << lsh) - 1) >> lsh; }
 
 // -------------------------------------------------------- wave reductions --
 __device__ __forceinline__ float wave_sum(float x) {

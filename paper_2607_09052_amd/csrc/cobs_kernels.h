@@ -26,6 +26,7 @@ struct SelectParams {
   float* part;      // [B*Hkv][nch][G][2]
   unsigned* cnt;    // [B*Hkv] arrival counters
   int hkv, hq, nbmax, tmax, r, s, w, mdt, fdt, nch, bpw;
+  int lsh;          // log2 of the block length
   int skew, vmean;  // records carry skew coefficients (scored) / a value mean (kept by the refresh)
   float c;
   RecLayout lay;
@@ -46,6 +47,7 @@ struct DecodeParams {
   float* part;      // [B*Hkv][nwg][G][D + 2]
   unsigned* cnt;    // [B*Hkv] arrival counters
   int hkv, hq, tmax, s, w, nwg, spw;   // spw: work items (segments or pieces) per workgroup
+  int lsh;          // log2 of the block length
   int units;        // B*Hkv
   float c;
   // nwg_s < 0: one output over the union.  nwg_s >= 0 (bf16 K/V): the
@@ -65,7 +67,7 @@ struct CompressParams {
   const int32_t* seq_lens;
   float* out;
   float* lse;
-  int hkv, hq, nbmax, tmax, mdt;
+  int hkv, hq, nbmax, tmax, mdt, lsh;
   float c;
   RecLayout lay;
 };
@@ -79,12 +81,12 @@ hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st
 bool select_on_matrix_cores(int mdt, int fdt);
 int select_min_bpw(int mdt, int fdt);
 hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int nbmax, hipStream_t st);
-bool select_refreshes(int r, bool kv_f32);
+bool select_refreshes(int r, bool kv_f32, int L);
 // Dense-key selectors (exact masses; `quest`: Quest boxes): the SelectParams of
 // the selector with `kv` set (bf16 keys).
 hipError_t launch_select_exact(SelectParams p, int d, int g, int batch, hipStream_t st, bool quest);
 int select_exact_min_bpw();
-int decode_max_wg(int s, int w, int nbmax, bool f32);
+int decode_max_wg(int s, int w, int nbmax, bool f32, int L);
 
 // Resident workgroups of `threads` threads per CU for a kernel, and the CU
 // count, of the current device (cached per device and kernel).

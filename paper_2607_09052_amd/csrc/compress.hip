@@ -100,7 +100,7 @@ __global__ __launch_bounds__(kCmpThreads) void compress_kernel(CompressParams p)
   const int unit = blockIdx.x;
   const int b = unit / p.hkv, h = unit % p.hkv;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
-  const int nb = (T + kL - 1) / kL;
+  const int nb = blocks_of(T, p.lsh);
   const uint8_t* recu = p.rec + (int64_t)unit * p.nbmax * p.lay.total;
   for (int idx = tid; idx < G * D; idx += kCmpThreads)
     qs[idx / D][idx % D] = p.q[((int64_t)b * p.hq + h * G) * D + idx] * p.c;

@@ -47,7 +47,13 @@ __device__ __forceinline__ int64_t wave_uniform(int64_t x) {
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-// Token range of work item `it` (PT tokens per item, kL / PT items per segment):
+// Items of at most PT tokens per block of L = 2^lsh tokens (L / PT, at least 1).
+template <int PT>
+__device__ __forceinline__ int items_per_block(int lsh) {
+  return (1 << lsh) > PT ? (1 << lsh) / PT : 1;
+}
+
+// Token range of work item `it` (PT tokens per item, items_per_block per segment):
 // n tokens from the element offset `base` of its first token, consecutive tokens
 // `rs` elements apart.  Segment i < s is selected block sel[i] (only while i is
 // inside the valid selection prefix), cut at the window start; segment s + j is
@@ -56,18 +62,19 @@ __device__ __forceinline__ int64_t wave_uniform(int64_t x) {
 template <int PT>
 __device__ __forceinline__ void item_range(const DecodeParams& p, int selv, int kvalid, int b, int h,
                                            int T, int ws, int it, int& n, int64_t& base) {
-  constexpr int IPS = kL / PT;
-  const int seg = it / IPS, part = it % IPS;
+  const int ips = items_per_block<PT>(p.lsh);
+  const int L = 1 << p.lsh;
+  const int seg = it / ips, part = it % ips;
   int t0 = 0, t1 = 0;
   if (seg < p.s) {
     if (seg < kvalid) {
-      t0 = selv * kL;
-      t1 = min(t0 + kL, ws);
+      t0 = selv * L;
+      t1 = min(t0 + L, ws);
     }
   } else {
-    const int jb = ws / kL + (seg - p.s);
-    t0 = max(ws, jb * kL);
-    t1 = min(T, jb * kL + kL);
+    const int jb = (ws >> p.lsh) + (seg - p.s);
+    t0 = max(ws, jb * L);
+    t1 = min(T, jb * L + L);
   }
   const int a0 = t0 + PT * part;
   n = max(0, min(t1 - a0, PT));
@@ -88,7 +95,7 @@ __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, in
   const int unit = b * p.hkv + h;
   const int32_t* sl = p.sel + (int64_t)unit * p.s;
   const int it = first + tid;
-  const int seg = it / (kL / PT);
+  const int seg = it / items_per_block<PT>(p.lsh);
   const int selv = (p.s > 0) ? sl[(tid < cnt && seg < p.s) ? seg : 0] : 0;
   int kv = p.s;                 // first entry breaking the ascending run of candidates
   for (int i = tid; i < p.s; i += NT) {
@@ -213,9 +220,9 @@ __device__ __forceinline__ void decode_task(const DecodeParams& p, int b, int h,
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   const int ws = max(0, T - p.w);
-  const int nc = (ws + kL - 1) / kL;
-  const int nwin = (T > ws) ? ((T - 1) / kL - ws / kL + 1) : 0;
-  const int nseg = p.s + nwin;
+  const int nc = blocks_of(ws, p.lsh);
+  const int nwin = (T > ws) ? (((T - 1) >> p.lsh) - (ws >> p.lsh) + 1) : 0;
+  const int nseg = items_per_block<64>(p.lsh) * (p.s + nwin);   // segments of <= 64 tokens
   const int seg_lo = wg * p.spw, seg_end = min(nseg, seg_lo + p.spw);
   const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;        // elements between consecutive tokens
 
@@ -234,7 +241,7 @@ __device__ __forceinline__ void decode_task(const DecodeParams& p, int b, int h,
 
   for (int sb = seg_lo; sb < seg_end; sb += kDecThreads) {
    const int cnt = min(kDecThreads, seg_end - sb);
-   decode_prologue<D, G, kL>(p, b, h, T, ws, nc, sb, cnt, sb == seg_lo, qs, s_red, pn_s, pbase_s);
+   decode_prologue<D, G, 64>(p, b, h, T, ws, nc, sb, cnt, sb == seg_lo, qs, s_red, pn_s, pbase_s);
    for (int it = wave; it < cnt; it += 4) {
     const int n = wave_uniform(pn_s[it]);
     if (n == 0) continue;
@@ -452,17 +459,18 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   const int ws = max(0, T - p.w);
-  const int nc = (ws + kL - 1) / kL;
-  const int nwin = (T > ws) ? ((T - 1) / kL - ws / kL + 1) : 0;
-  const int npiece = 2 * (p.s + nwin);
+  const int nc = blocks_of(ws, p.lsh);
+  const int nwin = (T > ws) ? (((T - 1) >> p.lsh) - (ws >> p.lsh) + 1) : 0;
+  const int ipb = items_per_block<PT>(p.lsh);
+  const int npiece = ipb * (p.s + nwin);
   // one output: the unit's pieces in order; two: the first nwg_s workgroups
   // take the selected blocks' pieces, the others the window's
   int pc_lo = wg * p.spw, pc_end = min(npiece, pc_lo + p.spw);
   if constexpr (BR) {
     if (wg < p.nwg_s) {
-      pc_end = min(2 * p.s, pc_lo + p.spw);
+      pc_end = min(ipb * p.s, pc_lo + p.spw);
     } else {
-      pc_lo = 2 * p.s + (wg - p.nwg_s) * p.spw;
+      pc_lo = ipb * p.s + (wg - p.nwg_s) * p.spw;
       pc_end = min(npiece, pc_lo + p.spw);
     }
   }
@@ -773,13 +781,18 @@ static DecodeKernel decode_kernel_d(int g, bool f32, bool br) {
 
 // Work items per (batch row, KV head): segments of <= 64 tokens (fp32 K/V) or
 // pieces of <= 32 (bf16 K/V) of the selected blocks and the window's blocks.
-int decode_items(int s, int w, int nbmax, bool f32) {
-  const int nwin_max = (w == 0) ? 0 : std::min(nbmax, (w + kL - 1) / kL + 1);
-  return (f32 ? 1 : 2) * (s + nwin_max);
+static int host_items_per_block(bool f32, int L) {
+  const int pt = f32 ? 64 : 32;
+  return L > pt ? L / pt : 1;
 }
 
-int decode_max_wg(int s, int w, int nbmax, bool f32) {
-  return std::max(1, std::min(kMaxDecodeWg, (decode_items(s, w, nbmax, f32) + 3) / 4));
+int decode_items(int s, int w, int nbmax, bool f32, int L) {
+  const int nwin_max = (w == 0) ? 0 : std::min(nbmax, (w + L - 1) / L + 1);
+  return host_items_per_block(f32, L) * (s + nwin_max);
+}
+
+int decode_max_wg(int s, int w, int nbmax, bool f32, int L) {
+  return std::max(1, std::min(kMaxDecodeWg, (decode_items(s, w, nbmax, f32, L) + 3) / 4));
 }
 
 // A unit's work items split over nwg <= kMaxDecodeWg workgroups (one partial
@@ -789,7 +802,8 @@ hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int 
   const bool br = p.nwg_s >= 0;
   const DecodeKernel k = (d == 128) ? decode_kernel_d<128>(g, f32, br) : decode_kernel_d<64>(g, f32, br);
   const int nt = f32 ? kDecThreads : (g <= 4 ? decode_threads<4>() : (g <= 8 ? decode_threads<8>() : decode_threads<16>()));
-  const int items = decode_items(p.s, p.w, nbmax, f32);
+  const int L = 1 << p.lsh;
+  const int items = decode_items(p.s, p.w, nbmax, f32, L);
   const int64_t units = (int64_t)batch * p.hkv;
   const int64_t slots = (int64_t)resident_workgroups(reinterpret_cast<const void*>(k), nt) * device_cus();
   // one round of the chip's resident workgroup slots, the items spread evenly
@@ -803,7 +817,7 @@ hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int 
   if (p.nwg_s >= 0) {
     // two outputs: no workgroup mixes the branches; the split stays within
     // the workspace's partial count
-    const int is = 2 * p.s, iw = items - is, cap = decode_max_wg(p.s, p.w, nbmax, false);
+    const int is = host_items_per_block(false, L) * p.s, iw = items - is, cap = decode_max_wg(p.s, p.w, nbmax, false, L);
     int sp = (int)spw;
     while ((is + sp - 1) / sp + (iw + sp - 1) / sp > cap) ++sp;
     p.spw = sp;

@@ -15,8 +15,8 @@ SelectKernel select_refresh_kernel_for(const SelectParams& p, int d, int g);
 bool select_on_matrix_cores(int mdt, int fdt) { return mdt != DT_F32 && fdt != DT_F32; }
 
 // The selector can recompute the newest block's record itself (bf16 keys,
-// rank <= 4).
-bool select_refreshes(int r, bool kv_f32) { return !kv_f32 && r <= 4; }
+// rank <= 4, blocks of kL tokens).
+bool select_refreshes(int r, bool kv_f32, int L) { return !kv_f32 && r <= 4 && L == kL; }
 
 int select_min_bpw(int mdt, int fdt) { return select_on_matrix_cores(mdt, fdt) ? 64 : 16; }
 

@@ -37,7 +37,8 @@ __device__ __forceinline__ void select_exact_task(const SelectParams& p, int b, 
   const int hcol = lane & 15, grp = lane >> 4;
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
-  const int nb = (T + kL - 1) / kL;
+  const int nb = blocks_of(T, p.lsh);
+  const int L = 1 << p.lsh;
   const int blk_lo = chunk * p.bpw, blk_hi = min(nb, blk_lo + p.bpw);
   const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;    // elements between consecutive tokens of a block
   const char* kbase = static_cast<const char*>(p.kv.k);
@@ -67,47 +68,53 @@ __device__ __forceinline__ void select_exact_task(const SelectParams& p, int b, 
 
   float run_m = -INFINITY, run_s = 0.0f;       // this wave's blocks, head hcol
   for (int blk = blk_lo + wave; blk < blk_hi; blk += kExactBlocksPerPass) {
-    const int n = min(kL, T - blk * kL);
-    const int64_t t0 = kv_offset(p.kv, b, h, blk * kL);
+    const int n = min(L, T - blk * L);
+    const int64_t t0 = kv_offset(p.kv, b, h, blk * L);
     float l = -INFINITY;
     if (t0 >= 0) {
-      // rows past n re-read row n - 1; their scores are masked
-      uint4 kr[4][KST];
+      // the block's rows in runs of 64 (one for L <= 64, two for L = 128), each
+      // a 64 x 16 score tile; rows past n re-read row n - 1 and are masked
+      float mx = -INFINITY, se = 0.0f;
+      for (int h0 = 0; h0 < n; h0 += 64) {
+        const int nh = min(64, n - h0);
+        uint4 kr[4][KST];
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        const uint4* row = reinterpret_cast<const uint4*>(
-            kbase + (t0 + (int64_t)min(16 * mt + hcol, n - 1) * rs) * 2 + 16 * grp);
+        for (int mt = 0; mt < 4; ++mt) {
+          const uint4* row = reinterpret_cast<const uint4*>(
+              kbase + (t0 + (int64_t)(h0 + min(16 * mt + hcol, nh - 1)) * rs) * 2 + 16 * grp);
 #pragma unroll
-        for (int kk = 0; kk < KST; ++kk) kr[mt][kk] = row[4 * kk];
-      }
-      float sc[4][4];
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
-        f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int kk = 0; kk < KST; ++kk) {
-          const sbf16x8_t a = __builtin_bit_cast(sbf16x8_t, kr[mt][kk]);
-#pragma unroll
-          for (int part = 0; part < 3; ++part) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qb[part][kk], acc, 0, 0, 0);
+          for (int kk = 0; kk < KST; ++kk) kr[mt][kk] = row[4 * kk];
         }
+        float sc[4][4];
 #pragma unroll
-        for (int v = 0; v < 4; ++v) sc[mt][v] = (16 * mt + 4 * grp + v < n) ? acc[v] : -INFINITY;
+        for (int mt = 0; mt < 4; ++mt) {
+          f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+          for (int kk = 0; kk < KST; ++kk) {
+            const sbf16x8_t a = __builtin_bit_cast(sbf16x8_t, kr[mt][kk]);
+#pragma unroll
+            for (int part = 0; part < 3; ++part) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qb[part][kk], acc, 0, 0, 0);
+          }
+#pragma unroll
+          for (int v = 0; v < 4; ++v) sc[mt][v] = (16 * mt + 4 * grp + v < nh) ? acc[v] : -INFINITY;
+        }
+        // log-sum-exp over these rows, head hcol (lanes hcol + 16 g)
+        float hm = -INFINITY;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) hm = fmaxf(hm, sc[mt][v]);
+        hm = fmaxf(hm, __shfl_xor(hm, 16, 64));
+        hm = fmaxf(hm, __shfl_xor(hm, 32, 64));
+        float hs = 0.0f;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) hs += (sc[mt][v] == -INFINITY) ? 0.0f : __expf(sc[mt][v] - hm);
+        hs += __shfl_xor(hs, 16, 64);
+        hs += __shfl_xor(hs, 32, 64);
+        lse_merge(mx, se, hm, hs);
       }
-      // log-sum-exp over the block's tokens, head hcol (lanes hcol + 16 g)
-      float mx = -INFINITY;
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) mx = fmaxf(mx, sc[mt][v]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      float se = 0.0f;
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) se += (sc[mt][v] == -INFINITY) ? 0.0f : __expf(sc[mt][v] - mx);
-      se += __shfl_xor(se, 16, 64);
-      se += __shfl_xor(se, 32, 64);
       l = mx + __logf(se);
     }
     if (grp == 0 && hcol < G) {
@@ -130,7 +137,7 @@ __device__ __forceinline__ void select_exact_task(const SelectParams& p, int b, 
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
   FinishLds& fin = *reinterpret_cast<FinishLds*>(pool);
-  const int nc = (max(0, T - p.w) + kL - 1) / kL;
+  const int nc = blocks_of(max(0, T - p.w), p.lsh);
   if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
   else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
   else finish_select<G, kMaxBlocksPerSeq / kSelThreads>(p, unit, T, fin);
@@ -175,7 +182,8 @@ __device__ __forceinline__ void select_quest_task(const SelectParams& p, int b, 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
-  const int nb = (T + kL - 1) / kL;
+  const int nb = blocks_of(T, p.lsh);
+  const int L = 1 << p.lsh;
   const int blk_lo = chunk * p.bpw, blk_hi = min(nb, blk_lo + p.bpw);
   const int64_t rs = p.kv.table ? p.kv.d : p.kv.st;
   const char* kbase = static_cast<const char*>(p.kv.k);
@@ -190,16 +198,15 @@ __device__ __forceinline__ void select_quest_task(const SelectParams& p, int b, 
 #pragma unroll
   for (int g = 0; g < G; ++g) { run_m[g] = -INFINITY; run_s[g] = 0.0f; }
   for (int blk = blk_lo + wave; blk < blk_hi; blk += kExactBlocksPerPass) {
-    const int n = min(kL, T - blk * kL);
-    const int64_t t0 = kv_offset(p.kv, b, h, blk * kL);
+    const int n = min(L, T - blk * L);
+    const int64_t t0 = kv_offset(p.kv, b, h, blk * L);
     float l[G];
     if (t0 >= 0) {
       float mn[CPL], mx[CPL];
 #pragma unroll
       for (int e = 0; e < CPL; ++e) { mn[e] = INFINITY; mx[e] = -INFINITY; }
       const char* col = kbase + t0 * 2 + lane * CPL * 2;
-#pragma unroll
-      for (int r0 = 0; r0 < kL; r0 += 16) {
+      for (int r0 = 0; r0 < n; r0 += 16) {
         uint32_t w[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -251,7 +258,7 @@ __device__ __forceinline__ void select_quest_task(const SelectParams& p, int b, 
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
   FinishLds& fin = *reinterpret_cast<FinishLds*>(pool);
-  const int nc = (max(0, T - p.w) + kL - 1) / kL;
+  const int nc = blocks_of(max(0, T - p.w), p.lsh);
   if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
   else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
   else finish_select<G, kMaxBlocksPerSeq / kSelThreads>(p, unit, T, fin);

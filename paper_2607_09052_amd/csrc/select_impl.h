@@ -161,7 +161,7 @@ __device__ __forceinline__ void finish_select(const SelectParams& p, int unit, i
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
   const int ws = max(0, T - p.w);
-  const int nc = (ws + kL - 1) / kL;                 // candidates: b L < T - w
+  const int nc = blocks_of(ws, p.lsh);               // candidates: b L < T - w
   const int k = min(p.s, nc);
   const int U = (nc + kSelThreads - 1) / kSelThreads;
   const __amdgpu_buffer_rsrc_t ellu = coherent_view(p.ell + (int64_t)unit * p.nbmax * G, 4u * p.nbmax * G);
@@ -380,7 +380,7 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
   const int tid = threadIdx.x;
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
-  const int nb = (T + kL - 1) / kL;
+  const int nb = blocks_of(T, p.lsh);
   const int grp = tid >> 4, ln = tid & 15;
   const int r = p.r, rlast = max(r - 1, 0);
   const int fstride = (r > 0) ? p.lay.vec_bytes : 0;
@@ -509,7 +509,7 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
   FinishLds& fin = *reinterpret_cast<FinishLds*>(pool);
-  const int nc = (max(0, T - p.w) + kL - 1) / kL;
+  const int nc = blocks_of(max(0, T - p.w), p.lsh);
   if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
   else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
   else finish_select<G, kMaxBlocksPerSeq / kSelThreads>(p, unit, T, fin);
@@ -575,7 +575,7 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int unit = b * p.hkv + h;
   const int T = clamp_len(p.seq_lens[b], p.tmax);
-  const int nb = (T + kL - 1) / kL;
+  const int nb = blocks_of(T, p.lsh);
   const int hcol = lane & 15, grp = lane >> 4;
   const int r = p.r, rlast = max(r - 1, 0);
   const int fstride = (r > 0) ? p.lay.vec_bytes : 0;
@@ -716,7 +716,7 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
   }
   if (!arrive_last(p.cnt + unit, (unsigned)p.nch, &s_last)) return;
   FinishLds& fin = *reinterpret_cast<FinishLds*>(pool);
-  const int nc = (max(0, T - p.w) + kL - 1) / kL;
+  const int nc = blocks_of(max(0, T - p.w), p.lsh);
   if (nc <= 2 * kSelThreads) finish_select<G, 2>(p, unit, T, fin);
   else if (nc <= 8 * kSelThreads) finish_select<G, 8>(p, unit, T, fin);
   else finish_select<G, kMaxBlocksPerSeq / kSelThreads>(p, unit, T, fin);
@@ -738,7 +738,7 @@ __global__ __launch_bounds__(kSelThreads) void select_mfma_kernel(SelectParams p
 template <size_t A, size_t B>
 constexpr size_t lds_max() { return A > B ? A : B; }
 
-// The decode step's selector (bf16 keys, r <= 4): the workgroup whose chunk
+// The decode step's selector (bf16 keys, r <= 4, L = kL): the workgroup whose chunk
 // holds row b's newest block first recomputes that block's record (its count,
 // mean and, once full, factors: the statistics follow the block as it fills,
 // §5.6), so the block's score and the normaliser over all blocks see the
@@ -747,7 +747,7 @@ constexpr size_t lds_max() { return A > B ? A : B; }
 template <int D, int G, int MDT, int FDT>
 constexpr size_t select_refresh_lds() {
   constexpr bool kMat = MDT != DT_F32 && FDT != DT_F32;
-  return lds_max<kMat ? select_mfma_lds<G, 4, FDT>() : select_valu_lds<G>(), stats_lds_bytes<D, 16, false>()>();
+  return lds_max<kMat ? select_mfma_lds<G, 4, FDT>() : select_valu_lds<G>(), stats_lds_bytes<D, 16, kL, false>()>();
 }
 
 template <int D, int G, int MDT, int FDT>
@@ -767,7 +767,7 @@ __device__ __forceinline__ void select_refresh_task(const SelectParams& p, char*
     a.skew = p.skew;
     a.vmean = p.vmean;
     a.lay = p.lay;
-    block_stats<D, 16, false>(a, b, h, j, min(kL, T - j * kL), pool);
+    block_stats<D, 16, kL, false>(a, b, h, j, min(kL, T - j * kL), pool);
     __builtin_amdgcn_s_waitcnt(0);       // the record is written before it is scored
     __syncthreads();
   }

@@ -30,7 +30,8 @@ def config_from(cfg_dict, **over):
     c = dict(batch=cfg_dict["B"], num_q_heads=cfg_dict["Hq"], num_kv_heads=cfg_dict["Hkv"],
              head_dim=cfg_dict["d"], max_seq_len=cfg_dict["T_max"], rank=cfg_dict["r"],
              budget=cfg_dict["s"], window=cfg_dict["w"], kv_dtype=cfg_dict["kv_dtype"],
-             mean_dtype=cfg_dict["mean_dtype"], factor_dtype=cfg_dict["factor_dtype"])
+             mean_dtype=cfg_dict["mean_dtype"], factor_dtype=cfg_dict["factor_dtype"],
+             block_size=cfg_dict.get("L", 64))
     c.update(over)
     return cobs.Config(**c)
 

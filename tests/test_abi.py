@@ -77,7 +77,7 @@ def test_workspace_sizes_are_aligned_and_ordered():
     (dict(num_q_heads=7), 1),          # Hq not a multiple of Hkv
     (dict(num_q_heads=6, num_kv_heads=2), 2),   # G = 3
     (dict(head_dim=96), 2),
-    (dict(block_size=32), 2),
+    (dict(block_size=256), 2),         # L in {32, 64, 128}
     (dict(rank=17), 2),
     (dict(rank=-1), 1),
     (dict(max_seq_len=4000), 1),       # not a multiple of L

@@ -452,44 +452,48 @@ def test_paged_kv_matches_contiguous():
 
 # -------------------------------------------------------- block statistics --
 
-def _stats_cache(law, d, nblk, tail, seed):
-    """One KV head whose blocks follow `law`; last block partial with `tail` tokens."""
+def _stats_cache(law, d, nblk, tail, seed, L=64):
+    """One KV head whose blocks of L keys follow `law`; last block partial with `tail` tokens."""
     blocks = []
     for i in range(nblk):
         if law == "mixed":
             lw = ["gauss", "spiked", "lowrank", "const"][i % 4]
         else:
             lw = law
-        blocks.append(synth.make_keys_block(64, d, lw, seed + i, rank=3))
+        blocks.append(synth.make_keys_block(L, d, lw, seed + i, rank=3))
     K = np.concatenate(blocks)
-    T = (nblk - 1) * 64 + tail
+    T = (nblk - 1) * L + tail
     return K, T
 
 
-@pytest.mark.parametrize("law,d,r", [("gauss", 128, 4), ("spiked", 128, 4), ("mixed", 128, 8),
-                                     ("gauss", 64, 2), ("spiked", 128, 12), ("lowrank", 64, 6)])
-def test_build_stats_matches_oracle(law, d, r):
-    nblk, tail = 12, 37
-    K, T = _stats_cache(law, d, nblk, tail, seed=100 * r + d)
-    Tmax = nblk * 64
+@pytest.mark.parametrize("law,d,r,L", [("gauss", 128, 4, 64), ("spiked", 128, 4, 64), ("mixed", 128, 8, 64),
+                                       ("gauss", 64, 2, 64), ("spiked", 128, 12, 64), ("lowrank", 64, 6, 64),
+                                       ("mixed", 128, 4, 32), ("gauss", 64, 6, 32), ("spiked", 128, 4, 128),
+                                       ("mixed", 128, 12, 128), ("gauss", 64, 2, 128)])
+def test_build_stats_matches_oracle(law, d, r, L):
+    """Block statistics of the paper's block length (L = 32, Sec. 7.1) and of
+    64 and 128: counts, means, Ky-Fan energy, orthogonality, rank-r subspace."""
+    nblk, tail = 12, min(37, L - 1)
+    K, T = _stats_cache(law, d, nblk, tail, seed=100 * r + d + L, L=L)
+    Tmax = nblk * L
     k = torch.from_numpy(K).view(1, 1, Tmax, d).to(torch.float32)
     cfg = _cfg(batch=1, num_q_heads=1, num_kv_heads=1, head_dim=d, max_seq_len=Tmax, rank=r,
-               kv_dtype="f32")
-    say(f"build law={law} d={d} r={r}")
+               kv_dtype="f32", block_size=L)
+    say(f"build law={law} d={d} r={r} L={L}")
     rec = cobs.new_summaries(cfg, DEV)
     cobs.cobs_build_block_stats(cfg, k.to(DEV), k.to(DEV), torch.tensor([T], dtype=torch.int32, device=DEV), rec)
     sync()
     counts, means, factors = R.decode(rec[0, 0].cpu().numpy(), d, r, "f32", "f32")
-    oc, om, of = M.block_statistics(K.astype(np.float64), T, 64, r)
+    oc, om, of = M.block_statistics(K.astype(np.float64), T, L, r)
     np.testing.assert_array_equal(counts, oc)
     scale = np.abs(K).max()
     np.testing.assert_allclose(means, om, rtol=0, atol=1e-6 * scale)
     for blk in range(nblk):
         n = int(oc[blk])
-        if n < 64:
+        if n < L:
             assert np.all(factors[blk] == 0)
             continue
-        ky_fan_checks(factors[blk], K[blk * 64:blk * 64 + 64].astype(np.float64), n, r)
+        ky_fan_checks(factors[blk], K[blk * L:blk * L + L].astype(np.float64), n, r)
         # sign convention: the largest-magnitude entry of each stored vector is positive
         for i in range(r):
             if np.any(factors[blk, i] != 0):

@@ -43,18 +43,22 @@ def _draw(seed):
     seq[0] = tmax
     if B > 1:
         seq[1] = int(rng.integers(1, 64))           # a row shorter than one block
-    # optional record parts (skew coefficients, value means), drawn last so the
-    # other draws of a seed are unchanged
+    # optional record parts (skew coefficients, value means) and the block
+    # length, drawn last so the other draws of a seed are unchanged; T_max is
+    # rounded up to whole blocks
     skew, vmean = bool(rng.random() < 0.3), bool(rng.random() < 0.3)
+    L = int(rng.choice([32, 64, 64, 128]))
+    tmax = -(-tmax // L) * L
+    seq[0] = tmax
     return dict(G=G, d=d, Hkv=Hkv, B=B, tmax=tmax, kv=kv, md=md, fd=fd, r=r, s=s, w=w, seq=seq,
-                skew=skew, vmean=vmean)
+                skew=skew, vmean=vmean, L=L)
 
 
 def _draw_long(seed):
     """As _draw, with T_max up to 1024 blocks, budgets up to 119 and windows up to 3000."""
     c = _draw(seed)
     rng = np.random.default_rng(seed + 777)
-    tmax = 64 * int(rng.integers(40, 1025))
+    tmax = c["L"] * int(rng.integers(40, 1025) * 64 // c["L"])
     seq = rng.integers(1, tmax + 1, size=c["B"]).astype(np.int32)
     seq[0] = tmax
     if c["B"] > 1:
@@ -97,10 +101,12 @@ def test_random_configuration_with_empty_rows(seed):
 def _check(c, data_seed, tag):
     G, d, Hkv, B, tmax = c["G"], c["d"], c["Hkv"], c["B"], c["tmax"]
     say(f"{tag}: {c}")
-    prob = synth.make_problem("c2", seed=data_seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"])
+    L = c.get("L", 64)
+    prob = synth.make_problem("c2", seed=data_seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"], L=L)
     cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
                       rank=c["r"], budget=c["s"], window=c["w"], kv_dtype=c["kv"], mean_dtype=c["md"],
-                      factor_dtype=c["fd"], skew=c.get("skew", False), value_mean=c.get("vmean", False))
+                      factor_dtype=c["fd"], skew=c.get("skew", False), value_mean=c.get("vmean", False),
+                      block_size=L)
     q, k, v = prob["q"], prob["k"], prob["v"]
     qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
     seq_d = torch.from_numpy(c["seq"]).to(DEV)
@@ -123,7 +129,7 @@ def _check(c, data_seed, tag):
     seq_c = np.clip(c["seq"], 0, tmax)                 # lengths as the library reads them
     for b in range(B):
         if int(seq_c[b]) > 0:
-            rec1[b, :, (int(seq_c[b]) - 1) // 64] = 0
+            rec1[b, :, (int(seq_c[b]) - 1) // L] = 0
     sel1 = torch.empty_like(sel_c)
     out1, lse1 = torch.empty_like(out), torch.empty_like(lse)
     cobs.cobs_decode_step(cfg, qd, kd, vd, seq_d, rec1, out1, cobs.new_workspace(cfg, cobs.OP_STEP, DEV),
@@ -136,7 +142,7 @@ def _check(c, data_seed, tag):
     sel_h, out_h, lse_h = sel_c.cpu().numpy(), out.cpu().numpy(), lse.cpu().numpy()
     for b in range(B):
         T = int(seq_c[b])
-        nb = -(-T // 64)
+        nb = -(-T // L)
         # block statistics of this row: every block of short contexts, else a
         # stride of them plus the last two
         blocks = None if nb <= 64 else sorted(set(range(0, nb, nb // 32)) | {nb - 2, nb - 1})
@@ -151,7 +157,7 @@ def _check(c, data_seed, tag):
             o, l = oracle_decode(q[b, gs].double().numpy(), f64(k[b, h]), f64(v[b, h]), T, sel_h[b, h], cfg)
             check_out(out_h[b, gs], lse_h[b, gs], o, l, c["kv"])
             if cfg.value_mean:
-                nb = -(-T // 64)
+                nb = -(-T // L)
                 parts = R.decode(rec_h[b, h, :nb], d, cfg.rank, c["md"], c["fd"], cfg.skew, True)
                 o, l = M.compression_attention(q[b, gs].double().numpy(), parts[0], parts[1], parts[4], cfg.scale)
                 check_out(out_c[b, gs].cpu().numpy(), lse_c[b, gs].cpu().numpy(), o, l, "f32")
@@ -171,9 +177,10 @@ def test_random_diagnostic_entry_points(seed):
     c["kv"] = "bf16"
     G, d, Hkv, B, tmax, s, w = c["G"], c["d"], c["Hkv"], c["B"], c["tmax"], c["s"], c["w"]
     say(f"random diagnostic config {seed}: {c}")
-    prob = synth.make_problem("c2", seed=6000 + seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype="bf16")
+    L = c["L"]
+    prob = synth.make_problem("c2", seed=6000 + seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype="bf16", L=L)
     cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
-                      rank=c["r"], budget=s, window=w, kv_dtype="bf16")
+                      rank=c["r"], budget=s, window=w, kv_dtype="bf16", block_size=L)
     q, k, v = prob["q"], prob["k"], prob["v"]
     qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
     seq_d = torch.from_numpy(c["seq"]).to(DEV)
@@ -195,18 +202,18 @@ def test_random_diagnostic_entry_points(seed):
     oracles = {"exact": M.osa_group_scores, "quest": M.quest_group_scores}
     for b in range(B):
         T = int(c["seq"][b])
-        nc = M.candidate_count(T, 64, w)
+        nc = M.candidate_count(T, L, w)
         for h in range(Hkv):
             gs = slice(h * G, (h + 1) * G)
             qg, Kg = q[b, gs].double().numpy(), f64(k[b, h])
             for name, (sel, scores) in outs.items():
-                sigma = oracles[name](qg, Kg, T, 64, cfg.scale)
+                sigma = oracles[name](qg, Kg, T, L, cfg.scale)
                 got = scores[b, h].cpu().numpy()
                 assert np.all(np.abs(got[:nc] - sigma[:nc]) <= SIGMA_TOL), (name, b, h)
                 assert np.all(np.isneginf(got[nc:])), (name, b, h)
                 if s > 0:
                     check_selection(sel[b, h, :s].cpu().numpy(), sigma, nc, s)
-            ref = M.branch_attention(qg, Kg, f64(v[b, h]), T, 64, w, sel_e[b, h].cpu().numpy(), cfg.scale)
+            ref = M.branch_attention(qg, Kg, f64(v[b, h]), T, L, w, sel_e[b, h].cpu().numpy(), cfg.scale)
             check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16")
             check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16")
 
@@ -220,21 +227,22 @@ def test_random_paged_cache_is_bitwise_contiguous(seed):
     c = _draw(7000 + seed)
     G, d, Hkv, B, tmax, s, w = c["G"], c["d"], c["Hkv"], c["B"], c["tmax"], c["s"], c["w"]
     say(f"random paged config {seed}: {c}")
-    prob = synth.make_problem("c2", seed=8000 + seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"])
+    L = c["L"]
+    prob = synth.make_problem("c2", seed=8000 + seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"], L=L)
     cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
                       rank=c["r"], budget=s, window=w, kv_dtype=c["kv"], mean_dtype=c["md"],
-                      factor_dtype=c["fd"], skew=c["skew"], value_mean=c["vmean"])
+                      factor_dtype=c["fd"], skew=c["skew"], value_mean=c["vmean"], block_size=L)
     q, k, v = prob["q"].to(DEV), prob["k"].to(DEV), prob["v"].to(DEV)
-    nbm = tmax // 64
+    nbm = tmax // L
     pages = B * nbm + 3
     perm = torch.randperm(pages, generator=torch.Generator().manual_seed(9000 + seed))[:B * nbm]
     table = perm.view(B, nbm).to(torch.int32)
-    kp = torch.zeros((pages, Hkv, 64, d), dtype=k.dtype, device=DEV)
+    kp = torch.zeros((pages, Hkv, L, d), dtype=k.dtype, device=DEV)
     vp = torch.zeros_like(kp)
     for b in range(B):
         for j in range(nbm):
-            kp[table[b, j]] = k[b, :, j * 64:(j + 1) * 64]
-            vp[table[b, j]] = v[b, :, j * 64:(j + 1) * 64]
+            kp[table[b, j]] = k[b, :, j * L:(j + 1) * L]
+            vp[table[b, j]] = v[b, :, j * L:(j + 1) * L]
     tab = table.to(DEV)
     seq_d = torch.from_numpy(c["seq"]).to(DEV)
 
@@ -245,7 +253,7 @@ def test_random_paged_cache_is_bitwise_contiguous(seed):
         rec = cobs.new_summaries(cfg, DEV)
         cobs.cobs_build_block_stats(cfg, kk, vv, seq_d, rec, **kw)
         res["rec"] = rec
-        sel = synth.make_selection(B, Hkv, c["seq"], 64, w, max(s, 1), seed=seed, fill="random")[:, :, :s]
+        sel = synth.make_selection(B, Hkv, c["seq"], L, w, max(s, 1), seed=seed, fill="random")[:, :, :s]
         sel = sel.contiguous().to(DEV)
         res["out"] = torch.empty((B, G * Hkv, d), dtype=torch.float32, device=DEV)
         res["lse"] = torch.empty((B, G * Hkv), dtype=torch.float32, device=DEV)

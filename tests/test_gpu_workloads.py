@@ -45,7 +45,8 @@ ID_DIFF_BOUND = {"f32": 0.01, "bf16": 0.01, "e2m1": 0.02}
 
 
 def _oracle_stats(K, T, cfg):
-    return M.stored_statistics(*M.block_statistics(K, T, 64, cfg.rank), cfg.mean_dtype, cfg.factor_dtype)
+    return M.stored_statistics(*M.block_statistics(K, T, cfg.block_size, cfg.rank), cfg.mean_dtype,
+                               cfg.factor_dtype)
 
 
 def _id_diff(a, b):
@@ -106,7 +107,8 @@ def _run_case(name, seed, units=None, **over):
     same = shared_exact = 0
     ndiff = ntot = 0
     T = int(c["T"])
-    nb = -(-T // 64)
+    L = cfg.block_size
+    nb = -(-T // L)
     for (b, h) in units:
         K, V = f64(k[b, h, :T]), f64(v[b, h, :T])
         qu = f64(q[b, h * G:(h + 1) * G])
@@ -116,7 +118,7 @@ def _run_case(name, seed, units=None, **over):
         shared_exact += _shared_bytes_check(cfg, rec_u, qu, K, V, T, sel[b, h].cpu().numpy(),
                                             out[b, sl].cpu().numpy(), lse[b, sl].cpu().numpy(),
                                             scores[b, h].cpu().numpy())
-        res = M.decode_unit(qu, K, V, T, 64, cfg.rank, cfg.budget, cfg.window, cfg.scale,
+        res = M.decode_unit(qu, K, V, T, L, cfg.rank, cfg.budget, cfg.window, cfg.scale,
                             cfg.mean_dtype, cfg.factor_dtype, stats=_oracle_stats(K, T, cfg))
         ora[(b, h)] = res
         nc = res["nc"]
@@ -157,9 +159,13 @@ def test_c1_tiny_single_head(golden_dir):
     ("c3", dict(B=2, Hq=8, Hkv=2, T=4096, s=16)),
     ("c4", dict(B=1, Hq=16, Hkv=2, T=8192, s=20)),
     ("c5", dict(B=2, Hq=8, Hkv=2, T=3000, s=16, steps=0)),
+    # the paper's block length (Sec. 7.1: L = 32) and L = 128
+    ("c2", dict(B=1, Hq=8, Hkv=2, T=4096, s=32, L=32)),
+    ("c3", dict(B=2, Hq=8, Hkv=2, T=4096, s=10, L=128)),
+    ("c5", dict(B=2, Hq=8, Hkv=2, T=3000, s=24, steps=0, L=32)),
 ])
 def test_reduced_workloads(name, over):
-    _run_case(name, 2000 + len(name) + over["T"], **over)
+    _run_case(name, 2000 + len(name) + over["T"] + over.get("L", 64), **over)
 
 
 def test_c2_full_size_every_unit():
