@@ -101,25 +101,65 @@ def scaled_eigenvectors_gram(Kb, r):
     return canonical_sign(xi)
 
 
-def block_statistics(K, T, L, r):
+def query_subspace(Q, s):
+    """U_Q of Sec. 5.4: the top-s eigenvectors of the query second moment
+    E[q q^T], estimated from a sample Q [N, d] as (1/N) sum q q^T; [d, s],
+    orthonormal columns, eigenvalues descending."""
+    Q = np.asarray(Q, dtype=np.float64)
+    M2 = Q.T @ Q / Q.shape[0]
+    lam, U = np.linalg.eigh(M2)
+    return U[:, ::-1][:, :int(s)]
+
+
+def energy_rank(Q, frac=0.9):
+    """Smallest k whose top-k eigenvalues of the query second moment hold at
+    least `frac` of its trace (the rank capturing 90 % of the query spectral
+    energy, Sec. 5.4 and Sec. 7.6.2)."""
+    Q = np.asarray(Q, dtype=np.float64)
+    lam = np.sort(np.linalg.eigvalsh(Q.T @ Q / Q.shape[0]))[::-1]
+    cum = np.cumsum(np.clip(lam, 0.0, None))
+    return int(np.searchsorted(cum, frac * cum[-1] * (1 - 1e-12)) + 1)
+
+
+def subspace_covariance(Sigma, U):
+    """B_b = U_Q^T Sigma_b U_Q, eq. (subspace)."""
+    U = np.asarray(U, dtype=np.float64)
+    return U.T @ np.asarray(Sigma, dtype=np.float64) @ U
+
+
+def subspace_factors(Kb, U, r):
+    """Top-r scaled eigenvectors xi^ss of B_b (eq. subspace-lowrank), [r, s]:
+    the Gram trick of Sec. 5.6 on the projected centred keys Kc U_Q (the
+    paper's route), with eigenvalues of the n x n Gram matrix; sign fixed as
+    for the full-space factors."""
+    Kb = np.asarray(Kb, dtype=np.float64)
+    return scaled_eigenvectors_gram(Kb @ np.asarray(U, dtype=np.float64), r)
+
+
+def block_statistics(K, T, L, r, U=None):
     """Counts, means and factors of every block of one KV head (Sec. 5.3).
 
-    K [>=T, d].  Returns counts [NB], means [NB, d], factors [NB, r, d].
-    A partial block stores zero factors.
+    K [>=T, d].  Returns counts [NB], means [NB, d], factors [NB, r, d], or
+    with a query subspace U [d, s] (Sec. 5.4) the subspace factors [NB, r, s]
+    of B_b = U^T Sigma_b U.  A partial block stores zero factors.
     """
     K = np.asarray(K, dtype=np.float64)
     d = K.shape[1]
+    fd = d if U is None else np.asarray(U).shape[1]
     nb = num_blocks(T, L)
     counts = np.zeros(nb, dtype=np.int64)
     means = np.zeros((nb, d))
-    factors = np.zeros((nb, r, d))
+    factors = np.zeros((nb, r, fd))
     for b in range(nb):
         n = block_count(T, L, b)
         Kb = K[b * L:b * L + n]
         counts[b] = n
         means[b] = block_mean(Kb)
         if n == L and r > 0:
-            factors[b] = scaled_eigenvectors(block_covariance(Kb), r)
+            if U is None:
+                factors[b] = scaled_eigenvectors(block_covariance(Kb), r)
+            else:
+                factors[b] = scaled_eigenvectors(subspace_covariance(block_covariance(Kb), U), r)
     return counts, means, factors
 
 
@@ -168,27 +208,30 @@ def stored_statistics(counts, means, factors, mean_dtype, factor_dtype, skews=No
     """Round-trip through the descriptor storage format (bf16 / fp32 / E2M1).
     With skew coefficients or value means, returns them too (5-tuple)."""
     d = means.shape[1]
-    r = factors.shape[1]
+    r, fdim = factors.shape[1], factors.shape[2]
     buf = rec.encode(counts, means, factors, mean_dtype, factor_dtype, skews, vmeans)
-    return rec.decode(buf, d, r, mean_dtype, factor_dtype, skews is not None, vmeans is not None)
+    return rec.decode(buf, d, r, mean_dtype, factor_dtype, skews is not None, vmeans is not None, fdim)
 
 
 # ---------------------------------------------------------------- scoring --
 
-def log_mass_estimate(q, counts, means, factors, c, skews=None):
+def log_mass_estimate(q, counts, means, factors, c, skews=None, U=None):
     """Second-order log-mass estimate of every block for every query head.
 
     eq. (trunc) with q <- c q and L <- n_b, curvature through eq. (gram):
         l_b^g = ln n_b + c q_g . kbar_b + (c^2 / 2) sum_i (xi_{b,i} . q_g)^2
     With skew coefficients gamma (Sec. 7.7, see skew_coefficients) the
     diagonal third-order term (c^3 / 6) sum_i gamma_{b,i} (xi_{b,i} . q_g)^3
-    is added.
-    q [G, d], counts [NB], means [NB, d], factors [NB, r, d]  ->  [NB, G].
+    is added.  With a query subspace U [d, s] the factors are subspace factors
+    [NB, r, s] and meet the projected query U^T q (eq. subspace-quad, eq. gram);
+    the mean term keeps the full q.
+    q [G, d], counts [NB], means [NB, d], factors [NB, r, d or s]  ->  [NB, G].
     """
     q = np.asarray(q, dtype=np.float64)
     lin = means @ q.T                                   # [NB, G]
+    qf = q if U is None else q @ np.asarray(U, dtype=np.float64)
     if factors.shape[1] > 0:
-        proj = np.einsum("brd,gd->bgr", factors, q)     # [NB, G, r]
+        proj = np.einsum("brd,gd->bgr", factors, qf)    # [NB, G, r]
         quad = (proj ** 2).sum(axis=2)
     else:
         proj = None

@@ -16,8 +16,9 @@ block, all offsets in bytes, little-endian, every record 16-byte aligned:
   S              float32  skew coefficient of factor i, i < r (skew records
                           only), zero-padded to a multiple of 16 bytes
   M              mean, d elements of the mean dtype
-  F = M + |mean| factors, r vectors of d elements of the factor dtype,
-                          vector i at F + i * |vector|
+  F = M + |mean| factors, r vectors of d elements of the factor dtype (of s
+                          elements for subspace factors, Sec. 5.4), vector i
+                          at F + i * |vector|
   V = F + r|vec| value mean, d elements of the mean dtype (value-mean
                           records only)
   total          rounded up to a multiple of 16 bytes
@@ -42,22 +43,23 @@ def _round16(x):
     return (x + 15) // 16 * 16
 
 
-def layout(d, r, mean_dtype, factor_dtype, skew=False, value_mean=False):
-    """Offsets and total size of one record."""
+def layout(d, r, mean_dtype, factor_dtype, skew=False, value_mean=False, fdim=None):
+    """Offsets and total size of one record (factor vectors of fdim elements,
+    d unless given)."""
     assert mean_dtype in DTYPES and factor_dtype in DTYPES
     fscale_bytes = _round16(4 * r) if factor_dtype == "e2m1" else 0
     skew_off = 16 + fscale_bytes
     mean_off = skew_off + (_round16(4 * r) if skew else 0)
     mean_bytes = _vec_bytes(d, mean_dtype)
     fac_off = mean_off + mean_bytes
-    vec_bytes = _vec_bytes(d, factor_dtype)
+    vec_bytes = _vec_bytes(d if fdim is None else fdim, factor_dtype)
     vmean_off = fac_off + r * vec_bytes
     total = _round16(vmean_off + (mean_bytes if value_mean else 0))
     return dict(mean_off=mean_off, mean_bytes=mean_bytes, fac_off=fac_off,
                 vec_bytes=vec_bytes, skew_off=skew_off, vmean_off=vmean_off, total=total)
 
 
-def algorithmic_bytes(d, r, mean_dtype, factor_dtype, skew=False):
+def algorithmic_bytes(d, r, mean_dtype, factor_dtype, skew=False, fdim=None):
     """Bytes a scorer must read per block, without layout padding.
 
     int32 count, the mean (plus its fp32 scale if E2M1) and the r factors
@@ -65,7 +67,7 @@ def algorithmic_bytes(d, r, mean_dtype, factor_dtype, skew=False):
     skew term, one more fp32 scalar per factor.
     """
     b = 4 + _vec_bytes(d, mean_dtype) + (4 if mean_dtype == "e2m1" else 0)
-    b += r * _vec_bytes(d, factor_dtype) + (4 * r if factor_dtype == "e2m1" else 0)
+    b += r * _vec_bytes(d if fdim is None else fdim, factor_dtype) + (4 * r if factor_dtype == "e2m1" else 0)
     return b + (4 * r if skew else 0)
 
 
@@ -100,8 +102,8 @@ def encode(counts, means, factors, mean_dtype, factor_dtype, skews=None, vmeans=
     means = np.asarray(means, dtype=np.float64)
     factors = np.asarray(factors, dtype=np.float64)
     nb, d = means.shape
-    r = factors.shape[1]
-    lay = layout(d, r, mean_dtype, factor_dtype, skews is not None, vmeans is not None)
+    r, fdim = factors.shape[1], factors.shape[2]
+    lay = layout(d, r, mean_dtype, factor_dtype, skews is not None, vmeans is not None, fdim)
     out = np.zeros((nb, lay["total"]), dtype=np.uint8)
     out[:, 0:4] = counts.astype(np.int32).view(np.uint8).reshape(nb, 4)
     mraw, mscale = _encode_vectors(means, mean_dtype)
@@ -124,12 +126,13 @@ def encode(counts, means, factors, mean_dtype, factor_dtype, skews=None, vmeans=
     return out
 
 
-def decode(buf, d, r, mean_dtype, factor_dtype, skew=False, value_mean=False):
+def decode(buf, d, r, mean_dtype, factor_dtype, skew=False, value_mean=False, fdim=None):
     """Decode records uint8 [NB, total] -> (counts int64 [NB], means [NB, d], factors [NB, r, d]),
     followed by the skew coefficients [NB, r] and the value means [NB, d] (None
     where absent) when either optional part is asked for."""
     buf = np.ascontiguousarray(np.asarray(buf, dtype=np.uint8))
-    lay = layout(d, r, mean_dtype, factor_dtype, skew, value_mean)
+    lay = layout(d, r, mean_dtype, factor_dtype, skew, value_mean, fdim)
+    fd = d if fdim is None else fdim
     assert buf.shape[-1] == lay["total"], (buf.shape, lay)
     nb = buf.shape[0]
     counts = np.ascontiguousarray(buf[:, 0:4]).view(np.int32).reshape(nb).astype(np.int64)
@@ -137,13 +140,13 @@ def decode(buf, d, r, mean_dtype, factor_dtype, skew=False, value_mean=False):
     mraw = buf[:, lay["mean_off"]:lay["mean_off"] + lay["mean_bytes"]]
     means = _decode_vectors(mraw, d, mean_dtype, mscale)
     if r == 0:
-        factors = np.zeros((nb, 0, d))
+        factors = np.zeros((nb, 0, fd))
     else:
         fraw = buf[:, lay["fac_off"]:lay["fac_off"] + r * lay["vec_bytes"]].reshape(nb, r, lay["vec_bytes"])
         fscale = None
         if factor_dtype == "e2m1":
             fscale = np.ascontiguousarray(buf[:, 16:16 + 4 * r]).view(np.float32).reshape(nb, r)
-        factors = _decode_vectors(fraw, d, factor_dtype, fscale)
+        factors = _decode_vectors(fraw, fd, factor_dtype, fscale)
     if not (skew or value_mean):
         return counts, means, factors
     skews = vmeans = None

@@ -10,7 +10,7 @@
 // every a, in the layout in which the matrix cores return them, which is the A
 // operand of Gamma W with the contraction index of each step permuted (no LDS
 // copy of Gamma).  Its top-r eigenvectors come from a fixed-count block power
-// iteration with P = 16 (r <= 4) or 32 columns, re-orthonormalised by
+// iteration with P = 16 (r <= 4, L <= 64) or 32 columns, re-orthonormalised by
 // Cholesky-QR after one product in the first two steps and after two
 // (Gamma^2) in the ten that follow, then a Rayleigh-Ritz step whose P x P
 // eigenproblem is solved by parallel cyclic Jacobi within one wave.  The scaled

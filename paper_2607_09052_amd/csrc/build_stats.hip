@@ -69,7 +69,9 @@ static hipError_t launch_build_dp(const BuildParams& p, dim3 grid, hipStream_t s
 }
 
 hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st) {
-  const bool big = p.r > 4;             // 16 columns converge for r <= 4, 32 beyond
+  // 16 columns converge for r <= 4 at L <= 64; 32 beyond r = 4, and at L = 128,
+  // where the 128 x 128 Gram matrix of unstructured keys has a flat top
+  const bool big = p.r > 4 || p.kv.lsh == 7;
   if (d == 128) return big ? launch_build_dp<128, 32>(p, grid, st) : launch_build_dp<128, 16>(p, grid, st);
   return big ? launch_build_dp<64, 32>(p, grid, st) : launch_build_dp<64, 16>(p, grid, st);
 }

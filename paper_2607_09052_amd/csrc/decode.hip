@@ -792,7 +792,9 @@ int decode_items(int s, int w, int nbmax, bool f32, int L) {
 }
 
 int decode_max_wg(int s, int w, int nbmax, bool f32, int L) {
-  return std::max(1, std::min(kMaxDecodeWg, (decode_items(s, w, nbmax, f32, L) + 3) / 4));
+  // the two-branch form needs a partial for each branch, whatever the item count
+  const int least = (s > 0 && w > 0) ? 2 : 1;
+  return std::max(least, std::min(kMaxDecodeWg, (decode_items(s, w, nbmax, f32, L) + 3) / 4));
 }
 
 // A unit's work items split over nwg <= kMaxDecodeWg workgroups (one partial
@@ -818,8 +820,12 @@ hipError_t launch_decode(DecodeParams p, int d, int g, bool f32, int batch, int 
     // two outputs: no workgroup mixes the branches; the split stays within
     // the workspace's partial count
     const int is = host_items_per_block(false, L) * p.s, iw = items - is, cap = decode_max_wg(p.s, p.w, nbmax, false, L);
+    // widen the share until both branches fit; at sp = max(is, iw) each takes
+    // one workgroup, and cap >= 2 whenever both are non-empty
     int sp = (int)spw;
-    while ((is + sp - 1) / sp + (iw + sp - 1) / sp > cap) ++sp;
+    const int sp_max = std::max(1, std::max(is, iw));
+    while ((is + sp - 1) / sp + (iw + sp - 1) / sp > cap && sp < sp_max) ++sp;
+    if ((is + sp - 1) / sp + (iw + sp - 1) / sp > cap) return hipErrorInvalidValue;
     p.spw = sp;
     p.nwg_s = (is + sp - 1) / sp;
     nwg = p.nwg = std::max(1, p.nwg_s + (iw + sp - 1) / sp);

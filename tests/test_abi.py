@@ -190,3 +190,14 @@ def test_noalloc_step_rejects_problems_beyond_its_scratch():
                                         fake, None, None) == 3
     assert lib.cobs_decode_step_noalloc(ctypes.byref(_cfg().c_struct()), None, ctypes.byref(kv), fake, fake,
                                         None, fake, None, None) == 1
+
+
+@pytest.mark.parametrize("L,s,w", [(32, 1, 64), (32, 1, 1), (64, 1, 1), (128, 1, 1), (32, 0, 64), (32, 5, 0)])
+def test_decode_workspace_holds_a_partial_per_branch(L, s, w):
+    """The two-branch decode needs one partial per non-empty branch: the decode
+    workspace holds at least two per unit whenever both budget and window are
+    positive, at every block length."""
+    cfg = _cfg(batch=1, num_q_heads=8, num_kv_heads=1, max_seq_len=2048, block_size=L, budget=s, window=w)
+    G, d = 8, cfg.head_dim
+    least = 2 if (s > 0 and w > 0) else 1
+    assert cobs.workspace_bytes(cfg, cobs.OP_DECODE) >= least * G * (d + 2) * 4 + 4

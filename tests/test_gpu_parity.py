@@ -316,15 +316,15 @@ def test_sparse_decode_matches_oracle(d, G, kv, s, w):
 
 @pytest.mark.parametrize("d,G,s,w", [(128, 4, 6, 256), (128, 8, 10, 100), (64, 2, 0, 128), (128, 1, 5, 0),
                                       (128, 16, 7, 300)])
-def test_sparse_decode_branches_match_oracle(d, G, s, w):
+def test_sparse_decode_branches_match_oracle(d, G, s, w, L=64, fill="random"):
     """Selection and window branches each against the oracle's attention on its
     own token set; merged by log-sum-exp they give cobs_sparse_decode's output."""
     seq = np.array([2048, 1000, 77, 700], np.int32)
     Hkv, Tmax = 2, 2048
     prob = _decode_problem(d, G, "bf16", seq, Hkv, Tmax, seed=d + 5 * G + s)
     cfg = _cfg(batch=len(seq), num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=Tmax,
-               budget=s, window=w)
-    sel = synth.make_selection(len(seq), Hkv, seq, 64, w, max(s, 1), seed=13 + s, fill="random")[:, :, :s]
+               budget=s, window=w, block_size=L)
+    sel = synth.make_selection(len(seq), Hkv, seq, L, w, max(s, 1), seed=13 + s, fill=fill)[:, :, :s]
     q, k, v = prob["q"], prob["k"], prob["v"]
     shp = (len(seq), G * Hkv, d)
     o_s, o_w, o_u = (torch.empty(shp, dtype=torch.float32, device=DEV) for _ in range(3))
@@ -341,7 +341,7 @@ def test_sparse_decode_branches_match_oracle(d, G, s, w):
     for b in range(len(seq)):
         for h in range(Hkv):
             gs = slice(h * G, (h + 1) * G)
-            ref = M.branch_attention(q[b, gs].double().numpy(), f64(k[b, h]), f64(v[b, h]), int(seq[b]), 64, w,
+            ref = M.branch_attention(q[b, gs].double().numpy(), f64(k[b, h]), f64(v[b, h]), int(seq[b]), L, w,
                                      sel[b, h].numpy(), cfg.scale)
             check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16")
             check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16")
@@ -356,6 +356,13 @@ def test_sparse_decode_branches_match_oracle(d, G, s, w):
     lu = l_u.cpu().numpy()
     fin = np.isfinite(lu)
     np.testing.assert_allclose((m + np.log(den))[fin], lu[fin], rtol=0, atol=2e-5)
+
+
+@pytest.mark.parametrize("L,s,w", [(32, 1, 64), (32, 1, 1), (32, 3, 40), (128, 1, 64)])
+def test_sparse_decode_branches_small_budgets_at_other_block_lengths(L, s, w):
+    """Few work items (one selected block, a window of one or two blocks) at
+    L = 32 and 128: each branch still gets its own workgroup and partial."""
+    test_sparse_decode_branches_match_oracle(128, 8, s, w, L, fill="full")
 
 
 def test_sparse_decode_one_workgroup_per_unit():

@@ -575,3 +575,103 @@ def test_records_with_skew_and_value_means_round_trip():
     lay, lay0 = R.layout(d, r, "f32", "f32", True, True), R.layout(d, r, "f32", "f32")
     np.testing.assert_array_equal(buf[:, lay["mean_off"]:lay["vmean_off"]], plain[:, lay0["mean_off"]:lay0["total"]])
     assert lay["total"] == lay0["total"] + 16 + 4 * d
+
+
+# ------------------------------------------------- subspace COBS (Sec. 5.4) --
+
+def _queries_with_spectrum(lam, seed):
+    """A query sample whose second moment (1/N) Q^T Q is exactly V diag(lam) V^T."""
+    d = len(lam)
+    rng = np.random.default_rng(seed)
+    V, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    Z, _ = np.linalg.qr(rng.standard_normal((d, d)))       # orthonormal rows: Z^T Z = I
+    Q = math.sqrt(d) * Z @ np.diag(np.sqrt(lam)) @ V.T
+    return Q, V
+
+
+def test_query_subspace_and_energy_rank_on_a_known_spectrum():
+    """U_Q spans the top-s eigenvectors of E[q q^T]; the rank capturing 90 % of
+    the spectral energy is where the cumulative eigenvalue sum first reaches it."""
+    lam = np.concatenate([np.full(10, 8.0), np.full(54, 0.1)])   # top 10 hold 80/85.4 = 93.7 %
+    Q, V = _queries_with_spectrum(lam, 3)
+    np.testing.assert_allclose(Q.T @ Q / len(Q), V @ np.diag(lam) @ V.T, atol=1e-12)
+    U = M.query_subspace(Q, 10)
+    np.testing.assert_allclose(U.T @ U, np.eye(10), atol=1e-12)
+    np.testing.assert_allclose(U @ U.T, V[:, :10] @ V[:, :10].T, atol=1e-10)
+    assert M.energy_rank(Q, 0.9) == 10
+    lam2 = np.linspace(2.0, 0.02, 64)
+    Q2, _ = _queries_with_spectrum(lam2, 4)
+    cum = np.cumsum(lam2) / lam2.sum()
+    assert M.energy_rank(Q2, 0.9) == int(np.argmax(cum >= 0.9)) + 1
+
+
+def test_subspace_dimension_rule_matches_the_figure(golden_dir):
+    """Figure "subspace-perlayer": each layer's full bar is 1.25 times the rank
+    capturing 90 % of the query energy (averaged over heads), to the unit."""
+    with open(os.path.join(golden_dir, "subspace_dims.txt")) as f:
+        rows = [l.split() for l in f if l.strip() and not l.startswith("#")]
+    for _, dark, extra in rows:
+        dark, full = int(dark), int(dark) + int(extra)
+        assert abs(full - 1.25 * dark) <= 1.0, (dark, full)
+
+
+def test_subspace_factors_with_the_whole_space_are_the_full_factors():
+    """U_Q = I (s = d): B_b = Sigma_b, the subspace factors are the full-space
+    factors and the scores agree."""
+    Kb = synth.make_keys_block(64, 32, "spiked", 61).astype(np.float64)
+    I = np.eye(32)
+    c1, m1, f1 = M.block_statistics(Kb, 64, 64, 4)
+    c2, m2, f2 = M.block_statistics(Kb, 64, 64, 4, U=I)
+    np.testing.assert_allclose(f2, f1, atol=1e-10)
+    q = np.random.default_rng(62).standard_normal((3, 32))
+    np.testing.assert_allclose(M.log_mass_estimate(q, c2, m2, f2, 0.3, U=I),
+                               M.log_mass_estimate(q, c1, m1, f1, 0.3), atol=1e-12)
+
+
+def test_subspace_quadratic_form_is_exact_inside_the_subspace():
+    """eq. (subspace-quad): with every direction of B_b kept (r = s), the
+    subspace score's curvature equals q^T Sigma_b q for q in the span of U_Q,
+    and only the in-subspace part of q otherwise (Sigma from the library)."""
+    rng = np.random.default_rng(63)
+    d, s = 48, 12
+    Kb = synth.make_keys_block(64, d, "gauss", 64).astype(np.float64)
+    U, _ = np.linalg.qr(rng.standard_normal((d, s)))
+    Sigma = np.cov(Kb.T, bias=True)
+    _, _, f = M.block_statistics(Kb, 64, 64, s, U=U)
+    q_in = (U @ rng.standard_normal((s, 2))).T
+    quad = ((f[0] @ (q_in @ U).T) ** 2).sum(axis=0)
+    np.testing.assert_allclose(quad, np.einsum("gd,de,ge->g", q_in, Sigma, q_in), rtol=1e-10)
+    q = rng.standard_normal((2, d))
+    quad = ((f[0] @ (q @ U).T) ** 2).sum(axis=0)
+    Pq = q @ U @ U.T
+    np.testing.assert_allclose(quad, np.einsum("gd,de,ge->g", Pq, Sigma, Pq), rtol=1e-10)
+    assert not np.allclose(quad, np.einsum("gd,de,ge->g", q, Sigma, q), rtol=1e-3)
+
+
+def test_subspace_gram_trick_equals_eigh_of_the_projected_covariance():
+    """Sec. 5.6 applied to Kc U_Q: the same factors as eigh(U^T Sigma U), with
+    the rank-r truncation of eq. (subspace-lowrank) the best one (Eckart-Young)."""
+    rng = np.random.default_rng(65)
+    Kb = synth.make_keys_block(64, 128, "spiked", 66).astype(np.float64)
+    U, _ = np.linalg.qr(rng.standard_normal((128, 40)))
+    a = M.subspace_factors(Kb, U, 4)
+    _, _, b = M.block_statistics(Kb, 64, 64, 4, U=U)
+    np.testing.assert_allclose(a, b[0], atol=1e-10)
+    B = U.T @ np.cov(Kb.T, bias=True) @ U
+    lam, W = np.linalg.eigh(B)
+    best = (W[:, ::-1][:, :4] * lam[::-1][:4]) @ W[:, ::-1][:, :4].T
+    np.testing.assert_allclose(a.T @ a, best, atol=1e-10)
+
+
+def test_subspace_records_store_s_element_factors():
+    """Record layout with factors of s elements (Table "quant": subspace r = 4,
+    s = 64 takes 512 B in bf16 and 144 B in E2M1, without the mean)."""
+    assert R.layout(128, 4, "bf16", "bf16", fdim=64)["vec_bytes"] * 4 == 512
+    lay = R.layout(128, 4, "bf16", "e2m1", fdim=64)
+    assert lay["vec_bytes"] * 4 + 4 * 4 == 144
+    assert R.algorithmic_bytes(128, 4, "bf16", "e2m1", fdim=64) == 4 + 256 + 144
+    rng = np.random.default_rng(67)
+    f = rng.standard_normal((3, 4, 64))
+    buf = R.encode(np.array([64, 64, 5]), rng.standard_normal((3, 128)), f, "f32", "f32")
+    _, _, f2 = R.decode(buf, 128, 4, "f32", "f32", fdim=64)
+    np.testing.assert_array_equal(f2, f.astype(np.float32).astype(np.float64))
