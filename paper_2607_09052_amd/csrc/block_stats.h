@@ -13,7 +13,7 @@
 // iteration with P = 16 (r <= 4, L <= 64) or 32 columns, re-orthonormalised by
 // Cholesky-QR after one product in the first two steps and after two
 // (Gamma^2) in the ten that follow, then a Rayleigh-Ritz step whose P x P
-// eigenproblem is solved by parallel cyclic Jacobi within one wave.  The scaled
+// eigenproblem is solved by parallel cyclic Jacobi.  The scaled
 // eigenvectors are xi_i = Kc^T w_i / sqrt(n) (their squared norms are the
 // eigenvalues of the 1/n covariance), with the sign that makes the
 // largest-magnitude entry positive.  A partial block (n < LB) stores its count,
@@ -31,6 +31,9 @@ namespace cobs {
 constexpr int kBuildThreads = 256;
 constexpr int kPowerIters = 12;        // orthonormalisations
 constexpr int kSinglePowerIters = 2;   // the first ones after one product, the others after two
+// Cyclic Jacobi sweeps on the P x P Rayleigh-Ritz matrix: at most four; a
+// sweep whose rotations all had |h_pq| <= 1e-6 sqrt(h_pp h_qq), or <= 2e-8
+// (the matrix has eigenvalues in [0, 1]), ends the iteration.
 constexpr int kJacobiSweeps = 4;
 
 // What the statistics of a block read and write.
@@ -98,8 +101,8 @@ struct StatsLds {
   static constexpr size_t hm = al(lm + 4 * P * (P + 1));   // [2][P(P+1)]
   static constexpr size_t vm = al(hm + 8 * P * (P + 1));   // [2][P(P+1)]
   static constexpr size_t xi = al(vm + 8 * P * (P + 1));   // [XR][D] factors
-  static constexpr size_t jac = al(xi + 4 * XR * D);       // Jacobi rotations: partner, c, s
-  static constexpr size_t order = al(jac + 12 * P);
+  static constexpr size_t jac = al(xi + 4 * XR * D);       // Jacobi rotations per wave: partner, c, s
+  static constexpr size_t order = al(jac + 4 * 12 * P);
   static constexpr size_t ritz = al(order + 4 * kMaxRank);
   static constexpr size_t skw = al(ritz + 4 * kMaxRank);   // skew coefficients
   static constexpr size_t diag = al(skw + 4 * kMaxRank);   // the waves' parts of trace(Gamma)
@@ -131,9 +134,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   float (*Hm)[P * (P + 1)] = reinterpret_cast<float (*)[P * (P + 1)]>(pool + Lay::hm);
   float (*Vm)[P * (P + 1)] = reinterpret_cast<float (*)[P * (P + 1)]>(pool + Lay::vm);
   float* Xi = reinterpret_cast<float*>(pool + Lay::xi);
-  int* partner = reinterpret_cast<int*>(pool + Lay::jac);
-  float* cself = reinterpret_cast<float*>(pool + Lay::jac + 4 * P);
-  float* cpart = reinterpret_cast<float*>(pool + Lay::jac + 8 * P);
+  int* partner = reinterpret_cast<int*>(pool + Lay::jac);        // [4 waves][partner, c, s][P]
   int* order = reinterpret_cast<int*>(pool + Lay::order);
   float* ritzval = reinterpret_cast<float*>(pool + Lay::ritz);
   float* skw = reinterpret_cast<float*>(pool + Lay::skw);
@@ -393,15 +394,23 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       Vm[0][a * (P + 1) + c] = (a == c) ? 1.0f : 0.0f;
     }
     __syncthreads();
-    // ---- eigenpairs of H by parallel cyclic Jacobi in wave 0 (round-robin
-    // pairing, index 0 fixed): per round, lanes < P/2 form one rotation each,
-    // then every lane updates its elements of H and V; LDS ordered by wave
-    // fences, no workgroup barriers
-    if (wave == 0) {
-      int cw = 0;
+    // ---- eigenpairs of H by parallel cyclic Jacobi (round-robin pairing,
+    // index 0 fixed).  Each wave forms the round's P/2 rotations itself (lanes
+    // < P/2, into its own LDS slot, ordered by wave fences), then the threads
+    // update their elements of H and V; one workgroup barrier per round.
+    // Every wave forms the same rotations from the same H, so the waves agree
+    // on when the sweeps end.
+    static_assert(NT == kBuildThreads, "one rotation slot per wave of the work layout");
+    int cw = 0;
+    {
+      int* partner_w = partner + (tid >> 6) * 3 * P;
+      float* cself_w = reinterpret_cast<float*>(partner_w + P);
+      float* cpart_w = reinterpret_cast<float*>(partner_w + 2 * P);
       for (int sweep = 0; sweep < kJacobiSweeps; ++sweep) {
+        bool moved = false;
         for (int rnd = 0; rnd < P - 1; ++rnd) {
-          if (lane < P / 2) {
+          bool big = false;
+          if (lw && lane < P / 2) {
             const int m1 = lane, m2 = P - 1 - lane;
             const int x = (m1 == 0) ? 0 : 1 + (m1 - 1 + rnd) % (P - 1);
             const int y = 1 + (m2 - 1 + rnd) % (P - 1);
@@ -409,36 +418,38 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
             const float* H = Hm[cw];
             const float app = H[pp * (P + 1) + pp], aqq = H[qq * (P + 1) + qq], apq = H[pp * (P + 1) + qq];
             float c = 1.0f, s = 0.0f;
+            big = fabsf(apq) > 1e-6f * sqrtf(fmaxf(app, 0.0f) * fmaxf(aqq, 0.0f)) && fabsf(apq) > 2e-8f;
             if (apq != 0.0f) {
               const float th = (aqq - app) / (2.0f * apq);
               const float t = (th >= 0.0f ? 1.0f : -1.0f) / (fabsf(th) + sqrtf(th * th + 1.0f));
               c = 1.0f / sqrtf(t * t + 1.0f);
               s = t * c;
             }
-            partner[pp] = qq; partner[qq] = pp;
-            cself[pp] = c; cpart[pp] = -s;
-            cself[qq] = c; cpart[qq] = s;
+            partner_w[pp] = qq; partner_w[qq] = pp;
+            cself_w[pp] = c; cpart_w[pp] = -s;
+            cself_w[qq] = c; cpart_w[qq] = s;
           }
+          moved = moved || __ballot(big) != 0;
           wave_lds_sync();
           const float* H = Hm[cw];
           const float* V = Vm[cw];
           float* H2 = Hm[cw ^ 1];
           float* V2 = Vm[cw ^ 1];
-          for (int idx = lane; idx < P * P; idx += 64) {
+          for (int idx = tid; lw && idx < P * P; idx += kBuildThreads) {
             const int a = idx / P, c = idx % P;
-            const int pa = partner[a], pc = partner[c];
-            const float sa = cself[a], ta = cpart[a], sc = cself[c], tc = cpart[c];
+            const int pa = partner_w[a], pc = partner_w[c];
+            const float sa = cself_w[a], ta = cpart_w[a], sc = cself_w[c], tc = cpart_w[c];
             H2[a * (P + 1) + c] = sa * sc * H[a * (P + 1) + c] + sa * tc * H[a * (P + 1) + pc] +
                                   ta * sc * H[pa * (P + 1) + c] + ta * tc * H[pa * (P + 1) + pc];
             V2[a * (P + 1) + c] = V[a * (P + 1) + c] * sc + V[a * (P + 1) + pc] * tc;
           }
-          wave_lds_sync();
+          __syncthreads();
           cw ^= 1;
         }
+        if (!moved) break;
       }
     }
-    const int cur = (kJacobiSweeps * (P - 1)) % 2;   // the buffer the last round wrote
-    __syncthreads();
+    const int cur = cw;                  // the buffer the last round wrote
     // ---- top-r Ritz values, descending, ties to the lower index (rank by counting)
     if (tid < P) {
       const float ta = Hm[cur][tid * (P + 1) + tid];
