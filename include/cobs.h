@@ -94,7 +94,7 @@ typedef struct {
   int32_t num_kv_heads;  /* Hkv >= 1                                                */
   int32_t head_dim;      /* d in {64, 128}                                          */
   int32_t max_seq_len;   /* T_max, cache capacity in tokens, a multiple of block_size */
-  int32_t block_size;    /* L = 64 (the only size the kernels implement)            */
+  int32_t block_size;    /* L in {32, 64, 128}                                      */
   int32_t rank;          /* r in [0, 16]; 0 gives the first-order (mean-pool) score */
   int32_t budget;        /* s >= 0 selected blocks per (batch row, KV head)         */
   int32_t window;        /* w >= 0 most recent tokens always attended               */
@@ -103,6 +103,22 @@ typedef struct {
   cobs_dtype_t factor_dtype; /* stored scaled eigenvectors: F32, BF16 or E2M1         */
   float softmax_scale;   /* c; 0 selects 1/sqrt(d)                                  */
   int32_t options;       /* bitwise OR of cobs_option_t; 0 for the plain method    */
+  /* Subspace factors (Sec. 5.4): with subspace_dim = s' > 0 every block stores
+   * the top-r scaled eigenvectors xi^ss of B_b = U_Q^T Sigma_b U_Q (s'
+   * elements each) instead of those of Sigma_b, and the curvature term is
+   * sum_i (xi^ss_i . U_Q^T q)^2; the mean term keeps the full q.
+   * subspace_dim: 0 (full-space factors) or s' in {32, 64, 96} below d
+   *   (COBS_ERR_UNSUPPORTED otherwise); needs rank in [1, 4] (INVALID_ARG
+   *   for rank 0, UNSUPPORTED above 4).  cobs_select and the decode steps score
+   *   subspace factors with BF16 or E2M1 mean and factors only (UNSUPPORTED
+   *   for F32); cobs_build_block_stats also writes F32 ones.
+   * query_basis: device fp32 [Hkv, d, s'], 16-byte aligned, U_Q of each KV
+   *   head (orthonormal columns spanning its query heads' subspace, e.g. the
+   *   top-s' eigenvectors of their E[q q^T]); read by the build, select and
+   *   step calls, owned by the caller; NULL exactly when subspace_dim = 0
+   *   (COBS_ERR_INVALID_ARG otherwise).                                       */
+  int32_t subspace_dim;
+  const float* query_basis;
 } cobs_config_t;
 
 /* KV cache of one layer.
@@ -136,7 +152,8 @@ typedef struct {
  *   16       float   scale of factor i, i < r (E2M1 factors only), zero padded to 16 B
  *   S        float   skew coefficient gamma_i, i < r (COBS_OPT_SKEW only), zero padded to 16 B
  *   M        mean: d elements of mean_dtype
- *   M+|mean| factors: r vectors of d elements of factor_dtype, vector-major
+ *   M+|mean| factors: r vectors of d (subspace: s') elements of factor_dtype,
+ *            vector-major
  *   V        value mean: d elements of mean_dtype (COBS_OPT_VALUE_MEAN only)
  *   size     rounded up to 16 B
  * Element sizes: F32 4 B, BF16 2 B, E2M1 one nibble (element 2j in the low nibble
@@ -171,7 +188,9 @@ cobs_status_t cobs_build_block_stats(const cobs_config_t* cfg, const cobs_kv_t* 
  *   sel:       device int32 [B, Hkv, budget], written: the min(s, #candidates)
  *              best candidate blocks in ascending order, then -1.
  *   scores:    optional device fp32 [B, Hkv, T_max/L], written: sigma_b for
- *              candidates, -inf for every other index.                         */
+ *              candidates, -inf for every other index.
+ * With subspace factors a first small launch writes U_Q^T q of every query
+ * head into the workspace (its size includes that region).                     */
 cobs_status_t cobs_select(const cobs_config_t* cfg, const float* q, const void* summaries,
                           const int32_t* seq_lens, int32_t* sel, float* scores, void* ws,
                           size_t ws_bytes, void* stream);
@@ -229,8 +248,9 @@ cobs_status_t cobs_sparse_decode_branches(const cobs_config_t* cfg, const float*
  * caller has already written the new token's K/V at position T-1 and counted
  * it in seq_lens), then select and attend.  Equivalent to
  * cobs_build_block_stats on block (T-1)/L, cobs_select and cobs_sparse_decode.
- * With bf16 K/V and rank <= 4 it is two launches (the selector's workgroup
- * that scores the newest block recomputes its record first), else three.
+ * With bf16 K/V, rank <= 4, L = 64 and full-space factors it is two launches
+ * (the selector's workgroup that scores the newest block recomputes its record
+ * first), else three (four with subspace factors: the query projection).
  *   summaries: in/out.   sel: optional device int32 [B, Hkv, budget] output.    */
 cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
                                const int32_t* seq_lens, void* summaries, int32_t* sel,

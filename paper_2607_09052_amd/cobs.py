@@ -34,7 +34,8 @@ class _Config(ctypes.Structure):
                 ("rank", ctypes.c_int32), ("budget", ctypes.c_int32), ("window", ctypes.c_int32),
                 ("kv_dtype", ctypes.c_int), ("mean_dtype", ctypes.c_int),
                 ("factor_dtype", ctypes.c_int), ("softmax_scale", ctypes.c_float),
-                ("options", ctypes.c_int32)]
+                ("options", ctypes.c_int32), ("subspace_dim", ctypes.c_int32),
+                ("query_basis", ctypes.c_void_p)]
 
 
 class _KV(ctypes.Structure):
@@ -98,16 +99,26 @@ class Config:
     block_size: int = BLOCK
     skew: bool = False           # records carry the diagonal third-cumulant coefficients
     value_mean: bool = False     # records carry the block's mean value (compression branch)
+    subspace_dim: int = 0        # subspace factors of this many elements (Sec. 5.4); 0: full space
+    # U_Q of every KV head for subspace factors: fp32 [Hkv, d, subspace_dim] on the GPU
+    query_basis: object = dataclasses.field(default=None, compare=False, repr=False)
 
     @property
     def options(self):
         return (OPT_SKEW if self.skew else 0) | (OPT_VALUE_MEAN if self.value_mean else 0)
 
     def c_struct(self):
+        basis = None
+        if self.query_basis is not None:
+            want = (self.num_kv_heads, self.head_dim, self.subspace_dim)
+            _need("query_basis", self.query_basis, torch.float32, math.prod(want))
+            if tuple(self.query_basis.shape) != want:
+                raise CobsError(f"query_basis must have shape {list(want)}, got {list(self.query_basis.shape)}")
+            basis = self.query_basis.data_ptr()
         return _Config(self.batch, self.num_q_heads, self.num_kv_heads, self.head_dim,
                        self.max_seq_len, self.block_size, self.rank, self.budget, self.window,
                        DTYPES[self.kv_dtype], DTYPES[self.mean_dtype], DTYPES[self.factor_dtype],
-                       float(self.softmax_scale), self.options)
+                       float(self.softmax_scale), self.options, int(self.subspace_dim), basis)
 
     @property
     def num_blocks(self):
@@ -237,7 +248,8 @@ def cobs_build_block_stats(cfg, k, v, seq_lens, summaries, first_block=0, num_bl
     _need("seq_lens", seq_lens, torch.int32, cfg.batch)
     _summaries(cfg, summaries)
     kv = _kv(cfg, k, v, block_table, num_pages)
-    _same_gpu(seq_lens=seq_lens, summaries=summaries, k=k, v=v, block_table=block_table)
+    _same_gpu(seq_lens=seq_lens, summaries=summaries, k=k, v=v, block_table=block_table,
+              query_basis=cfg.query_basis)
     _check(lib().cobs_build_block_stats(ctypes.byref(cfg.c_struct()), ctypes.byref(kv),
                                         _ptr(seq_lens), int(first_block), int(num_blocks),
                                         _ptr(summaries), _ptr(ws),
@@ -256,7 +268,8 @@ def cobs_select(cfg, q, summaries, seq_lens, sel, ws, scores=None, stream=None):
     _select_io(cfg, q, seq_lens, sel, scores)
     _summaries(cfg, summaries)
     nws = _ws(ws)
-    _same_gpu(q=q, summaries=summaries, seq_lens=seq_lens, sel=sel, scores=scores, ws=ws)
+    _same_gpu(q=q, summaries=summaries, seq_lens=seq_lens, sel=sel, scores=scores, ws=ws,
+              query_basis=cfg.query_basis)
     _check(lib().cobs_select(ctypes.byref(cfg.c_struct()), _ptr(q), _ptr(summaries),
                              _ptr(seq_lens), _ptr(sel), _ptr(scores), _ptr(ws), nws, _stream(stream, q)))
 
@@ -323,7 +336,7 @@ def cobs_decode_step(cfg, q, k, v, seq_lens, summaries, out, ws, sel=None, lse=N
     kv = _kv(cfg, k, v, block_table, num_pages)
     nws = _ws(ws)
     _same_gpu(q=q, k=k, v=v, seq_lens=seq_lens, summaries=summaries, sel=sel, out=out, lse=lse, ws=ws,
-              block_table=block_table)
+              block_table=block_table, query_basis=cfg.query_basis)
     _check(lib().cobs_decode_step(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
                                   _ptr(seq_lens), _ptr(summaries), _ptr(sel), _ptr(out), _ptr(lse),
                                   _ptr(ws), nws, _stream(stream, q)))
@@ -336,7 +349,7 @@ def cobs_decode_step_noalloc(cfg, q, k, v, seq_lens, summaries, out, sel=None, l
     _summaries(cfg, summaries)
     kv = _kv(cfg, k, v, block_table, num_pages)
     _same_gpu(q=q, k=k, v=v, seq_lens=seq_lens, summaries=summaries, sel=sel, out=out, lse=lse,
-              block_table=block_table)
+              block_table=block_table, query_basis=cfg.query_basis)
     _check(lib().cobs_decode_step_noalloc(ctypes.byref(cfg.c_struct()), _ptr(q), ctypes.byref(kv),
                                           _ptr(seq_lens), _ptr(summaries), _ptr(sel), _ptr(out), _ptr(lse),
                                           _stream(stream, q)))

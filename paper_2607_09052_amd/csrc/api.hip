@@ -41,6 +41,23 @@ cobs_status_t check_config(const cobs_config_t* c) {
   if (c->rank > kMaxRank) return COBS_ERR_UNSUPPORTED;
   if (c->max_seq_len / c->block_size > kMaxBlocksPerSeq) return COBS_ERR_UNSUPPORTED;
   if (c->options & ~(COBS_OPT_SKEW | COBS_OPT_VALUE_MEAN)) return COBS_ERR_INVALID_ARG;
+  // subspace factors (Sec. 5.4): a basis exactly when a dimension is given,
+  // rank in [1, 4] (the scorer's bf16 / E2M1 condition is checked by the calls
+  // that score: see check_scorer)
+  if (c->subspace_dim < 0) return COBS_ERR_INVALID_ARG;
+  if ((c->subspace_dim > 0) != (c->query_basis != nullptr)) return COBS_ERR_INVALID_ARG;
+  if (c->subspace_dim > 0) {
+    if (c->rank < 1 || !aligned(c->query_basis, 16)) return COBS_ERR_INVALID_ARG;
+    if (c->subspace_dim % 32 || c->subspace_dim >= c->head_dim || c->rank > 4) return COBS_ERR_UNSUPPORTED;
+  }
+  return COBS_OK;
+}
+
+// Subspace factors are scored on the matrix cores only: bf16 / E2M1 mean and
+// factors (a build with fp32 storage is allowed).
+cobs_status_t check_scorer(const cobs_config_t* c) {
+  if (c->subspace_dim > 0 && (c->mean_dtype == COBS_F32 || c->factor_dtype == COBS_F32))
+    return COBS_ERR_UNSUPPORTED;
   return COBS_OK;
 }
 
@@ -49,11 +66,13 @@ struct Derived {
   int L, lsh;           // block length and its log2
   int mdt, fdt, kv_f32;
   int skew, vmean;      // optional record parts
+  int fd;               // elements of a factor vector (d, or the subspace dimension)
+  const float* basis;   // U_Q [Hkv][d][fd] of subspace factors; null for full space
   float c;
   RecLayout lay;
   int nch_max;          // selector: workgroups (chunks) per unit, upper bound
   int nwg_max;          // decode: workgroups (partials) per unit, upper bound
-  size_t sel_ell, sel_part, sel_cnt, sel_bytes;
+  size_t sel_ell, sel_part, sel_cnt, sel_qt, sel_bytes;
   size_t dec_part, dec_cnt, dec_bytes;
   size_t step_sel, step_bytes;   // decode step: select region, decode region, selection
   int nchx_max;                  // exact-mass selector: chunks per unit, upper bound
@@ -81,7 +100,9 @@ Derived derive(const cobs_config_t* c) {
   v.c = c->softmax_scale > 0.0f ? c->softmax_scale : 1.0f / sqrtf((float)v.d);
   v.skew = (c->options & COBS_OPT_SKEW) ? 1 : 0;
   v.vmean = (c->options & COBS_OPT_VALUE_MEAN) ? 1 : 0;
-  v.lay = rec_layout(v.d, v.r, v.mdt, v.fdt, v.skew != 0, v.vmean != 0);
+  v.fd = c->subspace_dim > 0 ? c->subspace_dim : v.d;
+  v.basis = c->subspace_dim > 0 ? c->query_basis : nullptr;
+  v.lay = rec_layout(v.d, v.r, v.mdt, v.fdt, v.skew != 0, v.vmean != 0, v.fd);
 
   // grid bounds for the workspace; the launchers pick the actual grids within them
   v.nch_max = (v.nbmax + select_min_bpw(v.mdt, v.fdt) - 1) / select_min_bpw(v.mdt, v.fdt);
@@ -91,6 +112,7 @@ Derived derive(const cobs_config_t* c) {
   v.sel_ell = off;  off = round_up(off + sizeof(float) * (size_t)v.units * v.G * v.nbmax, kAlign);
   v.sel_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nch_max * v.G * 2, kAlign);
   v.sel_cnt = off;  off = round_up(off + sizeof(unsigned) * (size_t)v.units, kAlign);
+  v.sel_qt = off;   off = round_up(off + (v.basis ? sizeof(float) * (size_t)v.B * v.hq * v.fd : 0), kAlign);
   v.sel_bytes = off;
   off = 0;
   v.dec_part = off; off = round_up(off + sizeof(float) * (size_t)v.units * v.nwg_max * v.G * (v.d + 2), kAlign);
@@ -163,6 +185,8 @@ cobs_status_t run_build(const Derived& v, const cobs_kv_t* kv, const int32_t* se
   p.skew = v.skew;
   p.vmean = v.vmean;
   p.lay = v.lay;
+  p.basis = v.basis;
+  p.fd = v.fd;
   if (!tail && count == 0) return COBS_OK;
   dim3 grid(tail ? 1 : count, v.hkv, v.B);
   return hip_status(launch_build(p, v.d, grid, st));
@@ -200,6 +224,9 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
   p.vmean = v.vmean;
   p.c = v.c;
   p.lay = v.lay;
+  p.basis = v.basis;
+  p.qt = v.basis ? reinterpret_cast<float*>(ws + v.sel_qt) : nullptr;
+  p.fd = v.fd;
   return hip_status(launch_select(p, v.d, v.G, v.B, st));
 }
 
@@ -233,6 +260,9 @@ cobs_status_t run_select_exact(const Derived& v, const float* q, const cobs_kv_t
   p.vmean = 0;
   p.c = v.c;
   p.lay = v.lay;
+  p.basis = nullptr;
+  p.qt = nullptr;
+  p.fd = v.fd;
   return hip_status(launch_select_exact(p, v.d, v.G, v.B, st, quest));
 }
 
@@ -270,6 +300,7 @@ cobs_status_t check_step(const cobs_config_t* cfg, const float* q, const cobs_kv
                          const int32_t* seq_lens, void* summaries, float* out) {
   cobs_status_t s = check_config(cfg);
   if (s != COBS_OK) return s;
+  if ((s = check_scorer(cfg)) != COBS_OK) return s;
   const Derived v = derive(cfg);
   if ((s = check_kv(kv, v)) != COBS_OK) return s;
   if (!q || !seq_lens || !summaries || !out || !aligned(summaries, 16)) return COBS_ERR_INVALID_ARG;
@@ -282,7 +313,7 @@ cobs_status_t run_step(const Derived& v, const float* q, const cobs_kv_t* kv, co
                        void* summaries, int32_t* sel, float* out, float* lse, uint8_t* wsb, hipStream_t st) {
   cobs_status_t s;
   int32_t* selp = sel ? sel : reinterpret_cast<int32_t*>(wsb + v.step_sel);
-  if (select_refreshes(v.r, v.kv_f32 != 0, v.L)) {
+  if (!v.basis && select_refreshes(v.r, v.kv_f32 != 0, v.L)) {
     // the selector's launch recomputes the newest block's record before scoring
     if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st, kv)) != COBS_OK) return s;
     return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
@@ -401,6 +432,7 @@ cobs_status_t cobs_select(const cobs_config_t* cfg, const float* q, const void* 
                           size_t ws_bytes, void* stream) {
   cobs_status_t s = check_config(cfg);
   if (s != COBS_OK) return s;
+  if ((s = check_scorer(cfg)) != COBS_OK) return s;
   const Derived v = derive(cfg);
   if (!q || !summaries || !seq_lens || !sel || !aligned(summaries, 16)) return COBS_ERR_INVALID_ARG;
   if ((s = check_ws(ws, ws_bytes, v.sel_bytes)) != COBS_OK) return s;

@@ -43,6 +43,10 @@ struct StatsArgs {
   int hkv, nbmax, r, mdt, fdt;
   int skew, vmean;       // optional record parts: skew coefficients, value mean
   RecLayout lay;
+  // subspace factors (Sec. 5.4): U_Q of every KV head, [Hkv][D][fd] fp32 with
+  // orthonormal columns; null for full-space factors (fd = D)
+  const float* basis;
+  int fd;
 };
 
 __device__ __forceinline__ float init_sign(int i, int p) {
@@ -53,28 +57,27 @@ __device__ __forceinline__ float init_sign(int i, int p) {
   return (h & 1u) ? 1.0f : -1.0f;
 }
 
-// Encode one vector of D fp32 values held in LDS (`x`) into `dst` with the
-// given storage dtype, by one wave (no barriers).  For E2M1 the scale
-// fp32(max|x|)/6 is written to *scale_dst.
-template <int D>
-__device__ __forceinline__ void store_vector_wave(const float* x, int dt, uint8_t* dst, float* scale_dst,
+// Encode one vector of `len` fp32 values held in LDS (`x`, len a multiple of
+// 8) into `dst` with the given storage dtype, by one wave (no barriers).  For
+// E2M1 the scale fp32(max|x|)/6 is written to *scale_dst.
+__device__ __forceinline__ void store_vector_wave(const float* x, int len, int dt, uint8_t* dst, float* scale_dst,
                                                   int lane) {
   if (dt == DT_F32) {
-    for (int e = lane; e < D; e += 64) reinterpret_cast<float*>(dst)[e] = x[e];
+    for (int e = lane; e < len; e += 64) reinterpret_cast<float*>(dst)[e] = x[e];
     return;
   }
   if (dt == DT_BF16) {
-    for (int e = lane; e < D / 2; e += 64) {
+    for (int e = lane; e < len / 2; e += 64) {
       const uint32_t lo = f32_to_bf16_rne(x[2 * e]), hi = f32_to_bf16_rne(x[2 * e + 1]);
       reinterpret_cast<uint32_t*>(dst)[e] = lo | (hi << 16);
     }
     return;
   }
   float m = 0.0f;
-  for (int e = lane; e < D; e += 64) m = fmaxf(m, fabsf(x[e]));
+  for (int e = lane; e < len; e += 64) m = fmaxf(m, fabsf(x[e]));
   const float scale = wave_max(m) / 6.0f;
   if (lane == 0) *scale_dst = scale;
-  for (int e = lane; e < D / 8; e += 64) {
+  for (int e = lane; e < len / 8; e += 64) {
     uint32_t w = 0;
     if (scale > 0.0f) {
 #pragma unroll
@@ -84,7 +87,8 @@ __device__ __forceinline__ void store_vector_wave(const float* x, int dt, uint8_
   }
 }
 
-// LDS carve-out of the statistics pool (16-byte aligned pieces).
+// LDS carve-out of the statistics pool (16-byte aligned pieces); KF32: the
+// staged keys are fp32.
 template <int D, int P, int LB, bool KF32>
 struct StatsLds {
   static constexpr int KS = LB + 4;                        // row stride of the transposed keys
@@ -114,15 +118,19 @@ constexpr size_t stats_lds_bytes() { return StatsLds<D, P, LB, KF32>::bytes; }
 
 // Run by a workgroup of NT >= kBuildThreads threads; the work is laid out on
 // the first kBuildThreads (four waves), every thread takes part in the barriers.
-template <int D, int P, int LB, bool KF32, int NT = kBuildThreads>
+// KF32: fp32 keys.  SS: subspace factors (Sec. 5.4), the eigen-decomposition of
+// B_b = U_Q^T Sigma_b U_Q through the Gram trick on the projected centred keys
+// Kc U_Q, staged in fp32 (the LDS pool of stats_lds_bytes<D, P, LB, true>).
+template <int D, int P, int LB, bool KF32, bool SS = false, int NT = kBuildThreads>
 __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, int j, int n, char* pool) {
   static_assert(NT % 64 == 0 && NT >= kBuildThreads, "whole waves, at least four");
   static_assert(LB == 32 || LB == 64 || LB == 128, "block of 32, 64 or 128 tokens");
-  using Lay = StatsLds<D, P, LB, KF32>;
+  constexpr bool S32 = KF32 || SS;                 // fp32 staging
+  using Lay = StatsLds<D, P, LB, S32>;
   constexpr int KS = Lay::KS;
   constexpr int NT16 = LB / 16;                    // 16-row tiles of the block
   constexpr int RTW = (NT16 + 3) / 4;              // row tiles per wave
-  typedef typename std::conditional<KF32, float, uint16_t>::type kt_t;
+  typedef typename std::conditional<S32, float, uint16_t>::type kt_t;
   kt_t* KT = reinterpret_cast<kt_t*>(pool + Lay::kt);
   float* mean = reinterpret_cast<float*>(pool + Lay::mean);
   float* vmean = reinterpret_cast<float*>(pool + Lay::vmean);
@@ -139,11 +147,14 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   float* ritzval = reinterpret_cast<float*>(pool + Lay::ritz);
   float* skw = reinterpret_cast<float*>(pool + Lay::skw);
   float* diag_s = reinterpret_cast<float*>(pool + Lay::diag);
-  // centred key e of row i, as the block's fp32 arithmetic sees it
+  // centred key e of row i, as the block's fp32 arithmetic sees it (with SS,
+  // once projected: element e < fd of the projected centred row)
   auto kc = [&](int e, int i) -> float {
-    if constexpr (KF32) return KT[e * KS + i] - mean[e];
+    if constexpr (SS) return KT[e * KS + i];
+    else if constexpr (KF32) return KT[e * KS + i] - mean[e];
     else return __uint_as_float((uint32_t)KT[e * KS + i] << 16) - mean[e];
   };
+  const int fdim = SS ? p.fd : D;                  // elements of a factor
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -216,12 +227,50 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       const int i = r0 + ps * RPP;
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        if constexpr (KF32) KT[(e0 + q) * KS + i] = v[ps][q];
+        if constexpr (S32) KT[(e0 + q) * KS + i] = v[ps][q];
         else KT[(e0 + q) * KS + i] = (uint16_t)(__float_as_uint(v[ps][q]) >> 16);
       }
     }
     __syncthreads();
     const int lr = lane & 15, lk = lane >> 4;
+    if constexpr (SS) {
+      // ---- projection: row f < fd of the staged keys becomes sum_e U[e][f] kc_i[e],
+      // 16 x 16 output tiles (f, i) on the fp32 matrix cores, A[m][k] = U[e][f]
+      // (read from the basis), B[k][n] = the centred key (e, i); the tiles stay
+      // in registers until every wave has read the raw keys
+      constexpr int PT = (D / 16) * NT16;
+      constexpr int PTW = (PT + 3) / 4;
+      const float* U = p.basis + (int64_t)h * D * fdim;
+      const int nft = fdim / 16;
+      f32x4_t pacc[PTW];
+#pragma unroll
+      for (int k = 0; k < PTW; ++k) pacc[k] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      if (lw) {
+        for (int e = 0; e < D; e += 4) {
+#pragma unroll
+          for (int k = 0; k < PTW; ++k) {
+            const int tl = wave + 4 * k, ft = tl / NT16, it = tl % NT16;
+            if (ft < nft) {
+              const float kcv = KT[(e + lk) * KS + 16 * it + lr] - mean[e + lk];
+              pacc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(U[(int64_t)(e + lk) * fdim + 16 * ft + lr], kcv,
+                                                            pacc[k], 0, 0, 0);
+            }
+          }
+        }
+      }
+      __syncthreads();
+      if (lw) {
+#pragma unroll
+        for (int k = 0; k < PTW; ++k) {
+          const int tl = wave + 4 * k, ft = tl / NT16, it = tl % NT16;
+          if (ft < nft) {
+#pragma unroll
+            for (int vv = 0; vv < 4; ++vv) KT[(16 * ft + 4 * lk + vv) * KS + 16 * it + lr] = pacc[k][vv];
+          }
+        }
+      }
+      __syncthreads();
+    }
     // ---- Gram matrix Kc Kc^T on the fp32 matrix cores (v_mfma_f32_16x16x4_f32:
     // lane l supplies A[l%16][l/16] and B[l/16][l%16] and gets D[4(l/16)+v][l%16]).
     // For its row tiles t, a wave forms the tiles (a, t), a < LB/16, and keeps
@@ -234,12 +283,14 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
 #pragma unroll
       for (int a = 0; a < NT16; ++a) gr[k][a] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
       if (lw && t < NT16) {
-#pragma unroll 4
-        for (int e = 0; e < D; e += 4) {
-          const float bt = kc(e + lk, 16 * t + lr);
+        for (int e0 = 0; e0 < fdim; e0 += 16) {     // fdim: a multiple of 32
 #pragma unroll
-          for (int a = 0; a < NT16; ++a)
-            gr[k][a] = __builtin_amdgcn_mfma_f32_16x16x4f32(kc(e + lk, 16 * a + lr), bt, gr[k][a], 0, 0, 0);
+          for (int e = e0; e < e0 + 16; e += 4) {
+            const float bt = kc(e + lk, 16 * t + lr);
+#pragma unroll
+            for (int a = 0; a < NT16; ++a)
+              gr[k][a] = __builtin_amdgcn_mfma_f32_16x16x4f32(kc(e + lk, 16 * a + lr), bt, gr[k][a], 0, 0, 0);
+          }
         }
 #pragma unroll
         for (int a = 0; a < NT16; ++a)
@@ -475,7 +526,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
     for (int idx = tid; idx < r * D; idx += NT) {
       const int i = idx / D, e = idx % D;
       float s = 0.0f;
-      if (ritzval[i] > 1e-6f * top && top > 0.0f) {
+      if (e < fdim && ritzval[i] > 1e-6f * top && top > 0.0f) {
         for (int row = 0; row < LB; ++row) s += kc(e, row) * Yp[i * LB + row];
         s *= rs;
       }
@@ -488,7 +539,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       float best = -1.0f;
       int bidx = 0;
       if (i < r) {
-        for (int e = lt; e < D; e += 16) {
+        for (int e = lt; e < fdim; e += 16) {
           const float a = fabsf(Xi[i * D + e]);
           if (a > best) { best = a; bidx = e; }
         }
@@ -502,7 +553,7 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       const float pivot = (i < r) ? Xi[i * D + bidx] : 0.0f;
       __syncthreads();                   // every thread has read its pivot before any flip
       if (i < r && pivot < 0.0f) {
-        for (int e = lt; e < D; e += 16) Xi[i * D + e] = -Xi[i * D + e];
+        for (int e = lt; e < fdim; e += 16) Xi[i * D + e] = -Xi[i * D + e];
       }
       __syncthreads();
     }
@@ -512,12 +563,12 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       // projection on u_i standardised by its deviation
       for (int i = wave; lw && i < r; i += kBuildThreads / 64) {
         float nrm = 0.0f;
-        for (int e = lane; e < D; e += 64) nrm += Xi[i * D + e] * Xi[i * D + e];
+        for (int e = lane; e < fdim; e += 64) nrm += Xi[i * D + e] * Xi[i * D + e];
         const float lam = wave_sum(nrm);
         float z3 = 0.0f;
         for (int t = lane; t < LB; t += 64) {
           float pr = 0.0f;
-          for (int e = 0; e < D; ++e) pr += kc(e, t) * Xi[i * D + e];
+          for (int e = 0; e < fdim; ++e) pr += kc(e, t) * Xi[i * D + e];
           const float z = (lam > 0.0f) ? pr / lam : 0.0f;
           z3 += z * z * z;
         }
@@ -539,12 +590,12 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
   const int nvec = 1 + nr + (p.vmean ? 1 : 0);     // mean, factors, value mean
   for (int vi = wave; lw && vi < nvec; vi += kBuildThreads / 64) {
     if (vi == 0) {
-      store_vector_wave<D>(mean, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), lane);
+      store_vector_wave(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), lane);
     } else if (vi <= nr) {
-      store_vector_wave<D>(&Xi[(vi - 1) * D], p.fdt, R + lay.fac_off + (vi - 1) * lay.vec_bytes,
-                           reinterpret_cast<float*>(R + 16) + (vi - 1), lane);
+      store_vector_wave(&Xi[(vi - 1) * D], fdim, p.fdt, R + lay.fac_off + (vi - 1) * lay.vec_bytes,
+                        reinterpret_cast<float*>(R + 16) + (vi - 1), lane);
     } else {
-      store_vector_wave<D>(vmean, p.mdt, R + lay.vmean_off, reinterpret_cast<float*>(R + 8), lane);
+      store_vector_wave(vmean, D, p.mdt, R + lay.vmean_off, reinterpret_cast<float*>(R + 8), lane);
     }
   }
   // factors of a block without them, and the padding after the last vector

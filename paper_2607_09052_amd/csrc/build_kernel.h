@@ -1,0 +1,58 @@
+// The block statistics build kernel: one 256-thread workgroup per (batch row,
+// KV head, block) of LB tokens.
+#pragma once
+
+#include "block_stats.h"
+#include "cobs_kernels.h"
+
+namespace cobs {
+
+template <int D, int P, int LB, bool KF32, bool SS>
+__global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams p) {
+  __shared__ __align__(16) char pool[stats_lds_bytes<D, P, LB, KF32 || SS>()];
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int T = clamp_len(p.seq_lens[b], p.tmax);
+  if (T <= 0) return;
+  const int nb = (T + LB - 1) / LB;
+  const int j = p.tail_mode ? (T - 1) / LB : p.first_block + (int)blockIdx.x;
+  if (j < 0 || j >= nb) return;
+  StatsArgs a;
+  a.kv = p.kv;
+  a.rec = p.rec;
+  a.hkv = p.hkv;
+  a.nbmax = p.nbmax;
+  a.r = p.r;
+  a.mdt = p.mdt;
+  a.fdt = p.fdt;
+  a.skew = p.skew;
+  a.vmean = p.vmean;
+  a.lay = p.lay;
+  a.basis = p.basis;
+  a.fd = SS ? p.fd : D;
+  block_stats<D, P, LB, KF32, SS>(a, b, h, j, min(LB, T - j * LB), pool);
+}
+
+// Launch over `grid` for the block length of p.kv.
+template <int D, int P, bool SS>
+hipError_t launch_build_dp(const BuildParams& p, dim3 grid, hipStream_t st) {
+  switch (p.kv.lsh) {
+    case 5:
+      if (p.kv_f32) hipLaunchKernelGGL((build_stats_kernel<D, P, 32, true, SS>), grid, dim3(kBuildThreads), 0, st, p);
+      else hipLaunchKernelGGL((build_stats_kernel<D, P, 32, false, SS>), grid, dim3(kBuildThreads), 0, st, p);
+      break;
+    case 7:
+      if (p.kv_f32) hipLaunchKernelGGL((build_stats_kernel<D, P, 128, true, SS>), grid, dim3(kBuildThreads), 0, st, p);
+      else hipLaunchKernelGGL((build_stats_kernel<D, P, 128, false, SS>), grid, dim3(kBuildThreads), 0, st, p);
+      break;
+    default:
+      if (p.kv_f32) hipLaunchKernelGGL((build_stats_kernel<D, P, 64, true, SS>), grid, dim3(kBuildThreads), 0, st, p);
+      else hipLaunchKernelGGL((build_stats_kernel<D, P, 64, false, SS>), grid, dim3(kBuildThreads), 0, st, p);
+  }
+  return hipGetLastError();
+}
+
+// 16 columns converge for r <= 4 at L <= 64; 32 beyond r = 4, and at L = 128,
+// where the 128 x 128 Gram matrix of unstructured keys has a flat top.
+inline bool build_big_basis(const BuildParams& p) { return p.r > 4 || p.kv.lsh == 7; }
+
+}  // namespace cobs

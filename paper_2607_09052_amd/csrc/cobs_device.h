@@ -31,15 +31,17 @@ __host__ __device__ inline int vec_bytes(int d, int dt) {
   return dt == DT_F32 ? 4 * d : (dt == DT_BF16 ? 2 * d : d / 2);
 }
 
+// Factor vectors hold `fd` elements: d for full-space factors, the subspace
+// dimension for subspace factors (Sec. 5.4); 0 means d.
 __host__ __device__ inline RecLayout rec_layout(int d, int r, int mdt, int fdt, bool skew = false,
-                                                bool vmean = false) {
+                                                bool vmean = false, int fd = 0) {
   RecLayout l;
   const int fscale = (fdt == DT_E2M1) ? ((4 * r + 15) / 16) * 16 : 0;
   l.skew_off = 16 + fscale;
   l.mean_off = l.skew_off + (skew ? ((4 * r + 15) / 16) * 16 : 0);
   l.mean_bytes = vec_bytes(d, mdt);
   l.fac_off = l.mean_off + l.mean_bytes;
-  l.vec_bytes = vec_bytes(d, fdt);
+  l.vec_bytes = vec_bytes(fd > 0 ? fd : d, fdt);
   l.vmean_off = l.fac_off + r * l.vec_bytes;
   l.total = ((l.vmean_off + (vmean ? l.mean_bytes : 0) + 15) / 16) * 16;
   return l;

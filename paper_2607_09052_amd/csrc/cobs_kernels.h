@@ -14,6 +14,8 @@ struct BuildParams {
   int hkv, tmax, nbmax, r, mdt, fdt, first_block, tail_mode, kv_f32;
   int skew, vmean;      // optional record parts (skew coefficients, value mean)
   RecLayout lay;
+  const float* basis;   // subspace factors: U_Q [Hkv][d][fd] fp32; null: full space
+  int fd;               // elements of a factor vector
 };
 
 struct SelectParams {
@@ -30,6 +32,12 @@ struct SelectParams {
   int skew, vmean;  // records carry skew coefficients (scored) / a value mean (kept by the refresh)
   float c;
   RecLayout lay;
+  // subspace factors (Sec. 5.4): the basis U_Q [Hkv][d][fd] and the projected
+  // queries U_Q^T q [B, Hq, fd] (without c, written by the launcher) that meet
+  // the factors; null for full-space factors
+  const float* basis;
+  float* qt;
+  int fd;           // elements of a factor vector
   // decode step (bf16 K/V, r <= 4): the workgroup whose chunk holds a row's
   // newest block first recomputes that block's record in `tail_rec` (the same
   // records as `rec`) from the keys in `kv`; null: no refresh

@@ -11,6 +11,24 @@ typedef void (*SelectKernel)(SelectParams);
 SelectKernel select_valu_kernel_for(const SelectParams& p, int d, int g);
 SelectKernel select_mfma_kernel_for(const SelectParams& p, int d, int g);
 SelectKernel select_refresh_kernel_for(const SelectParams& p, int d, int g);
+SelectKernel select_ss_kernel_for(const SelectParams& p, int d, int g);
+
+// Projected queries U_Q^T q of Sec. 5.4 for every (batch row, query head): one
+// 128-thread workgroup each, thread f summing over the d elements in order.
+__global__ __launch_bounds__(128) void project_queries_kernel(const float* q, const float* basis, float* qt,
+                                                              int hq, int g, int d, int fd) {
+  __shared__ float qs[128];
+  const int64_t row = blockIdx.x;                  // b * Hq + query head
+  const int hk = (int)(row % hq) / g;
+  for (int e = threadIdx.x; e < d; e += 128) qs[e] = q[row * d + e];
+  __syncthreads();
+  const float* U = basis + (int64_t)hk * d * fd;
+  for (int f = threadIdx.x; f < fd; f += 128) {
+    float a = 0.0f;
+    for (int e = 0; e < d; ++e) a += qs[e] * U[(int64_t)e * fd + f];
+    qt[row * fd + f] = a;
+  }
+}
 
 bool select_on_matrix_cores(int mdt, int fdt) { return mdt != DT_F32 && fdt != DT_F32; }
 
@@ -22,16 +40,19 @@ int select_min_bpw(int mdt, int fdt) { return select_on_matrix_cores(mdt, fdt) ?
 
 hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st) {
   const bool mfma = select_on_matrix_cores(p.mdt, p.fdt);
-  const SelectKernel k = p.tail_rec ? select_refresh_kernel_for(p, d, g)
-                                    : (mfma ? select_mfma_kernel_for(p, d, g) : select_valu_kernel_for(p, d, g));
+  const bool ss = p.qt != nullptr;                 // subspace factors: matrix cores, no refresh
+  if (ss && (!mfma || p.tail_rec || !p.basis || d > 128)) return hipErrorInvalidValue;
+  const SelectKernel k = ss ? select_ss_kernel_for(p, d, g)
+                            : p.tail_rec ? select_refresh_kernel_for(p, d, g)
+                                         : (mfma ? select_mfma_kernel_for(p, d, g) : select_valu_kernel_for(p, d, g));
   if (!k) return hipErrorInvalidValue;
   const int base = select_min_bpw(p.mdt, p.fdt);
   const int64_t units = (int64_t)batch * p.hkv;
   // The grid is sized for the smaller resident count of the plain and the
   // refreshing selector, so the decode step and a standalone selection chunk
   // the blocks alike and their scores agree bitwise.
-  const SelectKernel kp = mfma ? select_mfma_kernel_for(p, d, g) : select_valu_kernel_for(p, d, g);
-  const SelectKernel kr = select_refresh_kernel_for(p, d, g);
+  const SelectKernel kp = ss ? k : mfma ? select_mfma_kernel_for(p, d, g) : select_valu_kernel_for(p, d, g);
+  const SelectKernel kr = ss ? nullptr : select_refresh_kernel_for(p, d, g);
   if (!kp) return hipErrorInvalidValue;
   int resident = resident_workgroups(reinterpret_cast<const void*>(kp), 256);
   if (kr) resident = std::min(resident, resident_workgroups(reinterpret_cast<const void*>(kr), 256));
@@ -41,6 +62,12 @@ hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st
   bpw = std::max<int64_t>(base, (bpw + base - 1) / base * base);
   p.bpw = (int)std::min<int64_t>(bpw, ((int64_t)p.nbmax + base - 1) / base * base);
   p.nch = (p.nbmax + p.bpw - 1) / p.bpw;
+  if (ss) {
+    hipLaunchKernelGGL(project_queries_kernel, dim3((unsigned)(batch * p.hq)), dim3(128), 0, st, p.q, p.basis, p.qt,
+                       p.hq, g, d, p.fd);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   hipLaunchKernelGGL(k, dim3(p.nch, p.hkv, batch), dim3(256), 0, st, p);
   return hipGetLastError();
 }

@@ -40,7 +40,8 @@ __device__ __forceinline__ void load_words(const uint8_t* src, uint32_t* w) {
     const uint2 u = *reinterpret_cast<const uint2*>(src);
     w[0] = u.x; w[1] = u.y;
   } else {
-    w[0] = *reinterpret_cast<const uint32_t*>(src);
+#pragma unroll
+    for (int k = 0; k < NW; ++k) w[k] = reinterpret_cast<const uint32_t*>(src)[k];
   }
 }
 
@@ -552,18 +553,45 @@ __device__ __forceinline__ sbf16x8_t tile_operand(const uint32_t* w, int kk) {
   }
 }
 
+// 8 NK query elements of a lane (x[8 kk + j], scaled by qs) as three bf16
+// parts each, whose products with a bf16 value are exact in fp32.
+template <int NK>
+__device__ __forceinline__ void split_query(const float* x, float qs, sbf16x8_t (&dst)[3][NK]) {
+  const float4* xg = reinterpret_cast<const float4*>(x);
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk) {
+    const float4 x0 = xg[2 * kk], x1 = xg[2 * kk + 1];
+    const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      float v = xs[j] * qs;
+#pragma unroll
+      for (int part = 0; part < 3; ++part) {
+        const uint32_t bb = f32_to_bf16_rne(v);
+        dst[part][kk][j] = __builtin_bit_cast(__bf16, (uint16_t)bb);
+        v -= __uint_as_float(bb << 16);
+      }
+    }
+  }
+}
+
 template <int G, int RMAX, int FDT>
 constexpr size_t select_mfma_lds() {
   return select_pool_bytes<4 * 16 * (1 + ((FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0)) * 16 + 2 * 4 * G * 4 +
                            4 * 16 * ((RMAX + 3) / 4) * 16>();
 }
 
-// `pool`: select_mfma_lds<G, RMAX, FDT>() bytes of LDS.
-template <int D, int G, int RMAX, int MDT, int FDT>
+// `pool`: select_mfma_lds<G, RMAX, FDT>() bytes of LDS.  FD < D: subspace
+// factors of FD elements (Sec. 5.4), whose B operand is the projected query
+// U_Q^T q (p.qt) instead of q; the mean keeps the full q.
+template <int D, int G, int RMAX, int MDT, int FDT, int FD = D>
 __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, int h, int chunk, char* pool) {
   static_assert(MDT != DT_F32 && FDT != DT_F32, "matrix-core scorer takes bf16 / E2M1 descriptors");
-  constexpr int KST = D / 32;                                  // k-steps per lane group
-  constexpr int MW = elem_bytes<MDT>(D / 4) / 4, FW = elem_bytes<FDT>(D / 4) / 4;
+  static_assert(FD % 32 == 0 && FD <= D, "factor dimension a multiple of 32, at most d");
+  constexpr bool kSS = FD < D;
+  constexpr int KST = D / 32;                                  // k-steps per lane group (mean)
+  constexpr int KSF = FD / 32;                                 // k-steps per lane group (factors)
+  constexpr int MW = elem_bytes<MDT>(D / 4) / 4, FW = elem_bytes<FDT>(FD / 4) / 4;
   constexpr int HU = 1 + ((FDT == DT_E2M1) ? (RMAX + 3) / 4 : 0);   // 16-byte header words used
   constexpr int KW = (RMAX + 3) / 4;                                 // 16-byte words of skew coefficients
   uint4 (*hdr_s)[16][HU] = reinterpret_cast<uint4 (*)[16][HU]>(pool);
@@ -607,28 +635,20 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
   Tile cur;
   load(blk_lo + 16 * wave, cur);
 
-  // B operands: head hcol (zero beyond G), d = grp*D/4 + 8*kk + j, three bf16 parts
+  // B operands: head hcol (zero beyond G), d = grp*D/4 + 8*kk + j, three bf16
+  // parts; subspace factors meet the projected query, f = grp*FD/4 + 8*kk + j
   sbf16x8_t qb[3][KST];
+  sbf16x8_t qbf[3][kSS ? KSF : 1];
   {
-    const float4* qg = reinterpret_cast<const float4*>(
-        p.q + ((int64_t)b * p.hq + h * G + min(hcol, G - 1)) * D + grp * (D / 4));
+    const int64_t qh = (int64_t)b * p.hq + h * G + min(hcol, G - 1);
     const float qs = (hcol < G) ? p.c : 0.0f;
-#pragma unroll
-    for (int kk = 0; kk < KST; ++kk) {
-      const float4 x0 = qg[2 * kk], x1 = qg[2 * kk + 1];
-      const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        float x = xs[j] * qs;
-#pragma unroll
-        for (int part = 0; part < 3; ++part) {
-          const uint32_t bb = f32_to_bf16_rne(x);
-          qb[part][kk][j] = __builtin_bit_cast(__bf16, (uint16_t)bb);
-          x -= __uint_as_float(bb << 16);
-        }
-      }
-    }
+    split_query<KST>(p.q + qh * D + grp * (D / 4), qs, qb);
+    if constexpr (kSS) split_query<KSF>(p.qt + qh * FD + grp * (FD / 4), qs, qbf);
   }
+  auto qfac = [&](int part, int kk) -> sbf16x8_t {
+    if constexpr (kSS) return qbf[part][kk];
+    else return qb[part][kk];
+  };
 
   float run_m = -INFINITY, run_s = 0.0f;   // this lane's blocks, head hcol
   for (int c0 = blk_lo + 16 * wave; c0 < blk_hi; c0 += 64) {
@@ -655,10 +675,11 @@ __device__ __forceinline__ void select_mfma_task(const SelectParams& p, int b, i
     for (int f = 0; f < RMAX; ++f) {
       af[f] = sf32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-      for (int kk = 0; kk < KST; ++kk) {
+      for (int kk = 0; kk < KSF; ++kk) {
         const sbf16x8_t a = tile_operand<FDT>(fw[f], kk);
 #pragma unroll
-        for (int part = 0; part < 3; ++part) af[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qb[part][kk], af[f], 0, 0, 0);
+        for (int part = 0; part < 3; ++part)
+          af[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qfac(part, kk), af[f], 0, 0, 0);
       }
     }
     wave_lds_sync();
@@ -729,10 +750,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(SelectParams p) {
   select_task<D, G, RMAX, MDT, FDT>(p, blockIdx.z, blockIdx.y, blockIdx.x, pool);
 }
 
-template <int D, int G, int RMAX, int MDT, int FDT>
+template <int D, int G, int RMAX, int MDT, int FDT, int FD = D>
 __global__ __launch_bounds__(kSelThreads) void select_mfma_kernel(SelectParams p) {
   __shared__ __align__(16) char pool[select_mfma_lds<G, RMAX, FDT>()];
-  select_mfma_task<D, G, RMAX, MDT, FDT>(p, blockIdx.z, blockIdx.y, blockIdx.x, pool);
+  select_mfma_task<D, G, RMAX, MDT, FDT, FD>(p, blockIdx.z, blockIdx.y, blockIdx.x, pool);
 }
 
 template <size_t A, size_t B>
@@ -767,6 +788,8 @@ __device__ __forceinline__ void select_refresh_task(const SelectParams& p, char*
     a.skew = p.skew;
     a.vmean = p.vmean;
     a.lay = p.lay;
+    a.basis = nullptr;
+    a.fd = D;
     block_stats<D, 16, kL, false>(a, b, h, j, min(kL, T - j * kL), pool);
     __builtin_amdgcn_s_waitcnt(0);       // the record is written before it is scored
     __syncthreads();

@@ -299,3 +299,33 @@ def _keys_block(n, d, law, seed, rank):
         return ((A @ rng.standard_normal((8, n))).T + math.sqrt(0.1) * rng.standard_normal((n, d))
                 + 0.3 * rng.standard_normal((1, d))).astype(np.float32)
     raise ValueError(law)
+
+
+# ------------------------------------------------- queries in a subspace --
+# Query law for the subspace factors: per KV head a random orthogonal d x d
+# matrix R_h (Gaussian matrix, QR, columns signed so diag of the triangular
+# factor is positive) and a decaying spectrum, q = R_h (sigma * z) with z
+# i.i.d. N(0, 1) and sigma_j^2 = exp(-j / tau): with tau = 30 at d = 128 the
+# leading 66 directions carry 90 % of the energy.  The first s' columns of R_h
+# span the top-s' directions of the population second moment.
+
+def query_rotation(Hkv, d, seed, tau=30.0):
+    """(R [Hkv, d, d] float32, sigma [d] float32) of the subspace query law."""
+    g = _gen("cpu", seed)
+    rot = torch.empty((Hkv, d, d), dtype=torch.float64)
+    for h in range(Hkv):
+        a = torch.randn(d, d, generator=g, dtype=torch.float64)
+        qm, rm = torch.linalg.qr(a)
+        rot[h] = qm * torch.sign(torch.diagonal(rm))[None, :]
+    sigma = torch.exp(-torch.arange(d, dtype=torch.float64) / (2.0 * tau))
+    return rot.to(torch.float32), sigma.to(torch.float32)
+
+
+def subspace_queries(rot, sigma, n, G, seed):
+    """n query rows [n, Hkv * G, d] float32 of the subspace law (head h * G + g
+    of row i draws from R_h)."""
+    Hkv, d, _ = rot.shape
+    g = _gen("cpu", seed)
+    z = torch.randn(n, Hkv, G, d, generator=g, dtype=torch.float32) * sigma
+    q = torch.einsum("hde,nhge->nhgd", rot, z)
+    return q.reshape(n, Hkv * G, d).contiguous()

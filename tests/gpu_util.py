@@ -40,17 +40,19 @@ def f64(t):
     return t.detach().to("cpu").to(torch.float64).numpy()
 
 
-def oracle_select(rec_unit, q_unit, T, cfg):
+def oracle_select(rec_unit, q_unit, T, cfg, U=None):
     """Oracle sigma, candidate count and selection of one unit from record bytes.
-    A row with no tokens has no blocks, no candidates and no selection."""
+    A row with no tokens has no blocks, no candidates and no selection.  U: the
+    unit's query basis for subspace factors."""
     if T <= 0:
         return np.zeros(0), 0, []
-    parts = R.decode(rec_unit, cfg.head_dim, cfg.rank, cfg.mean_dtype, cfg.factor_dtype, cfg.skew, cfg.value_mean)
+    parts = R.decode(rec_unit, cfg.head_dim, cfg.rank, cfg.mean_dtype, cfg.factor_dtype, cfg.skew, cfg.value_mean,
+                     cfg.subspace_dim or None)
     counts, means, factors = parts[:3]
     skews = parts[3] if cfg.skew else None
     nb = M.num_blocks(T, cfg.block_size)
     ell = M.log_mass_estimate(q_unit, counts[:nb], means[:nb], factors[:nb], cfg.scale,
-                              None if skews is None else skews[:nb])
+                              None if skews is None else skews[:nb], U)
     sigma = M.group_scores(ell)
     nc = M.candidate_count(T, cfg.block_size, cfg.window)
     return sigma, nc, M.select_top(sigma, nc, cfg.budget)
@@ -132,11 +134,14 @@ def unit_slices(cfg, b, h):
     return b, slice(h * G, (h + 1) * G)
 
 
-def ky_fan_checks(xi, K, n, r):
+def ky_fan_checks(xi, K, n, r, U=None):
     """Block statistics of the GPU (fp32 factors xi [r, d] of the n keys K) against
     the oracle: Ky-Fan energy, orthogonality and, where the eigengap allows,
-    closeness of the rank-r covariance."""
+    closeness of the rank-r covariance.  With a query basis U [d, s'] the
+    factors are subspace factors [r, s'] of B_b = U^T Sigma_b U (Sec. 5.4)."""
     Sig = M.block_covariance(K)
+    if U is not None:
+        Sig = M.subspace_covariance(Sig, U)
     lam = np.sort(np.clip(np.linalg.eigvalsh(Sig), 0, None))[::-1]
     etop = lam[:r].sum()
     e = float((xi ** 2).sum())
@@ -155,7 +160,7 @@ def ky_fan_checks(xi, K, n, r):
         assert np.linalg.norm(A - Bm) <= 1e-3 * np.linalg.norm(Bm), np.linalg.norm(A - Bm) / np.linalg.norm(Bm)
 
 
-def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None, V_unit=None):
+def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None, V_unit=None, U=None):
     """GPU block records of one unit against the oracle.
 
     rec32_unit: the unit's records built with fp32 mean and factors from the
@@ -163,12 +168,14 @@ def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None, V_unit=None
     fp32 rounding of the oracle's, zero factors for a partial block, Ky-Fan
     energy / orthogonality / rank-r subspace for full blocks, and the configured
     record byte-identical to the oracle's encoding of the fp32 statistics (the
-    storage rounding of Sec. 5.5).  `blocks`: block indices to check (default all)."""
+    storage rounding of Sec. 5.5).  `blocks`: block indices to check (default all).
+    U: the unit's query basis [d, s'] for subspace factors."""
     L, d, r = cfg.block_size, cfg.head_dim, cfg.rank
     nb = M.num_blocks(T, L)
     if nb == 0:
         return
-    parts = R.decode(rec32_unit[:nb], d, r, "f32", "f32", cfg.skew, cfg.value_mean)
+    fdim = cfg.subspace_dim or None
+    parts = R.decode(rec32_unit[:nb], d, r, "f32", "f32", cfg.skew, cfg.value_mean, fdim)
     counts, means, factors = parts[:3]
     skews, vmeans = (parts[3], parts[4]) if (cfg.skew or cfg.value_mean) else (None, None)
     K = np.asarray(K_unit, dtype=np.float64)
@@ -181,9 +188,10 @@ def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None, V_unit=None
         if n < L or r == 0:
             assert np.all(factors[j] == 0), j
         else:
-            ky_fan_checks(factors[j], Kb, n, r)
+            ky_fan_checks(factors[j], Kb, n, r, U)
         if skews is not None:
-            np.testing.assert_allclose(skews[j], M.skew_coefficients(Kb, factors[j]), rtol=1e-4, atol=2e-4)
+            Kp = Kb if U is None else Kb @ U
+            np.testing.assert_allclose(skews[j], M.skew_coefficients(Kp, factors[j]), rtol=1e-4, atol=2e-4)
         if vmeans is not None and V_unit is not None:
             Vb = np.asarray(V_unit, dtype=np.float64)[j * L:j * L + n]
             np.testing.assert_allclose(vmeans[j], M.block_mean(Vb), rtol=0, atol=1e-6 * max(np.abs(Vb).max(), 1e-30))

@@ -50,6 +50,85 @@ def test_record_bytes_match_oracle_layout(md, fd, d, r, skew, vmean):
                                   value_mean=vmean)) == R.layout(d, r, md, fd, skew, vmean)["total"]
 
 
+def _basis_struct(d=128, sd=96, hkv=2, **over):
+    """A config struct with subspace factors and a host stand-in basis address
+    (validation only dereferences nothing)."""
+    cfg = _cfg(head_dim=d, num_kv_heads=hkv, num_q_heads=4 * hkv, mean_dtype="bf16", factor_dtype="e2m1",
+               **over).c_struct()
+    cfg.subspace_dim = sd
+    cfg.query_basis = 1 << 20
+    return cfg
+
+
+@pytest.mark.parametrize("md", ["bf16", "e2m1"])
+@pytest.mark.parametrize("fd", ["bf16", "e2m1"])
+@pytest.mark.parametrize("d,sd", [(128, 32), (128, 64), (128, 96), (64, 32)])
+@pytest.mark.parametrize("skew", [False, True])
+def test_subspace_record_bytes_match_oracle_layout(md, fd, d, sd, skew):
+    cfg = _basis_struct(d=d, sd=sd, skew=skew)
+    cfg.mean_dtype = cobs.DTYPES[md]
+    cfg.factor_dtype = cobs.DTYPES[fd]
+    lay = R.layout(d, 4, md, fd, skew, False, fdim=sd)
+    assert cobs.lib().cobs_record_bytes(ctypes.byref(cfg)) == lay["total"]
+    assert lay["vec_bytes"] == {"bf16": 2, "e2m1": 0.5}[fd] * sd
+
+
+@pytest.mark.parametrize("edit,code", [
+    (dict(query_basis=None), 1),          # a dimension without a basis
+    (dict(subspace_dim=0), 1),            # a basis without a dimension
+    (dict(subspace_dim=-32), 1),
+    (dict(subspace_dim=48), 2),           # not a multiple of 32
+    (dict(subspace_dim=128), 2),          # s' = d is the full space
+    (dict(rank=0), 1),
+    (dict(rank=8), 2),
+    (dict(query_basis=(1 << 20) + 4), 1), # misaligned basis
+])
+def test_invalid_subspace_configs_are_rejected(edit, code):
+    cfg = _basis_struct()
+    for k, v in edit.items():
+        setattr(cfg, k, v)
+    lib = cobs.lib()
+    assert lib.cobs_record_bytes(ctypes.byref(cfg)) == 0
+    fake = ctypes.c_void_p(1 << 20)
+    assert lib.cobs_select(ctypes.byref(cfg), fake, fake, fake, fake, None, ctypes.c_void_p(256), 1 << 30,
+                           None) == code
+
+
+@pytest.mark.parametrize("edit", [dict(factor_dtype=0), dict(mean_dtype=0)])
+def test_subspace_scoring_needs_bf16_or_e2m1_descriptors(edit):
+    """fp32 subspace records are built (record size > 0) but not scored."""
+    cfg = _basis_struct()
+    for k, v in edit.items():
+        setattr(cfg, k, v)
+    lib = cobs.lib()
+    assert lib.cobs_record_bytes(ctypes.byref(cfg)) > 0
+    fake = ctypes.c_void_p(1 << 20)
+    assert lib.cobs_select(ctypes.byref(cfg), fake, fake, fake, fake, None, ctypes.c_void_p(256), 1 << 30,
+                           None) == 2
+    kv = cobs._KV(fake.value, fake.value, 0, 0, 128, None, 0)
+    assert lib.cobs_decode_step(ctypes.byref(cfg), fake, ctypes.byref(kv), fake, fake, None, fake, None,
+                                ctypes.c_void_p(256), 1 << 30, None) == 2
+
+
+def test_binding_checks_the_basis_shape():
+    import torch
+    cfg = _cfg(mean_dtype="bf16", factor_dtype="e2m1", subspace_dim=96,
+               query_basis=torch.zeros(2, 128, 64))
+    with pytest.raises(cobs.CobsError):
+        cfg.c_struct()
+    ok = _cfg(mean_dtype="bf16", factor_dtype="e2m1", subspace_dim=96, query_basis=torch.zeros(2, 128, 96))
+    assert cobs.record_bytes(ok) == R.layout(128, 4, "bf16", "e2m1", fdim=96)["total"]
+
+
+def test_subspace_select_workspace_holds_the_projected_queries():
+    full = _cfg(mean_dtype="bf16", factor_dtype="e2m1")
+    sub = _basis_struct(hkv=full.num_kv_heads)
+    lib = cobs.lib()
+    extra = lib.cobs_workspace_bytes(ctypes.byref(sub), 1) - cobs.workspace_bytes(full, 1)
+    need = 4 * full.batch * full.num_q_heads * 96
+    assert need <= extra < need + 256
+
+
 def test_unknown_options_and_compression_without_value_means_are_rejected():
     lib = cobs.lib()
     cfg = _cfg().c_struct()
