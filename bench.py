@@ -1,6 +1,6 @@
 """Decode-step benchmark of the COBS path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workloads c3,c2,c4,c5] [--copies M]
+    python bench.py [--steps K] [--warmup W] [--workloads c3,c2,c4,c5,c4ss] [--copies M]
                     [--no-cpu-baseline] [--traffic FILE] [--calibrate-copy MIB]
 
 One step = one cobs_decode_step call on one layer: refresh of the record of the
@@ -9,8 +9,10 @@ attention over the selected blocks plus the window, for every batch row and
 KV head.  Inputs are seeded synthetic tensors resident in HBM before timing.
 
 The first workload (default c3: B=32, 32k context, the largest single-GPU
-configuration at 32k) gives the headline line; the others (c2, c4, c5) are
-reported under "workloads" with the same fields.  For each workload:
+configuration at 32k) gives the headline line; the others (c2, c4, c5, and
+c4ss: c4 with subspace factors of 96 elements, Sec. 5.4, and queries drawn in a
+decaying-spectrum subspace) are reported under "workloads" with the same
+fields.  For each workload:
 
 The timed loop is a decode loop: every step appends one token, so the context
 of each layer copy advances by one per step through T_hi-63 .. T_hi (one full
@@ -61,10 +63,12 @@ def vec_bytes(d, dt):
 
 
 def descriptor_bytes(cfg):
-    """Bytes a scorer must read per block: count, mean (+scale), r factors (+scales)."""
+    """Bytes a scorer must read per block: count, mean (+scale), r factors (+scales);
+    subspace factors have subspace_dim elements."""
     d, r = cfg.head_dim, cfg.rank
+    fd = cfg.subspace_dim or d
     b = 4 + vec_bytes(d, cfg.mean_dtype) + (4 if cfg.mean_dtype == "e2m1" else 0)
-    return b + r * vec_bytes(d, cfg.factor_dtype) + (4 * r if cfg.factor_dtype == "e2m1" else 0)
+    return b + r * vec_bytes(fd, cfg.factor_dtype) + (4 * r if cfg.factor_dtype == "e2m1" else 0)
 
 
 def union_tokens(T, w, sel_row, L=64):
@@ -84,7 +88,8 @@ def union_tokens(T, w, sel_row, L=64):
 def algorithmic_bytes(cfg, seq_lens, sel):
     """Per-kernel algorithmic bytes of one decode step, from the actual selection.
 
-    select: every block's descriptor (unpadded), q, sel written.
+    select: every block's descriptor (unpadded), q, sel written; with subspace
+            factors also the basis U_Q once.
     decode: K and V of every attended token, q, sel, out and lse written.
     tail:   the keys of the block holding the newest token, its record written.
     keys:   every key of the cache once, q and sel (the exact-mass selector).
@@ -103,8 +108,9 @@ def algorithmic_bytes(cfg, seq_lens, sel):
         tail += Hkv * (n_tail * d * kv + cobs.record_bytes(cfg))
         for h in range(Hkv):
             dec += union_tokens(T, cfg.window, sel[b, h].tolist()) * d * kv * 2
-    return dict(select=score + q_bytes + sel_bytes, decode=dec + q_bytes + sel_bytes + out_bytes,
-                tail=tail, step=score + dec + tail + q_bytes + sel_bytes + out_bytes,
+    basis = Hkv * d * cfg.subspace_dim * 4
+    return dict(select=score + q_bytes + sel_bytes + basis, decode=dec + q_bytes + sel_bytes + out_bytes,
+                tail=tail + basis, step=score + dec + tail + q_bytes + sel_bytes + out_bytes + basis,
                 keys=keys + q_bytes + sel_bytes)
 
 
@@ -144,13 +150,15 @@ def prefill_summary(cfg, B, T, ms):
     the eigensolver here executes more (see executed_mflop_per_block).
     """
     L, d, r = 64, cfg.head_dim, cfg.rank
+    fd = cfg.subspace_dim or d                      # feature dimension of the Gram trick
     P = 16 if r <= 4 else 32
     full = B * cfg.num_kv_heads * (T // L)
     blocks = B * cfg.num_kv_heads * (-(-T // L))
-    method = 2 * L * L * d + 4 * L ** 3 / 3 + 2 * L * d * r
+    proj = 2 * L * d * fd if cfg.subspace_dim else 0    # Kc U_Q of the subspace factors
+    method = proj + 2 * L * L * fd + 4 * L ** 3 / 3 + 2 * L * fd * r
     # as built: Gram, 2 single + 10 double products Gamma W (23 with the last),
     # 12 re-orthonormalisations (Y^T Y and Y X^T), Rayleigh-Ritz, factors
-    executed = 2 * L * L * d + 23 * 2 * L * L * P + 12 * 4 * L * P * P + 2 * L * P * P + 2 * L * d * r
+    executed = proj + 2 * L * L * fd + 23 * 2 * L * L * P + 12 * 4 * L * P * P + 2 * L * P * P + 2 * L * fd * r
     kbytes = B * cfg.num_kv_heads * T * d * ESZ[cfg.kv_dtype] + blocks * cobs.record_bytes(cfg)
     return {"us": round(ms * 1e3, 1), "blocks": blocks, "full_blocks": full,
             "gflops": round(full * method / (ms * 1e-3) / 1e9, 1), "method_mflop_per_block": round(method / 1e6, 3),
@@ -301,13 +309,26 @@ def timed_steps(g_full, g_part, copies, k, stream):
     return start.elapsed_time(end) * 1e3
 
 
+SUBSPACE_DIM = 96
+
+
 def run_workload(name, args, dev, with_cpu):
-    """Every measurement of one workload; returns its result fields."""
-    prob = synth.make_problem(name, device=dev, steps=0)
+    """Every measurement of one workload; returns its result fields.  A name
+    ending in "ss" is the workload with subspace factors (Sec. 5.4) of
+    SUBSPACE_DIM elements and queries of the subspace law, U_Q the law's own
+    top directions."""
+    base = name[:-2] if name.endswith("ss") else name
+    prob = synth.make_problem(base, device=dev, steps=0)
     c = prob["cfg"]
+    sub = {}
+    if base != name:
+        G = c["Hq"] // c["Hkv"]
+        rot, sig = synth.query_rotation(c["Hkv"], c["d"], seed=synth.SEED_BASE + 90)
+        prob["q"] = synth.subspace_queries(rot, sig, c["B"], G, seed=synth.SEED_BASE + 91).to(dev)
+        sub = dict(subspace_dim=SUBSPACE_DIM, query_basis=rot[:, :, :SUBSPACE_DIM].contiguous().to(dev))
     cfg = cobs.Config(batch=c["B"], num_q_heads=c["Hq"], num_kv_heads=c["Hkv"], head_dim=c["d"],
                       max_seq_len=c["T_max"], rank=c["r"], budget=c["s"], window=c["w"],
-                      kv_dtype=c["kv_dtype"], mean_dtype=c["mean_dtype"], factor_dtype=c["factor_dtype"])
+                      kv_dtype=c["kv_dtype"], mean_dtype=c["mean_dtype"], factor_dtype=c["factor_dtype"], **sub)
     B, T_hi = c["B"], c["T"]
     t_lo = T_hi - CYCLE + 1
     seq_hi = torch.full((B,), T_hi, dtype=torch.int32, device=dev)
@@ -475,7 +496,8 @@ def run_workload(name, args, dev, with_cpu):
             "workload": f"{name}: B={B} Hq={c['Hq']} Hkv={c['Hkv']} d={c['d']} T={t_lo}..{T_hi} "
                         f"(decode loop, one block fill per {CYCLE} steps) L=64 r={c['r']} s={c['s']} "
                         f"w={c['w']}, K/V {c['kv_dtype']}, descriptors {c['mean_dtype']} mean / "
-                        f"{c['factor_dtype']} factors",
+                        f"{c['factor_dtype']} factors"
+                        + (f" of the {cfg.subspace_dim}-dim query subspace" if cfg.subspace_dim else ""),
             "bytes_per_step": round(ab["step"]),
             "layer_copies_rotated": copies,
             "fill_cycle_us": round(fill_cycle_us, 3),
@@ -510,7 +532,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2000)
     ap.add_argument("--warmup", type=int, default=200)
-    ap.add_argument("--workloads", default="c3,c2,c4,c5",
+    ap.add_argument("--workloads", default="c3,c2,c4,c5,c4ss",
                     help="comma-separated workloads; the first is the headline line")
     ap.add_argument("--copies", type=int, default=0, help="layer copies to rotate (0: >= 2 GB per sweep)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -537,9 +559,10 @@ def main():
         print("--steps must be >= 1 and --warmup >= 0", file=sys.stderr)
         sys.exit(2)
     names = [w.strip() for w in args.workloads.split(",") if w.strip()]
+    known = sorted(synth.CONFIGS) + [w + "ss" for w in sorted(synth.CONFIGS) if w != "c1"]
     for w in names:
-        if w not in synth.CONFIGS:
-            print(f"unknown workload {w}; choose from {sorted(synth.CONFIGS)}", file=sys.stderr)
+        if w not in known:
+            print(f"unknown workload {w}; choose from {known}", file=sys.stderr)
             sys.exit(2)
 
     dev = "cuda:0"

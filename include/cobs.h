@@ -250,7 +250,8 @@ cobs_status_t cobs_sparse_decode_branches(const cobs_config_t* cfg, const float*
  * cobs_build_block_stats on block (T-1)/L, cobs_select and cobs_sparse_decode.
  * With bf16 K/V, rank <= 4, L = 64 and full-space factors it is two launches
  * (the selector's workgroup that scores the newest block recomputes its record
- * first), else three (four with subspace factors: the query projection).
+ * first), else three (with subspace factors the newest block's build launch also
+ * writes U_Q^T q).
  *   summaries: in/out.   sel: optional device int32 [B, Hkv, budget] output.    */
 cobs_status_t cobs_decode_step(const cobs_config_t* cfg, const float* q, const cobs_kv_t* kv,
                                const int32_t* seq_lens, void* summaries, int32_t* sel,

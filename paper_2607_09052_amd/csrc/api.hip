@@ -167,8 +167,11 @@ cobs_status_t check_ws(void* ws, size_t ws_bytes, size_t need) {
 
 cobs_status_t hip_status(hipError_t e) { return e == hipSuccess ? COBS_OK : COBS_ERR_HIP; }
 
+// `q`, `qt` non-null (decode step, subspace factors): the launch also writes
+// the projected queries of every (b, h) to qt.
 cobs_status_t run_build(const Derived& v, const cobs_kv_t* kv, const int32_t* seq_lens, int first,
-                        int count, bool tail, void* summaries, hipStream_t st) {
+                        int count, bool tail, void* summaries, hipStream_t st, const float* q = nullptr,
+                        float* qt = nullptr) {
   BuildParams p;
   p.kv = make_view(kv, v);
   p.seq_lens = seq_lens;
@@ -187,6 +190,10 @@ cobs_status_t run_build(const Derived& v, const cobs_kv_t* kv, const int32_t* se
   p.lay = v.lay;
   p.basis = v.basis;
   p.fd = v.fd;
+  p.q = q;
+  p.qt = (v.basis && q && tail) ? qt : nullptr;
+  p.hq = v.hq;
+  p.g = v.G;
   if (!tail && count == 0) return COBS_OK;
   dim3 grid(tail ? 1 : count, v.hkv, v.B);
   return hip_status(launch_build(p, v.d, grid, st));
@@ -194,9 +201,11 @@ cobs_status_t run_build(const Derived& v, const cobs_kv_t* kv, const int32_t* se
 
 // `kv` non-null (decode step, bf16 K/V, r <= 4): the launch also recomputes
 // each row's newest block's record in these summaries before scoring it.
+// `qt_ready`: the projected queries of subspace factors are already in the
+// workspace (written by the decode step's build launch).
 cobs_status_t run_select(const Derived& v, const float* q, const void* summaries,
                          const int32_t* seq_lens, int32_t* sel, float* scores, uint8_t* ws,
-                         hipStream_t st, const cobs_kv_t* kv = nullptr) {
+                         hipStream_t st, const cobs_kv_t* kv = nullptr, bool qt_ready = false) {
   SelectParams p;
   p.tail_rec = kv ? static_cast<uint8_t*>(const_cast<void*>(summaries)) : nullptr;
   p.kv = kv ? make_view(kv, v) : KvView{};
@@ -226,6 +235,7 @@ cobs_status_t run_select(const Derived& v, const float* q, const void* summaries
   p.lay = v.lay;
   p.basis = v.basis;
   p.qt = v.basis ? reinterpret_cast<float*>(ws + v.sel_qt) : nullptr;
+  p.qt_ready = qt_ready ? 1 : 0;
   p.fd = v.fd;
   return hip_status(launch_select(p, v.d, v.G, v.B, st));
 }
@@ -262,6 +272,7 @@ cobs_status_t run_select_exact(const Derived& v, const float* q, const cobs_kv_t
   p.lay = v.lay;
   p.basis = nullptr;
   p.qt = nullptr;
+  p.qt_ready = 0;
   p.fd = v.fd;
   return hip_status(launch_select_exact(p, v.d, v.G, v.B, st, quest));
 }
@@ -318,8 +329,11 @@ cobs_status_t run_step(const Derived& v, const float* q, const cobs_kv_t* kv, co
     if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st, kv)) != COBS_OK) return s;
     return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
   }
-  if ((s = run_build(v, kv, seq_lens, 0, 0, true, summaries, st)) != COBS_OK) return s;
-  if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st)) != COBS_OK) return s;
+  // with subspace factors the build launch also projects the queries
+  float* qt = v.basis ? reinterpret_cast<float*>(wsb + v.sel_qt) : nullptr;
+  if ((s = run_build(v, kv, seq_lens, 0, 0, true, summaries, st, q, qt)) != COBS_OK) return s;
+  if ((s = run_select(v, q, summaries, seq_lens, selp, nullptr, wsb, st, nullptr, qt != nullptr)) != COBS_OK)
+    return s;
   return run_decode(v, q, kv, seq_lens, selp, out, lse, wsb + v.sel_bytes, st);
 }
 

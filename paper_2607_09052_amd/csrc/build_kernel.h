@@ -9,8 +9,15 @@ namespace cobs {
 
 template <int D, int P, int LB, bool KF32, bool SS>
 __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams p) {
-  __shared__ __align__(16) char pool[stats_lds_bytes<D, P, LB, KF32 || SS>()];
+  constexpr size_t kPool = stats_lds_bytes<D, P, LB, KF32 || SS>();
+  constexpr size_t kProj = SS ? sizeof(float) * kProjectLdsFloats : 0;
+  __shared__ __align__(16) char pool[kPool > kProj ? kPool : kProj];
   const int b = blockIdx.z, h = blockIdx.y;
+  // the decode step's build with subspace factors also projects the queries
+  // (the grid is one workgroup per (b, h) then, the condition uniform)
+  if constexpr (SS) {
+    if (p.qt) project_unit<D, kBuildThreads>(p.q, p.basis, p.qt, b, h, p.hq, p.g, p.fd, reinterpret_cast<float*>(pool));
+  }
   const int T = clamp_len(p.seq_lens[b], p.tmax);
   if (T <= 0) return;
   const int nb = (T + LB - 1) / LB;

@@ -114,6 +114,70 @@ __device__ __forceinline__ int64_t kv_offset(const KvView& kv, int b, int h, int
 
 __device__ __forceinline__ int clamp_len(int T, int tmax) { return T < 0 ? 0 : (T > tmax ? tmax : T); }
 
+// Projected queries U_Q^T q of Sec. 5.4 for the g <= 16 query heads of one
+// (batch row b, KV head h): qt[(b Hq + h g + i) FD + f] = sum_e q_i[e] U_h[e][f].
+// Called by all NT threads of a workgroup (three barriers inside).  The g
+// query rows are staged in `lds`; thread t takes column f = t % FD over the
+// D / PARTS rows of part t / FD (U_h read once, into registers, with
+// independent loads); the parts' partial sums meet in `lds` (after the
+// queries, g * PARTS * FD floats, at most 16 NT) and are added in part order.
+template <int D, int NT, int FD>
+__device__ __forceinline__ void project_unit_fd(const float* q, const float* basis, float* qt, int b, int h,
+                                                int hq, int g, float* lds) {
+  constexpr int PARTS = NT / FD, ROWS = D / PARTS;
+  static_assert(PARTS >= 1 && D % PARTS == 0 && ROWS % 4 == 0, "whole row parts");
+  const int t = threadIdx.x, f = t % FD, part = t / FD;
+  const bool live = part < PARTS;
+  const int e0 = (live ? part : 0) * ROWS;
+  const float* U = basis + ((int64_t)h * D + e0) * FD + f;
+  float u[ROWS];
+#pragma unroll
+  for (int e = 0; e < ROWS; ++e) u[e] = U[(int64_t)e * FD];
+  float* qs = lds;                       // [g][D]
+  lds += 16 * D;
+  const float4* qh = reinterpret_cast<const float4*>(q + ((int64_t)b * hq + (int64_t)h * g) * D);
+  for (int idx = t; idx < g * D / 4; idx += NT) reinterpret_cast<float4*>(qs)[idx] = qh[idx];
+  __syncthreads();
+  for (int i = 0; i < g; ++i) {
+    float a = 0.0f;
+#pragma unroll
+    for (int e = 0; e < ROWS; e += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(qs + i * D + e0 + e);
+      a += x.x * u[e];
+      a += x.y * u[e + 1];
+      a += x.z * u[e + 2];
+      a += x.w * u[e + 3];
+    }
+    if (live) lds[(i * PARTS + part) * FD + f] = a;
+  }
+  __syncthreads();
+  float* out = qt + ((int64_t)b * hq + (int64_t)h * g) * FD;
+  for (int idx = t; idx < g * FD; idx += NT) {
+    const int i = idx / FD, ff = idx % FD;
+    float s = 0.0f;
+#pragma unroll
+    for (int pp = 0; pp < PARTS; ++pp) s += lds[(i * PARTS + pp) * FD + ff];
+    out[(int64_t)i * FD + ff] = s;
+  }
+  __syncthreads();                       // `lds` is the caller's again
+}
+
+constexpr int kProjectLdsFloats = 16 * 128 + 16 * 256;   // project_unit's LDS at NT = 256
+
+// project_unit_fd for a subspace dimension fd in {32, 64, 96} below D.
+template <int D, int NT>
+__device__ __forceinline__ void project_unit(const float* q, const float* basis, float* qt, int b, int h, int hq,
+                                             int g, int fd, float* lds) {
+  static_assert(NT == 256, "LDS sized for 256 threads");
+  if constexpr (D == 128) {
+    if (fd == 32) project_unit_fd<128, NT, 32>(q, basis, qt, b, h, hq, g, lds);
+    else if (fd == 64) project_unit_fd<128, NT, 64>(q, basis, qt, b, h, hq, g, lds);
+    else project_unit_fd<128, NT, 96>(q, basis, qt, b, h, hq, g, lds);
+  } else {
+    project_unit_fd<D, NT, 32>(q, basis, qt, b, h, hq, g, lds);
+  }
+}
+
 // Blocks of 2^lsh tokens holding t tokens: ceil(t / L).
 __host__ __device__ __forceinline__ int blocks_of(int t, int lsh) { return (t + (1 << lsh) - 1) >> lsh; }
 

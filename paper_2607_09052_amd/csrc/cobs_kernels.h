@@ -16,6 +16,11 @@ struct BuildParams {
   RecLayout lay;
   const float* basis;   // subspace factors: U_Q [Hkv][d][fd] fp32; null: full space
   int fd;               // elements of a factor vector
+  // decode step with subspace factors: the workgroup of (b, h) also writes
+  // U_Q^T q of its query heads to qt (null: no projection)
+  const float* q;
+  float* qt;
+  int hq, g;
 };
 
 struct SelectParams {
@@ -37,6 +42,7 @@ struct SelectParams {
   // the factors; null for full-space factors
   const float* basis;
   float* qt;
+  int qt_ready;     // qt already written on this stream (the decode step's build launch)
   int fd;           // elements of a factor vector
   // decode step (bf16 K/V, r <= 4): the workgroup whose chunk holds a row's
   // newest block first recomputes that block's record in `tail_rec` (the same

@@ -13,21 +13,13 @@ SelectKernel select_mfma_kernel_for(const SelectParams& p, int d, int g);
 SelectKernel select_refresh_kernel_for(const SelectParams& p, int d, int g);
 SelectKernel select_ss_kernel_for(const SelectParams& p, int d, int g);
 
-// Projected queries U_Q^T q of Sec. 5.4 for every (batch row, query head): one
-// 128-thread workgroup each, thread f summing over the d elements in order.
-__global__ __launch_bounds__(128) void project_queries_kernel(const float* q, const float* basis, float* qt,
-                                                              int hq, int g, int d, int fd) {
-  __shared__ float qs[128];
-  const int64_t row = blockIdx.x;                  // b * Hq + query head
-  const int hk = (int)(row % hq) / g;
-  for (int e = threadIdx.x; e < d; e += 128) qs[e] = q[row * d + e];
-  __syncthreads();
-  const float* U = basis + (int64_t)hk * d * fd;
-  for (int f = threadIdx.x; f < fd; f += 128) {
-    float a = 0.0f;
-    for (int e = 0; e < d; ++e) a += qs[e] * U[(int64_t)e * fd + f];
-    qt[row * fd + f] = a;
-  }
+// Projected queries U_Q^T q of Sec. 5.4: one 256-thread workgroup per (KV
+// head, batch row).
+template <int D>
+__global__ __launch_bounds__(256) void project_queries_kernel(const float* q, const float* basis, float* qt,
+                                                              int hq, int g, int fd) {
+  __shared__ float lds[kProjectLdsFloats];
+  project_unit<D, 256>(q, basis, qt, blockIdx.y, blockIdx.x, hq, g, fd, lds);
 }
 
 bool select_on_matrix_cores(int mdt, int fdt) { return mdt != DT_F32 && fdt != DT_F32; }
@@ -62,9 +54,13 @@ hipError_t launch_select(SelectParams p, int d, int g, int batch, hipStream_t st
   bpw = std::max<int64_t>(base, (bpw + base - 1) / base * base);
   p.bpw = (int)std::min<int64_t>(bpw, ((int64_t)p.nbmax + base - 1) / base * base);
   p.nch = (p.nbmax + p.bpw - 1) / p.bpw;
-  if (ss) {
-    hipLaunchKernelGGL(project_queries_kernel, dim3((unsigned)(batch * p.hq)), dim3(128), 0, st, p.q, p.basis, p.qt,
-                       p.hq, g, d, p.fd);
+  if (ss && !p.qt_ready) {
+    if (d == 128)
+      hipLaunchKernelGGL(project_queries_kernel<128>, dim3((unsigned)p.hkv, (unsigned)batch), dim3(256), 0, st,
+                         p.q, p.basis, p.qt, p.hq, g, p.fd);
+    else
+      hipLaunchKernelGGL(project_queries_kernel<64>, dim3((unsigned)p.hkv, (unsigned)batch), dim3(256), 0, st,
+                         p.q, p.basis, p.qt, p.hq, g, p.fd);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
