@@ -201,6 +201,22 @@ def check_records(cfg, rec_unit, rec32_unit, K_unit, T, blocks=None, V_unit=None
         np.testing.assert_array_equal(got[j], want[j], err_msg=f"block {j}")
 
 
+def subspace_sigma_bound(ell, qg, U, factors, skews, c):
+    """Bound on |sigma_gpu - sigma_oracle| per block from the GPU's fp32
+    arithmetic: l_b^g summed in fp32 (a few ulps of |l|), and each
+    t = c xi . U^T q off by up to 1e-6 c |xi| |U^T q| (the projection and the
+    dot product in fp32), which moves (1/2) sum t^2 by sum |t| dt and the skew
+    term by sum |gamma| t^2 dt / 2; sigma_b takes the error of its own l_b^g
+    and of the normaliser ln Z^g, a weighted mean over all blocks."""
+    qf = qg @ U                                               # [G, s']
+    t = c * np.einsum("brf,gf->bgr", factors, qf)
+    dt = 1e-6 * c * np.linalg.norm(factors, axis=2)[:, None, :] * np.linalg.norm(qf, axis=1)[None, :, None]
+    dl = 4e-7 * np.abs(ell) + (np.abs(t) * dt).sum(axis=2)
+    if skews is not None:
+        dl += (np.abs(skews)[:, None, :] * t * t * dt).sum(axis=2) / 2
+    return SIGMA_TOL + dl.max(axis=1) + dl.max()
+
+
 def f32_config(cfg):
     """The same problem with fp32 mean and factor storage."""
     import dataclasses

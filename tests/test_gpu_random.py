@@ -6,8 +6,9 @@ selection, and the decode step against the three entry points.  A second draw
 takes contexts of up to 64k tokens (many selector chunks and decode workgroups
 per unit), a third checks the exact-mass and Quest selectors and the two-branch
 decode, and a fourth checks that a paged cache is bitwise the contiguous one.
-A fifth puts rows of length 0 beside the others.  COBS_RANDOM_SEEDS sets the
-number of seeds of each draw (default 24, 6, 8, 6 and 6) for a longer sweep."""
+A fifth puts rows of length 0 beside the others, a sixth draws subspace
+factors (Sec. 5.4).  COBS_RANDOM_SEEDS sets the number of seeds of each draw
+(default 24, 6, 8, 6, 6 and 8) for a longer sweep."""
 
 import os
 
@@ -20,7 +21,7 @@ from oracle import method as M
 from oracle import records as R
 from paper_2607_09052_amd import cobs
 from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_records, check_selection, f32_config, f64,
-                            oracle_decode, oracle_select, say, sync)
+                            oracle_decode, oracle_select, say, subspace_sigma_bound, sync)
 
 pytestmark = pytest.mark.gpu
 
@@ -98,15 +99,37 @@ def test_random_configuration_with_empty_rows(seed):
     _check(c, 13000 + seed, f"random config with empty rows {seed}")
 
 
+@pytest.mark.parametrize("seed", list(range(int(_N) if _N else 8)))
+def test_random_subspace_end_to_end(seed):
+    """Subspace factors: s' in {32, 64, 96} below d, U_Q the oracle's estimate
+    from a calibration sample of the subspace query law, queries of that law
+    (or i.i.d. Gaussian), bf16 / E2M1 descriptors, r in [1, 4]."""
+    c = _draw(14000 + seed)
+    rng = np.random.default_rng(15000 + seed)
+    c.update(md=["bf16", "e2m1"][int(rng.integers(2))], fd=["bf16", "e2m1"][int(rng.integers(2))],
+             r=int(rng.integers(1, 5)), sd=int(rng.choice([32, 64, 96] if c["d"] == 128 else [32])),
+             ssq=bool(rng.random() < 0.7))
+    _check(c, 16000 + seed, f"random subspace config {seed}")
+
+
 def _check(c, data_seed, tag):
     G, d, Hkv, B, tmax = c["G"], c["d"], c["Hkv"], c["B"], c["tmax"]
     say(f"{tag}: {c}")
     L = c.get("L", 64)
     prob = synth.make_problem("c2", seed=data_seed, B=B, Hq=G * Hkv, Hkv=Hkv, d=d, T=tmax, kv_dtype=c["kv"], L=L)
+    sub, U = {}, None
+    if c.get("sd"):
+        # U_Q per KV head: the oracle's estimate from 256 rows of the subspace law
+        rot, sig = synth.query_rotation(Hkv, d, data_seed + 1)
+        cal = synth.subspace_queries(rot, sig, 256, G, data_seed + 2)
+        U = np.stack([M.query_subspace(f64(cal[:, h * G:(h + 1) * G].reshape(-1, d)), c["sd"]) for h in range(Hkv)])
+        sub = dict(subspace_dim=c["sd"], query_basis=torch.from_numpy(U.astype(np.float32)).to(DEV))
+        if c["ssq"]:
+            prob["q"] = synth.subspace_queries(rot, sig, B, G, data_seed + 3)
     cfg = cobs.Config(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, head_dim=d, max_seq_len=tmax,
                       rank=c["r"], budget=c["s"], window=c["w"], kv_dtype=c["kv"], mean_dtype=c["md"],
                       factor_dtype=c["fd"], skew=c.get("skew", False), value_mean=c.get("vmean", False),
-                      block_size=L)
+                      block_size=L, **sub)
     q, k, v = prob["q"], prob["k"], prob["v"]
     qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
     seq_d = torch.from_numpy(c["seq"]).to(DEV)
@@ -148,9 +171,17 @@ def _check(c, data_seed, tag):
         blocks = None if nb <= 64 else sorted(set(range(0, nb, nb // 32)) | {nb - 2, nb - 1})
         for h in range(Hkv):
             gs = slice(h * G, (h + 1) * G)
-            check_records(cfg, rec_h[b, h], rec32_h[b, h], f64(k[b, h]), T, blocks, f64(v[b, h]))
-            sigma, nc, _ = oracle_select(rec_h[b, h], q[b, gs].double().numpy(), T, cfg)
-            assert np.all(np.abs(sc_h[b, h, :nc] - sigma[:nc]) <= SIGMA_TOL)
+            Uh = None if U is None else U[h]
+            check_records(cfg, rec_h[b, h], rec32_h[b, h], f64(k[b, h]), T, blocks, f64(v[b, h]), Uh)
+            sigma, nc, _ = oracle_select(rec_h[b, h], q[b, gs].double().numpy(), T, cfg, Uh)
+            tol = SIGMA_TOL
+            if Uh is not None and nc:
+                parts = R.decode(rec_h[b, h, :nb], d, cfg.rank, c["md"], c["fd"], cfg.skew, cfg.value_mean, c["sd"])
+                qg = q[b, gs].double().numpy()
+                ell = M.log_mass_estimate(qg, parts[0], parts[1], parts[2], cfg.scale,
+                                          parts[3] if cfg.skew else None, Uh)
+                tol = subspace_sigma_bound(ell, qg, Uh, parts[2], parts[3] if cfg.skew else None, cfg.scale)[:nc]
+            assert np.all(np.abs(sc_h[b, h, :nc] - sigma[:nc]) <= tol)
             assert np.all(np.isneginf(sc_h[b, h, nc:]))
             if c["s"] > 0:
                 check_selection(sel_h[b, h], sigma, nc, c["s"])
@@ -158,7 +189,7 @@ def _check(c, data_seed, tag):
             check_out(out_h[b, gs], lse_h[b, gs], o, l, c["kv"])
             if cfg.value_mean:
                 nb = -(-T // L)
-                parts = R.decode(rec_h[b, h, :nb], d, cfg.rank, c["md"], c["fd"], cfg.skew, True)
+                parts = R.decode(rec_h[b, h, :nb], d, cfg.rank, c["md"], c["fd"], cfg.skew, True, c.get("sd") or None)
                 o, l = M.compression_attention(q[b, gs].double().numpy(), parts[0], parts[1], parts[4], cfg.scale)
                 check_out(out_c[b, gs].cpu().numpy(), lse_c[b, gs].cpu().numpy(), o, l, "f32")
     assert torch.equal(rec1, rec)

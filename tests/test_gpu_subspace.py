@@ -18,8 +18,8 @@ import synth
 from oracle import method as M
 from oracle import records as R
 from paper_2607_09052_amd import cobs
-from tests.gpu_util import (DEV, SIGMA_TOL, check_records, check_selection, f32_config, f64, oracle_select, say,
-                            sync)
+from tests.gpu_util import (DEV, check_records, check_selection, f32_config, f64, oracle_select, say,
+                            subspace_sigma_bound, sync)
 
 pytestmark = pytest.mark.gpu
 
@@ -72,22 +72,6 @@ def test_subspace_build_matches_oracle(d, sd, L, kv, r, md, fd, skew, law):
                           U=U[h])
 
 
-def _sigma_bound(ell, qg, U, factors, skews, c):
-    """Bound on |sigma_gpu - sigma_oracle| per block from the GPU's fp32
-    arithmetic: l_b^g summed in fp32 (a few ulps of |l|), and each
-    t = c xi . U^T q off by up to 1e-6 c |xi| |U^T q| (the projection and the
-    dot product in fp32), which moves (1/2) sum t^2 by sum |t| dt and the skew
-    term by sum |gamma| t^2 dt / 2; sigma_b takes the error of its own l_b^g
-    and of the normaliser ln Z^g, a weighted mean over all blocks."""
-    qf = qg @ U                                               # [G, s']
-    t = c * np.einsum("brf,gf->bgr", factors, qf)
-    dt = 1e-6 * c * np.linalg.norm(factors, axis=2)[:, None, :] * np.linalg.norm(qf, axis=1)[None, :, None]
-    dl = 4e-7 * np.abs(ell) + (np.abs(t) * dt).sum(axis=2)
-    if skews is not None:
-        dl += (np.abs(skews)[:, None, :] * t * t * dt).sum(axis=2) / 2
-    return SIGMA_TOL + dl.max(axis=1) + dl.max()
-
-
 SELECT_CASES = [
     # d, s', G, L, mean, factor, skew, subspace-law queries
     (128, 96, 4, 64, "bf16", "e2m1", False, True),
@@ -132,7 +116,7 @@ def test_subspace_select_matches_oracle(d, sd, G, L, md, fd, skew, ssq):
             nb = M.num_blocks(Tb, L)
             parts = R.decode(rec[b, h, :nb].cpu().numpy(), d, r, md, fd, skew, False, sd)
             ell = M.log_mass_estimate(qg, parts[0], parts[1], parts[2], cfg.scale, parts[3] if skew else None, U[h])
-            tol = _sigma_bound(ell, qg, U[h], parts[2], parts[3] if skew else None, cfg.scale)[:nc]
+            tol = subspace_sigma_bound(ell, qg, U[h], parts[2], parts[3] if skew else None, cfg.scale)[:nc]
             err = np.abs(got[:nc] - sigma[:nc])
             assert np.all(err <= tol), float((err - tol).max())
             # the curvature term moves the scores: the first-order scores differ
