@@ -20,6 +20,8 @@
 // mean and zero factors.  LDS comes from a caller's pool of stats_lds_bytes().
 #pragma once
 
+#include <utility>
+
 #include <type_traits>
 
 #include "cobs_kernels.h"
@@ -75,7 +77,7 @@ __device__ __forceinline__ void store_vector_wave(const float* x, int len, int d
   }
   float m = 0.0f;
   for (int e = lane; e < len; e += 64) m = fmaxf(m, fabsf(x[e]));
-  const float scale = wave_max(m) / 6.0f;
+  const float scale = wave_max_rows(m) / 6.0f;
   if (lane == 0) *scale_dst = scale;
   for (int e = lane; e < len / 8; e += 64) {
     uint32_t w = 0;
@@ -84,6 +86,127 @@ __device__ __forceinline__ void store_vector_wave(const float* x, int len, int d
       for (int j = 0; j < 8; ++j) w |= e2m1_code(x[8 * e + j], scale) << (4 * j);
     }
     reinterpret_cast<uint32_t*>(dst)[e] = w;
+  }
+}
+
+// Value of lane c of each row of 16 lanes, to every lane of that row (DPP
+// row_newbcast; c a compile-time constant).
+template <int C>
+__device__ __forceinline__ float row_bcast(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), 0x150 + C, 0xf, 0xf, false));
+}
+
+template <int P>
+__device__ __forceinline__ void cholesky_inverse_lanes(const float* Sm, float* Lm, int lane);
+
+// Cholesky of the column-normalised S' = N S N (N = diag(S)^-1/2), S' = L L^T,
+// and X = L^-1, by one wave: lane k of each row of 16 lanes holds row k of L,
+// then column k of X (the four rows compute the same copy; entries pass
+// between lanes by row broadcasts); lanes 0..P-1 write N X^T to Lm (row stride
+// P + 1).  S is read from Sm (row stride P + 1).  A pivot of S' below 1e-6
+// (column k nearly inside the span of the earlier ones, whatever its length)
+// gives a zero column, so a direction of small eigenvalue is kept as long as
+// it is independent.  The basis only has to be well conditioned, so the
+// reciprocal square roots are the hardware's (about 1 ulp).
+template <int P>
+__device__ __forceinline__ void cholesky_inverse(const float* Sm, float* Lm, int lane) {
+  if constexpr (P != 16) {
+    cholesky_inverse_lanes<P>(Sm, Lm, lane);
+    return;
+  }
+  float row[P];
+  const int li = lane & 15;
+  const float dl = Sm[li * (P + 1) + li];
+  const float rnl = dl > 0.0f ? __builtin_amdgcn_rsqf(dl) : 0.0f;
+#pragma unroll
+  for (int c = 0; c < P; ++c) {
+    const float dc = Sm[c * (P + 1) + c];
+    const float rnc = dc > 0.0f ? __builtin_amdgcn_rsqf(dc) : 0.0f;
+    row[c] = Sm[li * (P + 1) + c] * rnl * rnc;
+  }
+  const float thr = 1e-6f;
+  float rdl = 0.0f;                      // 1 / L[li][li] (0 for a dropped column)
+  auto step = [&](auto kc) {
+    constexpr int k = decltype(kc)::value;
+    const float piv = row_bcast<k>(row[k]);
+    const bool ok = piv > thr;
+    const float rdk = ok ? __builtin_amdgcn_rsqf(piv) : 0.0f;
+    const float dk = piv * rdk;
+    rdl = (li == k) ? rdk : rdl;
+    const float lk = (li > k) ? row[k] * rdk : 0.0f;        // L[li][k], 0 on and above the diagonal
+    row[k] = (li == k) ? dk : ((li > k) ? lk : row[k]);
+    [&]<int... cs>(std::integer_sequence<int, cs...>) {
+      ((cs > k ? (void)(row[cs] -= lk * row_bcast<cs>(row[k])) : (void)0), ...);
+    }(std::make_integer_sequence<int, P>{});
+  };
+  [&]<int... ks>(std::integer_sequence<int, ks...>) {
+    (step(std::integral_constant<int, ks>{}), ...);
+  }(std::make_integer_sequence<int, P>{});
+  // X = L^-1 by forward substitution, lane c computing column c
+  float x[P];
+  auto fwd = [&](auto kc) {
+    constexpr int k = decltype(kc)::value;
+    float acc = (k == li) ? 1.0f : 0.0f;
+    [&]<int... ms>(std::integer_sequence<int, ms...>) {
+      ((ms < k ? (void)(acc -= row_bcast<k>(row[ms]) * x[ms]) : (void)0), ...);
+    }(std::make_integer_sequence<int, P>{});
+    x[k] = acc * row_bcast<k>(rdl);
+  };
+  [&]<int... ks>(std::integer_sequence<int, ks...>) {
+    (fwd(std::integral_constant<int, ks>{}), ...);
+  }(std::make_integer_sequence<int, P>{});
+  // W = Y N X^T: lane c stores X[k][c] N_cc at Lm[c][k]
+  if (lane < P) {
+#pragma unroll
+    for (int k = 0; k < P; ++k) Lm[lane * (P + 1) + k] = x[k] * rnl;
+  }
+}
+
+// The same for P = 32 (two rows of 16 lanes): lane k < P holds row k of L,
+// entries pass by lane reads into scalar registers.
+template <int P>
+__device__ __forceinline__ void cholesky_inverse_lanes(const float* Sm, float* Lm, int lane) {
+  float row[P], rn[P];
+  const int li = lane < P ? lane : 0;
+#pragma unroll
+  for (int c = 0; c < P; ++c) {
+    const float dc = Sm[c * (P + 1) + c];
+    rn[c] = dc > 0.0f ? 1.0f / sqrtf(dc) : 0.0f;
+  }
+  float rnl = rn[0];
+#pragma unroll
+  for (int c = 1; c < P; ++c) rnl = (c == li) ? rn[c] : rnl;
+#pragma unroll
+  for (int c = 0; c < P; ++c) row[c] = Sm[li * (P + 1) + c] * rnl * rn[c];
+  const float thr = 1e-6f;
+  float rd[P];
+#pragma unroll
+  for (int k = 0; k < P; ++k) {
+    const float piv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[k]), k));
+    const bool ok = piv > thr && piv > 0.0f;
+    const float dk = ok ? sqrtf(piv) : 0.0f;
+    const float rdk = ok ? 1.0f / dk : 0.0f;
+    rd[k] = rdk;
+    if (lane > k) row[k] *= rdk;
+    if (lane == k) row[k] = dk;
+#pragma unroll
+    for (int c = k + 1; c < P; ++c) {
+      const float lck = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[k]), c));
+      if (lane > k) row[c] -= row[k] * lck;
+    }
+  }
+  float x[P];
+#pragma unroll
+  for (int k = 0; k < P; ++k) {
+    float acc = (k == lane) ? 1.0f : 0.0f;
+#pragma unroll
+    for (int m = 0; m < k; ++m)
+      acc -= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[m]), k)) * x[m];
+    x[k] = acc * rd[k];
+  }
+  if (lane < P) {
+#pragma unroll
+    for (int k = 0; k < P; ++k) Lm[lane * (P + 1) + k] = x[k] * rnl;
   }
 }
 
@@ -361,57 +484,8 @@ __device__ __forceinline__ void block_stats(const StatsArgs& p, int b, int h, in
       }
       // ---- S = Y^T Y
       gram_pp(Yp, Yp, Sm);
-      // ---- Cholesky of the column-normalised S' = N S N (N = diag(S)^-1/2),
-      // S' = L L^T, and X = L^-1, in wave 0: lane k < P holds row k of L, then
-      // column k of X.  A pivot of S' below 1e-6 (column k nearly inside the
-      // span of the earlier ones, whatever its length) gives a zero column, so
-      // a direction of small eigenvalue is kept as long as it is independent.
-      if (wave == 0) {
-        float row[P], rn[P];
-        const int li = lane < P ? lane : 0;
-#pragma unroll
-        for (int c = 0; c < P; ++c) {
-          const float dc = Sm[c * (P + 1) + c];
-          rn[c] = dc > 0.0f ? 1.0f / sqrtf(dc) : 0.0f;
-        }
-        float rnl = rn[0];
-#pragma unroll
-        for (int c = 1; c < P; ++c) rnl = (c == li) ? rn[c] : rnl;
-#pragma unroll
-        for (int c = 0; c < P; ++c) row[c] = Sm[li * (P + 1) + c] * rnl * rn[c];
-        const float thr = 1e-6f;
-        float rd[P];
-#pragma unroll
-        for (int k = 0; k < P; ++k) {
-          const float piv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[k]), k));
-          const bool ok = piv > thr && piv > 0.0f;
-          const float dk = ok ? sqrtf(piv) : 0.0f;
-          const float rdk = ok ? 1.0f / dk : 0.0f;
-          rd[k] = rdk;
-          if (lane > k) row[k] *= rdk;
-          if (lane == k) row[k] = dk;
-#pragma unroll
-          for (int c = k + 1; c < P; ++c) {
-            const float lck = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[k]), c));
-            if (lane > k) row[c] -= row[k] * lck;
-          }
-        }
-        // X = L^-1 by forward substitution, lane c computing column c
-        float x[P];
-#pragma unroll
-        for (int k = 0; k < P; ++k) {
-          float acc = (k == lane) ? 1.0f : 0.0f;
-#pragma unroll
-          for (int m = 0; m < k; ++m)
-            acc -= __int_as_float(__builtin_amdgcn_readlane(__float_as_int(row[m]), k)) * x[m];
-          x[k] = acc * rd[k];
-        }
-        // W = Y N X^T: lane c stores X[k][c] N_cc at Lm[c][k]
-        if (lane < P) {
-#pragma unroll
-          for (int k = 0; k < P; ++k) Lm[lane * (P + 1) + k] = x[k] * rnl;
-        }
-      }
+      // ---- Cholesky-QR: N X^T of S = Y^T Y in wave 0
+      if (wave == 0) cholesky_inverse<P>(Sm, Lm, lane);
       __syncthreads();
       // ---- W = Y (N X^T): operand B[k][c] = Lm[k][c]
 #pragma unroll

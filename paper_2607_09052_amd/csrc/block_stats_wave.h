@@ -1,0 +1,661 @@
+// Block statistics of one block by one wave (Sec. 5.3, Gram trick of
+// Sec. 5.6, storage of Sec. 5.5), for blocks of LB = 32 or 64 tokens with
+// rank r <= 4 and full-space factors: the method and the arithmetic of
+// block_stats (16 power-iteration columns), laid out so that a wave needs no
+// workgroup barrier and several blocks stream through a CU at once.
+//
+//   * Lane (lk, lr) = (lane / 16, lane % 16) reads rows 16 t + lr of the block
+//     and the d / 4 columns [lk d/4, (lk+1) d/4), first for the column means
+//     (fp64 sums, reduced over the 16 lanes of a row group), then again,
+//     centred, as the operands of the Gram matrix: at k-step (chunk, e) lane
+//     group lk contributes column lk d/4 + 8 chunk + e, for every row tile as
+//     both A and B operand of v_mfma_f32_16x16x4_f32.
+//   * The Gram matrix stays in registers in the MFMA result layout:
+//     g[t][u][v] = Gamma[16 t + 4 lk + v][16 u + lr].  By symmetry that is the
+//     A operand of Gamma W with the contraction index 16 a + 4 lk + v, and the
+//     result of a product is the B operand of the next one, so the power
+//     iteration's products need no LDS.  Y^T Y takes the same registers as
+//     both operands.  Only the re-orthonormalisation W = Y N X^T (the
+//     Cholesky of cholesky_inverse), the Rayleigh-Ritz matrix, Jacobi and
+//     the factors go through the wave's LDS.
+//   * Factors: lane l owns columns (d / 64) l .. of xi and reads those columns
+//     of every key (a second pass over the block in L2).
+#pragma once
+
+#include "block_stats.h"
+
+namespace cobs {
+
+// The record of a block by one wave: the header (count; scales and skew
+// coefficients default 0), then, once those stores are done, every stored
+// vector (mean, nr factors from Xi, value mean) and zeros up to the record size.
+template <int D>
+__device__ __forceinline__ void write_record_wave(const StatsArgs& p, uint8_t* R, int n, int nr, const float* mean,
+                                                  const float* Xi, const float* vmean, const float* skw, int lane) {
+  const RecLayout lay = p.lay;
+  for (int idx = lane; idx < lay.mean_off / 4; idx += 64)
+    reinterpret_cast<uint32_t*>(R)[idx] = (idx == 0) ? (uint32_t)n : 0u;
+  __builtin_amdgcn_s_waitcnt(0);
+  if (nr > 0 && p.skew && lane < nr) reinterpret_cast<float*>(R + lay.skew_off)[lane] = skw[lane];
+  store_vector_wave(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), lane);
+  for (int vi = 0; vi < nr; ++vi)
+    store_vector_wave(&Xi[vi * D], D, p.fdt, R + lay.fac_off + vi * lay.vec_bytes,
+                      reinterpret_cast<float*>(R + 16) + vi, lane);
+  if (p.vmean) store_vector_wave(vmean, D, p.mdt, R + lay.vmean_off, reinterpret_cast<float*>(R + 8), lane);
+  // factors of a block without them, and the padding after the last vector
+  const int fac_end = lay.fac_off + nr * lay.vec_bytes;
+  for (int idx = fac_end / 4 + lane; idx < lay.vmean_off / 4; idx += 64) reinterpret_cast<uint32_t*>(R)[idx] = 0u;
+  const int end = lay.vmean_off + (p.vmean ? lay.mean_bytes : 0);
+  for (int idx = end / 4 + lane; idx < lay.total / 4; idx += 64) reinterpret_cast<uint32_t*>(R)[idx] = 0u;
+}
+
+// LDS of one wave (16-byte aligned pieces).
+template <int D, int LB>
+struct WaveStatsLds {
+  static constexpr int P = 16, PS = P + 1;
+  static constexpr size_t al(size_t x) { return (x + 15) / 16 * 16; }
+  static constexpr size_t mean = 0;                        // [D]
+  static constexpr size_t vmean = al(mean + 4 * D);        // [D]
+  static constexpr size_t yp = al(vmean + 4 * D);          // [LB][PS]: Y, then W, by rows
+  static constexpr size_t sm = al(yp + 4 * LB * PS);       // [P][PS]
+  static constexpr size_t lm = al(sm + 4 * P * PS);        // [P][PS]
+  static constexpr size_t hm = al(lm + 4 * P * PS);        // [2][P][PS]
+  static constexpr size_t vm = al(hm + 8 * P * PS);        // [2][P][PS]
+  static constexpr size_t wr = al(vm + 8 * P * PS);        // [4][LB] Ritz vectors
+  static constexpr size_t xi = al(wr + 4 * 4 * LB);        // [4][D] factors
+  static constexpr size_t jac = al(xi + 4 * 4 * D);        // Jacobi rotations: c, s per pair [P/2][2]
+  static constexpr size_t misc = al(jac + 4 * 3 * P);      // order[4], ritz[4], skew[4], trace
+  static constexpr size_t bytes = al(misc + 4 * 16);
+};
+
+template <int D, int LB>
+constexpr size_t wave_stats_lds_bytes() { return WaveStatsLds<D, LB>::bytes; }
+
+// The configurations block_stats_wave covers.
+__host__ __device__ inline bool wave_stats_applies(int r, int lsh, bool subspace) {
+  return r <= 4 && (lsh == 5 || lsh == 6) && !subspace;
+}
+
+// One block by the calling wave (lane = threadIdx.x % 64; every lane of the
+// wave calls it; no workgroup barrier inside).  `pool`: the wave's
+// wave_stats_lds_bytes<D, LB>() bytes of LDS.
+template <int D, int LB, bool KF32>
+__device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int h, int j, int n, char* pool) {
+  static_assert(LB == 32 || LB == 64, "blocks of 32 or 64 tokens");
+  static_assert(D == 64 || D == 128, "d = 64 or 128");
+  using Lay = WaveStatsLds<D, LB>;
+  constexpr int P = Lay::P, PS = Lay::PS;
+  constexpr int NT16 = LB / 16;                 // 16-row tiles of the block
+  constexpr int CPL = D / 4;                    // columns of a lane group
+  constexpr int NCH = CPL / 8;                  // 8-column chunks of a lane group
+  constexpr int EPL = D / 64;                   // factor columns of a lane
+  float* mean = reinterpret_cast<float*>(pool + Lay::mean);
+  float* vmean = reinterpret_cast<float*>(pool + Lay::vmean);
+  float* Yp = reinterpret_cast<float*>(pool + Lay::yp);
+  float* Sm = reinterpret_cast<float*>(pool + Lay::sm);
+  float* Lm = reinterpret_cast<float*>(pool + Lay::lm);
+  float (*Hm)[P * PS] = reinterpret_cast<float (*)[P * PS]>(pool + Lay::hm);
+  float (*Vm)[P * PS] = reinterpret_cast<float (*)[P * PS]>(pool + Lay::vm);
+  float* Wr = reinterpret_cast<float*>(pool + Lay::wr);
+  float* Xi = reinterpret_cast<float*>(pool + Lay::xi);
+  float* rot = reinterpret_cast<float*>(pool + Lay::jac);
+  int* order = reinterpret_cast<int*>(pool + Lay::misc);
+  float* ritzval = reinterpret_cast<float*>(pool + Lay::misc) + 4;
+  float* skw = reinterpret_cast<float*>(pool + Lay::misc) + 8;
+
+  const int lane = threadIdx.x & 63, lr = lane & 15, lk = lane >> 4;
+  const int r = p.r;
+
+  // 8 columns lk CPL + 8 q .. + 7 of rows 16 t + lr (zero past the block's n
+  // rows), as raw words (the loads in flight) and then as floats
+  struct Raw {
+    uint4 w[KF32 ? 2 : 1];
+  };
+  int64_t roff[NT16];                           // row offsets, -1: no row
+#pragma unroll
+  for (int t = 0; t < NT16; ++t) {
+    const int i = 16 * t + lr;
+    roff[t] = (i < n) ? kv_offset(p.kv, b, h, j * LB + i) : -1;
+  }
+  auto load_raw = [&](const void* base, int q, Raw* raw) {
+#pragma unroll
+    for (int t = 0; t < NT16; ++t) {
+      if (roff[t] >= 0) {
+        if constexpr (KF32) {
+          const uint4* src = reinterpret_cast<const uint4*>(static_cast<const float*>(base) + roff[t] + lk * CPL + 8 * q);
+          raw[t].w[0] = src[0];
+          raw[t].w[1] = src[1];
+        } else {
+          raw[t].w[0] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + roff[t] + lk * CPL + 8 * q);
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < (KF32 ? 2 : 1); ++k) raw[t].w[k] = make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+  };
+  auto unpack = [&](const Raw* raw, float (*x)[8]) {
+#pragma unroll
+    for (int t = 0; t < NT16; ++t) {
+      if constexpr (KF32) {
+        const uint4 a = raw[t].w[0], c = raw[t].w[1];
+        x[t][0] = __uint_as_float(a.x); x[t][1] = __uint_as_float(a.y);
+        x[t][2] = __uint_as_float(a.z); x[t][3] = __uint_as_float(a.w);
+        x[t][4] = __uint_as_float(c.x); x[t][5] = __uint_as_float(c.y);
+        x[t][6] = __uint_as_float(c.z); x[t][7] = __uint_as_float(c.w);
+      } else {
+        const uint4 a = raw[t].w[0];
+        x[t][0] = bf16_lo(a.x); x[t][1] = bf16_hi(a.x); x[t][2] = bf16_lo(a.y); x[t][3] = bf16_hi(a.y);
+        x[t][4] = bf16_lo(a.z); x[t][5] = bf16_hi(a.z); x[t][6] = bf16_lo(a.w); x[t][7] = bf16_hi(a.w);
+      }
+    }
+  };
+  // column means into LDS: fp64 sums (exact for the block's fp32 values unless
+  // their magnitudes span > 2^29), one rounding to fp32, so a block of
+  // identical rows centres to exact zeros
+  auto column_mean = [&](const Raw (*raw)[NT16], float* out) {
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) {
+      float x[NT16][8];
+      unpack(raw[q], x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        double cs = 0.0;
+#pragma unroll
+        for (int t = 0; t < NT16; ++t) cs += (double)x[t][e];
+        cs = row16_sum_last(cs);
+        if (lr == 15) out[lk * CPL + 8 * q + e] = (float)(cs / (double)n);
+      }
+    }
+    wave_lds_sync();
+  };
+  // the keys' words stay in registers for the Gram matrix (bf16 keys)
+  Raw kraw[NCH][NT16];
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) load_raw(p.kv.k, q, kraw[q]);
+  column_mean(kraw, mean);
+  if (p.vmean) {
+    Raw vraw[NCH][NT16];
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) load_raw(p.kv.v, q, vraw[q]);
+    column_mean(vraw, vmean);
+  }
+
+  const bool factors = (n == LB) && (r > 0);
+  uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
+  if (factors) {
+    // ---- Gram matrix Kc Kc^T: g[t][u][v] = Gamma[16 t + 4 lk + v][16 u + lr]
+    f32x4_t g[NT16][NT16];
+#pragma unroll
+    for (int t = 0; t < NT16; ++t)
+#pragma unroll
+      for (int u = 0; u < NT16; ++u) g[t][u] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    // bf16 keys: the words of the mean pass; fp32 keys: loaded again, chunk
+    // q + 1 in flight while chunk q is multiplied
+    Raw rcur[NT16], rnext[NT16];
+    if constexpr (KF32) load_raw(p.kv.k, 0, rnext);
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) {
+      if constexpr (KF32) {
+#pragma unroll
+        for (int t = 0; t < NT16; ++t) rcur[t] = rnext[t];
+        if (q + 1 < NCH) load_raw(p.kv.k, q + 1, rnext);
+      } else {
+#pragma unroll
+        for (int t = 0; t < NT16; ++t) rcur[t] = kraw[q][t];
+      }
+      float x[NT16][8];
+      unpack(rcur, x);
+      const float4 m0 = *reinterpret_cast<const float4*>(mean + lk * CPL + 8 * q);
+      const float4 m1 = *reinterpret_cast<const float4*>(mean + lk * CPL + 8 * q + 4);
+      const float mm[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+#pragma unroll
+      for (int t = 0; t < NT16; ++t)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[t][e] -= mm[e];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int t = 0; t < NT16; ++t)
+#pragma unroll
+          for (int u = 0; u < NT16; ++u)
+            g[t][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[t][e], x[u][e], g[t][u], 0, 0, 0);
+    }
+    float diag = 0.0f;
+#pragma unroll
+    for (int t = 0; t < NT16; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (4 * lk + v == lr) diag += g[t][t][v];
+    // The products use Gamma / trace(Gamma), eigenvalues in [0, 1], so that the
+    // fourth powers in Y^T Y stay far from the fp32 range at any key scale.
+    const float trace = wave_sum_rows(diag);
+    const float gsc = trace > 0.0f ? 1.0f / trace : 0.0f;
+
+    // Gamma as three bf16 parts (hi + mid + lo = the fp32 value) in the bf16
+    // matrix-core operand layout: for output tile t and k-chunk c, lane group
+    // lk supplies the contraction indices 16 a + 4 lk + v, a in {2c, 2c + 1}
+    constexpr int KC = NT16 / 2;                  // 32-index k-chunks
+    sbf16x8_t gp[3][NT16][KC];
+#pragma unroll
+    for (int t = 0; t < NT16; ++t)
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float x = g[2 * c + i / 4][t][i % 4];
+#pragma unroll
+          for (int part = 0; part < 3; ++part) {
+            const uint32_t hb = f32_to_bf16_rne(x);
+            gp[part][t][c][i] = __builtin_bit_cast(__bf16, (uint16_t)hb);
+            x -= __uint_as_float(hb << 16);
+          }
+        }
+    // dst = (Gamma / trace) src, both in the result layout: row 16 t + 4 lk + v,
+    // column lr.  The power iteration's products take the three leading
+    // cross terms of the bf16 parts (relative error ~1e-5, which the iteration
+    // absorbs); the last one (exact) feeds the Rayleigh-Ritz step and takes
+    // all terms down to 2^-24.
+    auto product = [&](const f32x4_t* src, f32x4_t* dst, bool exact) {
+      sbf16x8_t wp[3][KC];
+#pragma unroll
+      for (int c = 0; c < KC; ++c)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float x = src[2 * c + i / 4][i % 4];
+#pragma unroll
+          for (int part = 0; part < 3; ++part) {
+            const uint32_t hb = f32_to_bf16_rne(x);
+            wp[part][c][i] = __builtin_bit_cast(__bf16, (uint16_t)hb);
+            x -= __uint_as_float(hb << 16);
+          }
+        }
+#pragma unroll
+      for (int t = 0; t < NT16; ++t) {
+        f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int c = 0; c < KC; ++c) {
+          if (exact) {
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[2][t][c], wp[0][c], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[1][t][c], wp[1][c], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[0][t][c], wp[2][c], acc, 0, 0, 0);
+          }
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[1][t][c], wp[0][c], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[0][t][c], wp[1][c], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[0][t][c], wp[0][c], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) dst[t][v] = acc[v] * gsc;
+      }
+    };
+    // X^T Y (P x P) into out (row stride PS), X and Y in the result layout
+    auto small_gram = [&](const f32x4_t* X, const f32x4_t* Y, float* out) {
+      f32x4_t acc0 = {0.0f, 0.0f, 0.0f, 0.0f}, acc1 = acc0;
+#pragma unroll
+      for (int t = 0; t < NT16; ++t)
+#pragma unroll
+        for (int v = 0; v < 4; v += 2) {
+          acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(X[t][v], Y[t][v], acc0, 0, 0, 0);
+          acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(X[t][v + 1], Y[t][v + 1], acc1, 0, 0, 0);
+        }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) out[(4 * lk + v) * PS + lr] = acc0[v] + acc1[v];
+    };
+    // rows of a result-layout matrix into Yp (row stride PS)
+    auto to_rows = [&](const f32x4_t* X) {
+#pragma unroll
+      for (int t = 0; t < NT16; ++t)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) Yp[(16 * t + 4 * lk + v) * PS + lr] = X[t][v];
+    };
+
+    f32x4_t w[NT16], y[NT16];
+#pragma unroll
+    for (int a = 0; a < NT16; ++a)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) w[a][v] = init_sign(16 * a + 4 * lk + v, lr);
+#pragma unroll 1
+    for (int it = 0; it <= kPowerIters; ++it) {
+      product(w, y, it == kPowerIters);
+      if (it == kPowerIters) break;      // the last product feeds the Rayleigh-Ritz step
+      if (it >= kSinglePowerIters) {       // Gamma^2 W (W is replaced below)
+        product(y, w, false);
+#pragma unroll
+        for (int t = 0; t < NT16; ++t) y[t] = w[t];
+      }
+      // ---- W = Y N X^T, the Cholesky-QR of Y
+      small_gram(y, y, Sm);
+      to_rows(y);
+      wave_lds_sync();
+      cholesky_inverse<P>(Sm, Lm, lane);
+      wave_lds_sync();
+#pragma unroll
+      for (int t = 0; t < NT16; ++t) {
+        f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int k0 = 0; k0 < P; k0 += 4)
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(Yp[(16 * t + lr) * PS + k0 + lk], Lm[(k0 + lk) * PS + lr], acc,
+                                                    0, 0, 0);
+        w[t] = acc;
+      }
+      wave_lds_sync();                   // Yp, Sm and Lm are rewritten by the next iteration
+    }
+
+    // ---- Rayleigh-Ritz: H = W^T (Gamma W), symmetrised; V = I
+    small_gram(w, y, Sm);
+    to_rows(w);                          // W by rows, for the Ritz vectors
+    wave_lds_sync();
+#pragma unroll
+    for (int k = 0; k < P * P / 64; ++k) {
+      const int idx = lane + 64 * k, a = idx / P, c = idx % P;
+      Hm[0][a * PS + c] = 0.5f * (Sm[a * PS + c] + Sm[c * PS + a]);
+      Vm[0][a * PS + c] = (a == c) ? 1.0f : 0.0f;
+    }
+    wave_lds_sync();
+    // ---- eigenpairs of H by parallel cyclic Jacobi (round-robin pairing,
+    // index 0 fixed).  In round rnd slot m in [0, P) holds index 0 (m = 0) or
+    // 1 + (m - 1 + rnd) mod (P - 1), and slots m and P - 1 - m form a pair.
+    // H and V^T stay in registers in the MFMA result layout (element
+    // [4 lk + v][lr]); a round is H <- J^T (H J) and V^T <- J^T V^T, twelve
+    // matrix-core products, with J (the round's eight rotations) built in the
+    // same layout.  By symmetry H's layout is also the A operand of H J.
+    // Lanes < P/2 form the rotations from H's entries, passed through LDS.
+    // bf16 keys: the factor pass's words (the lane's EPL columns of every row)
+    // load during Jacobi, which does not touch memory
+    uint32_t xraw[KF32 ? 1 : LB];
+    if constexpr (!KF32) {
+#pragma unroll
+      for (int row = 0; row < LB; ++row) {
+        const int64_t off0 = kv_offset(p.kv, b, h, j * LB + row);   // -1: a page outside the pool (zero keys)
+        const uint16_t* src = static_cast<const uint16_t*>(p.kv.k) + (off0 < 0 ? 0 : off0) + EPL * lane;
+        if (off0 < 0) xraw[row] = 0u;
+        else if constexpr (EPL == 2) xraw[row] = *reinterpret_cast<const uint32_t*>(src);
+        else xraw[row] = *src;
+      }
+    }
+    auto slot_index = [&](int m, int rnd) { return m == 0 ? 0 : 1 + (m - 1 + rnd) % (P - 1); };
+    auto index_slot = [&](int x, int rnd) { return x == 0 ? 0 : 1 + (x - 1 + (P - 1) - rnd) % (P - 1); };
+    f32x4_t hr, vt;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      hr[v] = Hm[0][(4 * lk + v) * PS + lr];
+      vt[v] = (4 * lk + v == lr) ? 1.0f : 0.0f;
+    }
+#pragma unroll 1
+    for (int sweep = 0; sweep < kJacobiSweeps; ++sweep) {
+      bool moved = false;
+#pragma unroll 1
+      for (int rnd = 0; rnd < P - 1; ++rnd) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) Hm[0][(4 * lk + v) * PS + lr] = hr[v];
+        wave_lds_sync();
+        bool big = false;
+        if (lane < P / 2) {
+          const int x = slot_index(lane, rnd), yy = slot_index(P - 1 - lane, rnd);
+          const int pp = min(x, yy), qq = max(x, yy);
+          const float app = Hm[0][pp * PS + pp], aqq = Hm[0][qq * PS + qq], apq = Hm[0][pp * PS + qq];
+          big = fabsf(apq) > 1e-6f * sqrtf(fmaxf(app, 0.0f) * fmaxf(aqq, 0.0f)) && fabsf(apq) > 2e-8f;
+          float c = 1.0f, sn = 0.0f;
+          if (apq != 0.0f) {
+            const float th = (aqq - app) * __builtin_amdgcn_rcpf(2.0f * apq);
+            const float tt = (th >= 0.0f ? 1.0f : -1.0f) * __builtin_amdgcn_rcpf(fabsf(th) + sqrtf(th * th + 1.0f));
+            c = __builtin_amdgcn_rsqf(tt * tt + 1.0f);
+            sn = tt * c;
+          }
+          rot[2 * lane] = c;
+          rot[2 * lane + 1] = sn;
+        }
+        moved = moved || __ballot(big) != 0;
+        wave_lds_sync();
+        // J[x][y]: c on the diagonal; at y = partner(x), -s if y < x else s
+        f32x4_t jr;
+        {
+          const int my = index_slot(lr, rnd), mpy = P - 1 - my;
+          const int py = slot_index(mpy, rnd);
+          const int pr = min(my, mpy);
+          const float c = rot[2 * pr], sn = rot[2 * pr + 1];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int x = 4 * lk + v;
+            jr[v] = (x == lr) ? c : ((x == py) ? ((lr < x) ? -sn : sn) : 0.0f);
+          }
+        }
+        f32x4_t m4 = {0.0f, 0.0f, 0.0f, 0.0f}, h2 = m4, v2 = m4;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) m4 = __builtin_amdgcn_mfma_f32_16x16x4f32(hr[v], jr[v], m4, 0, 0, 0);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          h2 = __builtin_amdgcn_mfma_f32_16x16x4f32(jr[v], m4[v], h2, 0, 0, 0);
+          v2 = __builtin_amdgcn_mfma_f32_16x16x4f32(jr[v], vt[v], v2, 0, 0, 0);
+        }
+        hr = h2;
+        vt = v2;
+      }
+      if (!moved) break;
+    }
+    // the eigenvalues on H's diagonal, V = (V^T)^T by rows, for the ranking and the Ritz vectors
+    const int cw = 0;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      Hm[0][(4 * lk + v) * PS + lr] = hr[v];
+      Vm[0][lr * PS + 4 * lk + v] = vt[v];
+    }
+    wave_lds_sync();
+    // ---- top-r Ritz values, descending, ties to the lower index (rank by counting)
+    if (lane < P) {
+      const float ta = Hm[cw][lane * PS + lane];
+      int rank = 0;
+      for (int c = 0; c < P; ++c) {
+        const float tc = Hm[cw][c * PS + c];
+        rank += (tc > ta) || (tc == ta && c < lane);
+      }
+      if (rank < r) { order[rank] = lane; ritzval[rank] = ta; }
+    }
+    wave_lds_sync();
+    // Ritz vectors w_i = W V[:, order_i], lane = row
+    if (lane < LB) {
+      for (int i = 0; i < r; ++i) {
+        const int col = order[i];
+        float s = 0.0f;
+#pragma unroll
+        for (int a = 0; a < P; ++a) s += Yp[lane * PS + a] * Vm[cw][a * PS + col];
+        Wr[i * LB + lane] = s;
+      }
+    }
+    wave_lds_sync();
+    // xi_i = Kc^T w_i / sqrt(n): lane l owns columns EPL l .. EPL l + EPL - 1
+    const float rs = 1.0f / sqrtf((float)n);
+    const float top = ritzval[0];
+    {
+      float xs[4][EPL];
+      float mc[EPL];
+#pragma unroll
+      for (int c = 0; c < EPL; ++c) mc[c] = mean[EPL * lane + c];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int c = 0; c < EPL; ++c) xs[i][c] = 0.0f;
+      if constexpr (!KF32) {
+#pragma unroll
+        for (int r4 = 0; r4 < LB; r4 += 4) {
+          float4 w4[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            w4[i] = (i < r) ? *reinterpret_cast<const float4*>(Wr + i * LB + r4) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int row = r4 + rr;
+            float kx[EPL];
+            if constexpr (EPL == 2) {
+              kx[0] = bf16_lo(xraw[row]);
+              kx[1] = bf16_hi(xraw[row]);
+            } else {
+              kx[0] = bf16_lo(xraw[row]);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float wi = rr == 0 ? w4[i].x : rr == 1 ? w4[i].y : rr == 2 ? w4[i].z : w4[i].w;
+#pragma unroll
+              for (int c = 0; c < EPL; ++c) xs[i][c] += (kx[c] - mc[c]) * wi;
+            }
+          }
+        }
+      }
+      // fp32 keys: the lane's columns of 16 rows at a time, their loads in flight together
+#pragma unroll 1
+      for (int r0 = 0; KF32 && r0 < LB; r0 += 16) {
+        float kv_[16][EPL];
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+          const int64_t off0 = kv_offset(p.kv, b, h, j * LB + r0 + rr);   // -1: a page outside the pool (zero keys)
+          const int64_t off = (off0 < 0 ? 0 : off0) + EPL * lane;
+          if (off0 < 0) {
+#pragma unroll
+            for (int c = 0; c < EPL; ++c) kv_[rr][c] = 0.0f;
+          } else if constexpr (KF32) {
+            if constexpr (EPL == 2) {
+              const float2 a = *reinterpret_cast<const float2*>(static_cast<const float*>(p.kv.k) + off);
+              kv_[rr][0] = a.x; kv_[rr][1] = a.y;
+            } else {
+              kv_[rr][0] = static_cast<const float*>(p.kv.k)[off];
+            }
+          } else {
+            if constexpr (EPL == 2) {
+              const uint32_t a = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(p.kv.k) + off);
+              kv_[rr][0] = bf16_lo(a); kv_[rr][1] = bf16_hi(a);
+            } else {
+              kv_[rr][0] = __uint_as_float((uint32_t)static_cast<const uint16_t*>(p.kv.k)[off] << 16);
+            }
+          }
+        }
+#pragma unroll
+        for (int rr = 0; rr < 16; ++rr) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float wi = (i < r) ? Wr[i * LB + r0 + rr] : 0.0f;
+#pragma unroll
+            for (int c = 0; c < EPL; ++c) xs[i][c] += (kv_[rr][c] - mc[c]) * wi;
+          }
+        }
+      }
+      // sign: the largest-magnitude entry positive (lowest index on ties): the
+      // lane's first largest entry, the wave's largest magnitude, the lowest
+      // lane holding it
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (i >= r) break;
+        const bool keep = ritzval[i] > 1e-6f * top && top > 0.0f;
+        float best = -1.0f, sbest = 0.0f;
+#pragma unroll
+        for (int c = 0; c < EPL; ++c) {
+          xs[i][c] = keep ? xs[i][c] * rs : 0.0f;
+          const float a = fabsf(xs[i][c]);
+          if (a > best) { best = a; sbest = xs[i][c]; }
+        }
+        const float m = wave_max_rows(best);
+        const uint64_t holders = __ballot(best == m);
+        const int src = (int)__builtin_ctzll(holders);
+        const float pivot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sbest), src));
+#pragma unroll
+        for (int c = 0; c < EPL; ++c) Xi[i * D + EPL * lane + c] = (pivot < 0.0f) ? -xs[i][c] : xs[i][c];
+      }
+    }
+    wave_lds_sync();
+    if (p.skew) {
+      // skew coefficient of factor i (lane t = token t): gamma_i = (1/n) sum_t
+      // z_t^3 with z_t = (xi_i . kc_t) / |xi_i|^2, the projection on u_i
+      // standardised by its deviation; the r projections of a token together
+      float lam[4], pr[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float nrm = 0.0f;
+        if (i < r) {
+#pragma unroll
+          for (int c = 0; c < EPL; ++c) nrm += Xi[i * D + EPL * lane + c] * Xi[i * D + EPL * lane + c];
+        }
+        lam[i] = wave_sum_rows(nrm);
+        pr[i] = 0.0f;
+      }
+      if (lane < LB) {
+        const int64_t off0 = kv_offset(p.kv, b, h, j * LB + lane);
+        const int64_t off = off0 < 0 ? 0 : off0;
+#pragma unroll 1
+        for (int e0 = 0; e0 < D; e0 += 8) {
+          float kk[8];
+          if (off0 < 0) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) kk[e] = 0.0f;
+          } else if constexpr (KF32) {
+            const float4* src = reinterpret_cast<const float4*>(static_cast<const float*>(p.kv.k) + off + e0);
+            const float4 a = src[0], c = src[1];
+            kk[0] = a.x; kk[1] = a.y; kk[2] = a.z; kk[3] = a.w; kk[4] = c.x; kk[5] = c.y; kk[6] = c.z; kk[7] = c.w;
+          } else {
+            const uint4 a = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p.kv.k) + off + e0);
+            kk[0] = bf16_lo(a.x); kk[1] = bf16_hi(a.x); kk[2] = bf16_lo(a.y); kk[3] = bf16_hi(a.y);
+            kk[4] = bf16_lo(a.z); kk[5] = bf16_hi(a.z); kk[6] = bf16_lo(a.w); kk[7] = bf16_hi(a.w);
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) kk[e] -= mean[e0 + e];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            if (i < r) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) pr[i] += kk[e] * Xi[i * D + e0 + e];
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (i >= r) break;
+        const float z = (lane < LB && lam[i] > 0.0f) ? pr[i] / lam[i] : 0.0f;
+        const float s3 = wave_sum_rows(z * z * z);
+        if (lane == 0) skw[i] = s3 / (float)n;
+      }
+      wave_lds_sync();
+    }
+  }
+
+  write_record_wave<D>(p, R, n, factors ? r : 0, mean, Xi, vmean, skw, lane);
+}
+
+// A block with fewer than LB tokens (count and means only, zero factors) by a
+// 256-thread workgroup: the column means are exact fp64 sums rounded once, so
+// the record is bitwise the one block_stats_wave writes.  `pool`: at least
+// block_mean_lds_bytes<D>() bytes of LDS.
+template <int D>
+constexpr size_t block_mean_lds_bytes() { return 8 * 256 + 8 * D; }
+
+template <int D, int LB>
+__device__ __forceinline__ void block_mean_wg(const StatsArgs& p, int b, int h, int j, int n, char* pool) {
+  static_assert(256 % D == 0, "whole columns per thread group");
+  constexpr int NH = 256 / D;                  // threads per column
+  double* sums = reinterpret_cast<double*>(pool);             // [NH][D]
+  float* mean = reinterpret_cast<float*>(pool + 8 * 256);     // [D]
+  float* vmean = mean + D;                                    // [D]
+  const int tid = threadIdx.x, e = tid % D, part = tid / D;
+  auto column_mean = [&](const uint16_t* base, float* out) {
+    double s = 0.0;
+    for (int i = part; i < n; i += NH) {
+      const int64_t off = kv_offset(p.kv, b, h, j * LB + i);
+      if (off >= 0) s += (double)__uint_as_float((uint32_t)base[off + e] << 16);
+    }
+    sums[part * D + e] = s;
+    __syncthreads();
+    if (tid < D) {
+      double t = 0.0;
+#pragma unroll
+      for (int q = 0; q < NH; ++q) t += sums[q * D + tid];
+      out[tid] = (float)(t / (double)n);
+    }
+    __syncthreads();
+  };
+  column_mean(static_cast<const uint16_t*>(p.kv.k), mean);
+  if (p.vmean) column_mean(static_cast<const uint16_t*>(p.kv.v), vmean);
+  if (tid < 64) {
+    uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
+    write_record_wave<D>(p, R, n, 0, mean, nullptr, vmean, nullptr, tid);
+  }
+}
+
+}  // namespace cobs

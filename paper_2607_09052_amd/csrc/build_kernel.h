@@ -3,6 +3,7 @@
 #pragma once
 
 #include "block_stats.h"
+#include "block_stats_wave.h"
 #include "cobs_kernels.h"
 
 namespace cobs {
@@ -37,6 +38,45 @@ __global__ __launch_bounds__(kBuildThreads) void build_stats_kernel(BuildParams 
   a.basis = p.basis;
   a.fd = SS ? p.fd : D;
   block_stats<D, P, LB, KF32, SS>(a, b, h, j, min(LB, T - j * LB), pool);
+}
+
+// One 64-thread workgroup (one wave) per (batch row, KV head, block) of LB
+// tokens: the configurations of block_stats_wave.
+template <int D, int LB, bool KF32>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2))) void build_stats_wave_kernel(BuildParams p) {
+  __shared__ __align__(16) char pool[wave_stats_lds_bytes<D, LB>()];
+  const int b = blockIdx.z, h = blockIdx.y;
+  const int T = clamp_len(p.seq_lens[b], p.tmax);
+  if (T <= 0) return;
+  const int nb = (T + LB - 1) / LB;
+  const int j = p.tail_mode ? (T - 1) / LB : p.first_block + (int)blockIdx.x;
+  if (j < 0 || j >= nb) return;
+  StatsArgs a;
+  a.kv = p.kv;
+  a.rec = p.rec;
+  a.hkv = p.hkv;
+  a.nbmax = p.nbmax;
+  a.r = p.r;
+  a.mdt = p.mdt;
+  a.fdt = p.fdt;
+  a.skew = p.skew;
+  a.vmean = p.vmean;
+  a.lay = p.lay;
+  a.basis = nullptr;
+  a.fd = D;
+  block_stats_wave<D, LB, KF32>(a, b, h, j, min(LB, T - j * LB), pool);
+}
+
+template <int D>
+hipError_t launch_build_wave(const BuildParams& p, dim3 grid, hipStream_t st) {
+  if (p.kv.lsh == 5) {
+    if (p.kv_f32) hipLaunchKernelGGL((build_stats_wave_kernel<D, 32, true>), grid, dim3(64), 0, st, p);
+    else hipLaunchKernelGGL((build_stats_wave_kernel<D, 32, false>), grid, dim3(64), 0, st, p);
+  } else {
+    if (p.kv_f32) hipLaunchKernelGGL((build_stats_wave_kernel<D, 64, true>), grid, dim3(64), 0, st, p);
+    else hipLaunchKernelGGL((build_stats_wave_kernel<D, 64, false>), grid, dim3(64), 0, st, p);
+  }
+  return hipGetLastError();
 }
 
 // Launch over `grid` for the block length of p.kv.

@@ -1,6 +1,8 @@
 // Device-side helpers shared by the COBS kernels (gfx950, wave64).
 #pragma once
 
+#include <type_traits>
+
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -46,6 +48,9 @@ __host__ __device__ inline RecLayout rec_layout(int d, int r, int mdt, int fdt, 
   l.total = ((l.vmean_off + (vmean ? l.mean_bytes : 0) + 15) / 16) * 16;
   return l;
 }
+
+// Eight bf16 values: an operand of the bf16 matrix-core instructions.
+typedef __bf16 sbf16x8_t __attribute__((ext_vector_type(8)));
 
 // ------------------------------------------------------------ conversions --
 __device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
@@ -258,6 +263,52 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // Sum over each row of 16 lanes, result in every lane of the row (DPP only).
+// Maximum over each row of 16 lanes, result in every lane of the row (DPP only).
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x141, 0xF, 0xF, false)));
+  x = fmaxf(x, __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x140, 0xF, 0xF, false)));
+  return x;
+}
+
+__device__ __forceinline__ float row16_sum(float x);
+
+// Sum / maximum over the whole wave by DPP within rows of 16 lanes and lane
+// reads across them; every lane of the wave must be active.
+__device__ __forceinline__ float wave_sum_rows(float x) {
+  x = row16_sum(x);
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return (a + b) + (c + d);
+}
+__device__ __forceinline__ float wave_max_rows(float x) {
+  x = row16_max(x);
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return fmaxf(fmaxf(a, b), fmaxf(c, d));
+}
+
+// fp64 sum over each row of 16 lanes by shifted partial sums (DPP row_shr on
+// both halves); lane 15 of the row holds the total.  Every lane must be active.
+__device__ __forceinline__ double row16_sum_last(double x) {
+  auto shr = [](double v, auto nc) -> double {
+    constexpr int n = decltype(nc)::value;
+    const int lo = __builtin_amdgcn_update_dpp(0, __double2loint(v), 0x110 + n, 0xF, 0xF, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, __double2hiint(v), 0x110 + n, 0xF, 0xF, true);
+    return __hiloint2double(hi, lo);
+  };
+  x += shr(x, std::integral_constant<int, 1>{});
+  x += shr(x, std::integral_constant<int, 2>{});
+  x += shr(x, std::integral_constant<int, 4>{});
+  x += shr(x, std::integral_constant<int, 8>{});
+  return x;
+}
+
 __device__ __forceinline__ float row16_sum(float x) {
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0xB1, 0xF, 0xF, false));  // xor 1
   x += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x4E, 0xF, 0xF, false));  // xor 2

@@ -17,6 +17,7 @@
 #pragma once
 
 #include "block_stats.h"
+#include "block_stats_wave.h"
 
 namespace cobs {
 
@@ -532,7 +533,6 @@ __device__ __forceinline__ void select_task(const SelectParams& p, int b, int h,
 // The 16 blocks' headers (count, scales) go through LDS to the lanes that
 // hold their results.
 // ---------------------------------------------------------------------------
-typedef __bf16 sbf16x8_t __attribute__((ext_vector_type(8)));
 typedef float sf32x4_t __attribute__((ext_vector_type(4)));
 
 // k-step kk (8 consecutive elements) of a lane's operand slice.
@@ -763,12 +763,13 @@ constexpr size_t lds_max() { return A > B ? A : B; }
 // holds row b's newest block first recomputes that block's record (its count,
 // mean and, once full, factors: the statistics follow the block as it fills,
 // §5.6), so the block's score and the normaliser over all blocks see the
-// cache as it is now.  The block statistics routine runs with 16 power
-// iteration columns on the same LDS pool.
+// cache as it is now.  Wave 0 runs the one-wave block statistics routine on
+// the same LDS pool while the other waves wait at the barrier.
 template <int D, int G, int MDT, int FDT>
 constexpr size_t select_refresh_lds() {
   constexpr bool kMat = MDT != DT_F32 && FDT != DT_F32;
-  return lds_max<kMat ? select_mfma_lds<G, 4, FDT>() : select_valu_lds<G>(), stats_lds_bytes<D, 16, kL, false>()>();
+  return lds_max<kMat ? select_mfma_lds<G, 4, FDT>() : select_valu_lds<G>(),
+                 lds_max<wave_stats_lds_bytes<D, kL>(), block_mean_lds_bytes<D>()>()>();
 }
 
 template <int D, int G, int MDT, int FDT>
@@ -790,7 +791,11 @@ __device__ __forceinline__ void select_refresh_task(const SelectParams& p, char*
     a.lay = p.lay;
     a.basis = nullptr;
     a.fd = D;
-    block_stats<D, 16, kL, false>(a, b, h, j, min(kL, T - j * kL), pool);
+    // a full block by one wave (bitwise the build's); a partial one, whose
+    // record is its exact means, by the whole workgroup
+    const int n = min(kL, T - j * kL);
+    if (n < kL) block_mean_wg<D, kL>(a, b, h, j, n, pool);
+    else if (threadIdx.x < 64) block_stats_wave<D, kL, false>(a, b, h, j, n, pool);
     __builtin_amdgcn_s_waitcnt(0);       // the record is written before it is scored
     __syncthreads();
   }
