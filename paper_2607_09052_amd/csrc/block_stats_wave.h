@@ -66,10 +66,13 @@ struct WaveStatsLds {
   static constexpr size_t jac = al(xi + 4 * 4 * D);        // Jacobi rotations: c, s per pair [P/2][2]
   static constexpr size_t misc = al(jac + 4 * 3 * P);      // order[4], ritz[4], skew[4], trace
   static constexpr size_t bytes = al(misc + 4 * 16);
+  // Gamma's bf16 parts when they are kept in LDS: [3][NT16][NT16 / 2][64 lanes] x 16 bytes
+  static constexpr size_t gparts = bytes;
+  static constexpr size_t bytes_glds = al(gparts + (size_t)3 * (LB / 16) * (LB / 32) * 64 * 16);
 };
 
-template <int D, int LB>
-constexpr size_t wave_stats_lds_bytes() { return WaveStatsLds<D, LB>::bytes; }
+template <int D, int LB, bool GLDS = false>
+constexpr size_t wave_stats_lds_bytes() { return GLDS ? WaveStatsLds<D, LB>::bytes_glds : WaveStatsLds<D, LB>::bytes; }
 
 // The configurations block_stats_wave covers.
 __host__ __device__ inline bool wave_stats_applies(int r, int lsh, bool subspace) {
@@ -78,8 +81,11 @@ __host__ __device__ inline bool wave_stats_applies(int r, int lsh, bool subspace
 
 // One block by the calling wave (lane = threadIdx.x % 64; every lane of the
 // wave calls it; no workgroup barrier inside).  `pool`: the wave's
-// wave_stats_lds_bytes<D, LB>() bytes of LDS.
-template <int D, int LB, bool KF32>
+// wave_stats_lds_bytes<D, LB, GLDS>() bytes of LDS.  GLDS: Gamma's bf16 parts
+// live in LDS and the factor pass loads its keys when it runs (fewer
+// registers, for a caller that has other work in flight); the operations and
+// so the record are the same either way.
+template <int D, int LB, bool KF32, bool GLDS = false>
 __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int h, int j, int n, char* pool) {
   static_assert(LB == 32 || LB == 64, "blocks of 32 or 64 tokens");
   static_assert(D == 64 || D == 128, "d = 64 or 128");
@@ -169,11 +175,12 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     }
     wave_lds_sync();
   };
-  // the keys' words stay in registers for the Gram matrix (bf16 keys)
-  Raw kraw[NCH][NT16];
+  {
+    Raw kraw[NCH][NT16];
 #pragma unroll
-  for (int q = 0; q < NCH; ++q) load_raw(p.kv.k, q, kraw[q]);
-  column_mean(kraw, mean);
+    for (int q = 0; q < NCH; ++q) load_raw(p.kv.k, q, kraw[q]);
+    column_mean(kraw, mean);
+  }
   if (p.vmean) {
     Raw vraw[NCH][NT16];
 #pragma unroll
@@ -190,20 +197,14 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     for (int t = 0; t < NT16; ++t)
 #pragma unroll
       for (int u = 0; u < NT16; ++u) g[t][u] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-    // bf16 keys: the words of the mean pass; fp32 keys: loaded again, chunk
-    // q + 1 in flight while chunk q is multiplied
+    // the keys again (L2), chunk q + 1 in flight while chunk q is multiplied
     Raw rcur[NT16], rnext[NT16];
-    if constexpr (KF32) load_raw(p.kv.k, 0, rnext);
-#pragma unroll
+    load_raw(p.kv.k, 0, rnext);
+#pragma unroll 1
     for (int q = 0; q < NCH; ++q) {
-      if constexpr (KF32) {
 #pragma unroll
-        for (int t = 0; t < NT16; ++t) rcur[t] = rnext[t];
-        if (q + 1 < NCH) load_raw(p.kv.k, q + 1, rnext);
-      } else {
-#pragma unroll
-        for (int t = 0; t < NT16; ++t) rcur[t] = kraw[q][t];
-      }
+      for (int t = 0; t < NT16; ++t) rcur[t] = rnext[t];
+      if (q + 1 < NCH) load_raw(p.kv.k, q + 1, rnext);
       float x[NT16][8];
       unpack(rcur, x);
       const float4 m0 = *reinterpret_cast<const float4*>(mean + lk * CPL + 8 * q);
@@ -236,21 +237,34 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     // matrix-core operand layout: for output tile t and k-chunk c, lane group
     // lk supplies the contraction indices 16 a + 4 lk + v, a in {2c, 2c + 1}
     constexpr int KC = NT16 / 2;                  // 32-index k-chunks
-    sbf16x8_t gp[3][NT16][KC];
+    sbf16x8_t gp[GLDS ? 1 : 3][GLDS ? 1 : NT16][GLDS ? 1 : KC];
+    sbf16x8_t* gpl = reinterpret_cast<sbf16x8_t*>(pool + Lay::gparts);
 #pragma unroll
     for (int t = 0; t < NT16; ++t)
 #pragma unroll
-      for (int c = 0; c < KC; ++c)
+      for (int c = 0; c < KC; ++c) {
+        sbf16x8_t parts[3];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           float x = g[2 * c + i / 4][t][i % 4];
 #pragma unroll
           for (int part = 0; part < 3; ++part) {
             const uint32_t hb = f32_to_bf16_rne(x);
-            gp[part][t][c][i] = __builtin_bit_cast(__bf16, (uint16_t)hb);
+            parts[part][i] = __builtin_bit_cast(__bf16, (uint16_t)hb);
             x -= __uint_as_float(hb << 16);
           }
         }
+#pragma unroll
+        for (int part = 0; part < 3; ++part) {
+          if constexpr (GLDS) gpl[((part * NT16 + t) * KC + c) * 64 + lane] = parts[part];
+          else gp[part][t][c] = parts[part];
+        }
+      }
+    auto gpart = [&](int part, int t, int c) -> sbf16x8_t {
+      if constexpr (GLDS) return gpl[((part * NT16 + t) * KC + c) * 64 + lane];
+      else return gp[part][t][c];
+    };
+    if constexpr (GLDS) wave_lds_sync();
     // dst = (Gamma / trace) src, both in the result layout: row 16 t + 4 lk + v,
     // column lr.  The power iteration's products take the three leading
     // cross terms of the bf16 parts (relative error ~1e-5, which the iteration
@@ -276,13 +290,13 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
           if (exact) {
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[2][t][c], wp[0][c], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[1][t][c], wp[1][c], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[0][t][c], wp[2][c], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(2, t, c), wp[0][c], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[1][c], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[2][c], acc, 0, 0, 0);
           }
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[1][t][c], wp[0][c], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[0][t][c], wp[1][c], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gp[0][t][c], wp[0][c], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[0][c], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[1][c], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[0][c], acc, 0, 0, 0);
         }
 #pragma unroll
         for (int v = 0; v < 4; ++v) dst[t][v] = acc[v] * gsc;
@@ -362,8 +376,9 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     // Lanes < P/2 form the rotations from H's entries, passed through LDS.
     // bf16 keys: the factor pass's words (the lane's EPL columns of every row)
     // load during Jacobi, which does not touch memory
-    uint32_t xraw[KF32 ? 1 : LB];
-    if constexpr (!KF32) {
+    constexpr bool kPre = !KF32 && !GLDS;
+    uint32_t xraw[kPre ? LB : 1];
+    if constexpr (kPre) {
 #pragma unroll
       for (int row = 0; row < LB; ++row) {
         const int64_t off0 = kv_offset(p.kv, b, h, j * LB + row);   // -1: a page outside the pool (zero keys)
@@ -475,7 +490,7 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int c = 0; c < EPL; ++c) xs[i][c] = 0.0f;
-      if constexpr (!KF32) {
+      if constexpr (kPre) {
 #pragma unroll
         for (int r4 = 0; r4 < LB; r4 += 4) {
           float4 w4[4];
@@ -501,9 +516,9 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
           }
         }
       }
-      // fp32 keys: the lane's columns of 16 rows at a time, their loads in flight together
+      // otherwise the lane's columns of 16 rows at a time, their loads in flight together
 #pragma unroll 1
-      for (int r0 = 0; KF32 && r0 < LB; r0 += 16) {
+      for (int r0 = 0; !kPre && r0 < LB; r0 += 16) {
         float kv_[16][EPL];
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {

@@ -769,7 +769,7 @@ template <int D, int G, int MDT, int FDT>
 constexpr size_t select_refresh_lds() {
   constexpr bool kMat = MDT != DT_F32 && FDT != DT_F32;
   return lds_max<kMat ? select_mfma_lds<G, 4, FDT>() : select_valu_lds<G>(),
-                 lds_max<wave_stats_lds_bytes<D, kL>(), block_mean_lds_bytes<D>()>()>();
+                 lds_max<wave_stats_lds_bytes<D, kL, true>(), block_mean_lds_bytes<D>()>()>();
 }
 
 template <int D, int G, int MDT, int FDT>
@@ -795,7 +795,7 @@ __device__ __forceinline__ void select_refresh_task(const SelectParams& p, char*
     // record is its exact means, by the whole workgroup
     const int n = min(kL, T - j * kL);
     if (n < kL) block_mean_wg<D, kL>(a, b, h, j, n, pool);
-    else if (threadIdx.x < 64) block_stats_wave<D, kL, false>(a, b, h, j, n, pool);
+    else if (threadIdx.x < 64) block_stats_wave<D, kL, false, true>(a, b, h, j, n, pool);
     __builtin_amdgcn_s_waitcnt(0);       // the record is written before it is scored
     __syncthreads();
   }
