@@ -1,8 +1,9 @@
 // Block statistics of one block by one wave (Sec. 5.3, Gram trick of
 // Sec. 5.6, storage of Sec. 5.5), for blocks of LB = 32 or 64 tokens with
-// rank r <= 4 and full-space factors: the method and the arithmetic of
-// block_stats (16 power-iteration columns), laid out so that a wave needs no
-// workgroup barrier and several blocks stream through a CU at once.
+// rank r <= 4 and full-space factors: the method of block_stats (16
+// power-iteration columns, the same counts of products, pivot rule and Jacobi
+// termination), laid out so that a wave needs no workgroup barrier and several
+// blocks stream through a CU at once.
 //
 //   * Lane (lk, lr) = (lane / 16, lane % 16) reads rows 16 t + lr of the block
 //     and the d / 4 columns [lk d/4, (lk+1) d/4), first for the column means
@@ -15,9 +16,12 @@
 //     A operand of Gamma W with the contraction index 16 a + 4 lk + v, and the
 //     result of a product is the B operand of the next one, so the power
 //     iteration's products need no LDS.  Y^T Y takes the same registers as
-//     both operands.  Only the re-orthonormalisation W = Y N X^T (the
-//     Cholesky of cholesky_inverse), the Rayleigh-Ritz matrix, Jacobi and
-//     the factors go through the wave's LDS.
+//     both operands.  The products Gamma W run on the bf16 matrix cores with
+//     Gamma and W each split into three bf16 parts (hi + mid + lo, the fp32
+//     value exactly).  Only the re-orthonormalisation W = Y N X^T (the
+//     Cholesky of cholesky_inverse), the Rayleigh-Ritz matrix, the Jacobi
+//     rotations and the factors go through the wave's LDS; Jacobi applies its
+//     rotations as matrix-core products on registers.
 //   * Factors: lane l owns columns (d / 64) l .. of xi and reads those columns
 //     of every key (a second pass over the block in L2).
 #pragma once
@@ -49,26 +53,33 @@ __device__ __forceinline__ void write_record_wave(const StatsArgs& p, uint8_t* R
   for (int idx = end / 4 + lane; idx < lay.total / 4; idx += 64) reinterpret_cast<uint32_t*>(R)[idx] = 0u;
 }
 
-// LDS of one wave (16-byte aligned pieces).
+// LDS of one wave (16-byte aligned pieces).  Gamma's bf16 parts kept in LDS
+// (the low part, or all three) live from the split of Gamma to the last
+// product of the power iteration; the Rayleigh-Ritz, Jacobi and factor
+// buffers, written after that product, take the same bytes.
 template <int D, int LB>
 struct WaveStatsLds {
   static constexpr int P = 16, PS = P + 1;
   static constexpr size_t al(size_t x) { return (x + 15) / 16 * 16; }
+  static constexpr size_t mx(size_t a, size_t b) { return a > b ? a : b; }
   static constexpr size_t mean = 0;                        // [D]
   static constexpr size_t vmean = al(mean + 4 * D);        // [D]
   static constexpr size_t yp = al(vmean + 4 * D);          // [LB][PS]: Y, then W, by rows
   static constexpr size_t sm = al(yp + 4 * LB * PS);       // [P][PS]
   static constexpr size_t lm = al(sm + 4 * P * PS);        // [P][PS]
-  static constexpr size_t hm = al(lm + 4 * P * PS);        // [2][P][PS]
-  static constexpr size_t vm = al(hm + 8 * P * PS);        // [2][P][PS]
-  static constexpr size_t wr = al(vm + 8 * P * PS);        // [4][LB] Ritz vectors
+  static constexpr size_t misc = al(lm + 4 * P * PS);      // order[4], ritz[4], skew[4], trace
+  // one bf16 part of Gamma: [NT16][NT16 / 2][64 lanes] x 16 bytes
+  static constexpr size_t part_bytes = (size_t)(LB / 16) * (LB / 32) * 64 * 16;
+  static constexpr size_t gparts = al(misc + 4 * 16);
+  static constexpr size_t hm = gparts;                     // [P][PS]
+  static constexpr size_t vm = al(hm + 4 * P * PS);        // [P][PS]
+  static constexpr size_t wr = al(vm + 4 * P * PS);        // [4][LB] Ritz vectors
   static constexpr size_t xi = al(wr + 4 * 4 * LB);        // [4][D] factors
   static constexpr size_t jac = al(xi + 4 * 4 * D);        // Jacobi rotations: c, s per pair [P/2][2]
-  static constexpr size_t misc = al(jac + 4 * 3 * P);      // order[4], ritz[4], skew[4], trace
-  static constexpr size_t bytes = al(misc + 4 * 16);
-  // Gamma's bf16 parts when they are kept in LDS: [3][NT16][NT16 / 2][64 lanes] x 16 bytes
-  static constexpr size_t gparts = bytes;
-  static constexpr size_t bytes_glds = al(gparts + (size_t)3 * (LB / 16) * (LB / 32) * 64 * 16);
+  static constexpr size_t chk = al(jac + 4 * 3 * P);       // Jacobi stop test: diagonal [P], ranks [P], threshold
+  static constexpr size_t late = al(chk + 4 * (2 * P + 4));
+  static constexpr size_t bytes = mx(late, gparts + part_bytes);
+  static constexpr size_t bytes_glds = mx(late, gparts + 3 * part_bytes);
 };
 
 template <int D, int LB, bool GLDS = false>
@@ -100,8 +111,10 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
   float* Yp = reinterpret_cast<float*>(pool + Lay::yp);
   float* Sm = reinterpret_cast<float*>(pool + Lay::sm);
   float* Lm = reinterpret_cast<float*>(pool + Lay::lm);
-  float (*Hm)[P * PS] = reinterpret_cast<float (*)[P * PS]>(pool + Lay::hm);
-  float (*Vm)[P * PS] = reinterpret_cast<float (*)[P * PS]>(pool + Lay::vm);
+  float* Hm = reinterpret_cast<float*>(pool + Lay::hm);
+  float* Vm = reinterpret_cast<float*>(pool + Lay::vm);
+  float* cdiag = reinterpret_cast<float*>(pool + Lay::chk);
+  int* crank = reinterpret_cast<int*>(pool + Lay::chk) + P;
   float* Wr = reinterpret_cast<float*>(pool + Lay::wr);
   float* Xi = reinterpret_cast<float*>(pool + Lay::xi);
   float* rot = reinterpret_cast<float*>(pool + Lay::jac);
@@ -117,11 +130,15 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
   struct Raw {
     uint4 w[KF32 ? 2 : 1];
   };
+  // the block's first token and the stride between its tokens (a page holds
+  // one block); kbase < 0: its page is outside the pool (zero keys)
+  const int64_t kbase = kv_offset(p.kv, b, h, j * LB);
+  const int64_t rs = p.kv.table ? (int64_t)p.kv.d : p.kv.st;
   int64_t roff[NT16];                           // row offsets, -1: no row
 #pragma unroll
   for (int t = 0; t < NT16; ++t) {
     const int i = 16 * t + lr;
-    roff[t] = (i < n) ? kv_offset(p.kv, b, h, j * LB + i) : -1;
+    roff[t] = (i < n && kbase >= 0) ? kbase + i * rs : -1;
   }
   auto load_raw = [&](const void* base, int q, Raw* raw) {
 #pragma unroll
@@ -159,34 +176,32 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
   // column means into LDS: fp64 sums (exact for the block's fp32 values unless
   // their magnitudes span > 2^29), one rounding to fp32, so a block of
   // identical rows centres to exact zeros
-  auto column_mean = [&](const Raw (*raw)[NT16], float* out) {
+  // (the loads of QB chunks in flight together: all of them for bf16 keys)
+  constexpr int QB = KF32 ? (NCH > 1 ? NCH / 2 : 1) : NCH;
+  auto column_mean = [&](const void* base, float* out) {
 #pragma unroll
-    for (int q = 0; q < NCH; ++q) {
-      float x[NT16][8];
-      unpack(raw[q], x);
+    for (int q0 = 0; q0 < NCH; q0 += QB) {
+      Raw raw[QB][NT16];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        double cs = 0.0;
+      for (int q = 0; q < QB; ++q) load_raw(base, q0 + q, raw[q]);
 #pragma unroll
-        for (int t = 0; t < NT16; ++t) cs += (double)x[t][e];
-        cs = row16_sum_last(cs);
-        if (lr == 15) out[lk * CPL + 8 * q + e] = (float)(cs / (double)n);
+      for (int q = 0; q < QB; ++q) {
+        float x[NT16][8];
+        unpack(raw[q], x);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          double cs = 0.0;
+#pragma unroll
+          for (int t = 0; t < NT16; ++t) cs += (double)x[t][e];
+          cs = row16_sum_last(cs);
+          if (lr == 15) out[lk * CPL + 8 * (q0 + q) + e] = (float)(cs / (double)n);
+        }
       }
     }
     wave_lds_sync();
   };
-  {
-    Raw kraw[NCH][NT16];
-#pragma unroll
-    for (int q = 0; q < NCH; ++q) load_raw(p.kv.k, q, kraw[q]);
-    column_mean(kraw, mean);
-  }
-  if (p.vmean) {
-    Raw vraw[NCH][NT16];
-#pragma unroll
-    for (int q = 0; q < NCH; ++q) load_raw(p.kv.v, q, vraw[q]);
-    column_mean(vraw, vmean);
-  }
+  column_mean(p.kv.k, mean);
+  if (p.vmean) column_mean(p.kv.v, vmean);
 
   const bool factors = (n == LB) && (r > 0);
   uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
@@ -235,9 +250,11 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
 
     // Gamma as three bf16 parts (hi + mid + lo = the fp32 value) in the bf16
     // matrix-core operand layout: for output tile t and k-chunk c, lane group
-    // lk supplies the contraction indices 16 a + 4 lk + v, a in {2c, 2c + 1}
+    // lk supplies the contraction indices 16 a + 4 lk + v, a in {2c, 2c + 1}.
+    // The low part, which only the last product takes, is kept in LDS (GLDS:
+    // all three).
     constexpr int KC = NT16 / 2;                  // 32-index k-chunks
-    sbf16x8_t gp[GLDS ? 1 : 3][GLDS ? 1 : NT16][GLDS ? 1 : KC];
+    sbf16x8_t gp[GLDS ? 1 : 2][GLDS ? 1 : NT16][GLDS ? 1 : KC];
     sbf16x8_t* gpl = reinterpret_cast<sbf16x8_t*>(pool + Lay::gparts);
 #pragma unroll
     for (int t = 0; t < NT16; ++t)
@@ -256,15 +273,15 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
         }
 #pragma unroll
         for (int part = 0; part < 3; ++part) {
-          if constexpr (GLDS) gpl[((part * NT16 + t) * KC + c) * 64 + lane] = parts[part];
+          if (GLDS || part == 2) gpl[(((GLDS ? part : 0) * NT16 + t) * KC + c) * 64 + lane] = parts[part];
           else gp[part][t][c] = parts[part];
         }
       }
     auto gpart = [&](int part, int t, int c) -> sbf16x8_t {
-      if constexpr (GLDS) return gpl[((part * NT16 + t) * KC + c) * 64 + lane];
+      if (GLDS || part == 2) return gpl[(((GLDS ? part : 0) * NT16 + t) * KC + c) * 64 + lane];
       else return gp[part][t][c];
     };
-    if constexpr (GLDS) wave_lds_sync();
+    wave_lds_sync();
     // dst = (Gamma / trace) src, both in the result layout: row 16 t + 4 lk + v,
     // column lr.  The power iteration's products take the three leading
     // cross terms of the bf16 parts (relative error ~1e-5, which the iteration
@@ -362,8 +379,8 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
 #pragma unroll
     for (int k = 0; k < P * P / 64; ++k) {
       const int idx = lane + 64 * k, a = idx / P, c = idx % P;
-      Hm[0][a * PS + c] = 0.5f * (Sm[a * PS + c] + Sm[c * PS + a]);
-      Vm[0][a * PS + c] = (a == c) ? 1.0f : 0.0f;
+      Hm[a * PS + c] = 0.5f * (Sm[a * PS + c] + Sm[c * PS + a]);
+      Vm[a * PS + c] = (a == c) ? 1.0f : 0.0f;
     }
     wave_lds_sync();
     // ---- eigenpairs of H by parallel cyclic Jacobi (round-robin pairing,
@@ -378,14 +395,16 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     // load during Jacobi, which does not touch memory
     constexpr bool kPre = !KF32 && !GLDS;
     uint32_t xraw[kPre ? LB : 1];
+    // (a block whose page is outside the pool reads page 0, which always
+    // exists, and masks the words to zero keys)
+    const uint32_t kmask = kbase < 0 ? 0u : ~0u;
+    const int64_t kb0 = kbase < 0 ? 0 : kbase;
     if constexpr (kPre) {
+      const uint16_t* src = static_cast<const uint16_t*>(p.kv.k) + kb0 + EPL * lane;
 #pragma unroll
       for (int row = 0; row < LB; ++row) {
-        const int64_t off0 = kv_offset(p.kv, b, h, j * LB + row);   // -1: a page outside the pool (zero keys)
-        const uint16_t* src = static_cast<const uint16_t*>(p.kv.k) + (off0 < 0 ? 0 : off0) + EPL * lane;
-        if (off0 < 0) xraw[row] = 0u;
-        else if constexpr (EPL == 2) xraw[row] = *reinterpret_cast<const uint32_t*>(src);
-        else xraw[row] = *src;
+        if constexpr (EPL == 2) xraw[row] = *reinterpret_cast<const uint32_t*>(src + row * rs) & kmask;
+        else xraw[row] = src[row * rs] & kmask;
       }
     }
     auto slot_index = [&](int m, int rnd) { return m == 0 ? 0 : 1 + (m - 1 + rnd) % (P - 1); };
@@ -393,22 +412,64 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     f32x4_t hr, vt;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      hr[v] = Hm[0][(4 * lk + v) * PS + lr];
+      hr[v] = Hm[(4 * lk + v) * PS + lr];
       vt[v] = (4 * lk + v == lr) ? 1.0f : 0.0f;
     }
+    // The top r eigenpairs are settled, and the remaining rotations would only
+    // mix directions outside them, when every entry of H in a row or column
+    // of the r largest diagonal entries passes the rotation threshold and the
+    // Gershgorin disc of every other row lies below the r-th largest diagonal
+    // entry.  Wave-uniform.
+    auto top_settled = [&]() -> bool {
+      float cs = 0.0f;                   // column lr's off-diagonal |H|, this lane's rows
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        if (4 * lk + v == lr) cdiag[lr] = hr[v];
+        else cs += fabsf(hr[v]);
+      }
+      cs += __shfl_xor(cs, 16);
+      cs += __shfl_xor(cs, 32);
+      wave_lds_sync();
+      if (lane < P) {
+        const float ta = cdiag[lane];
+        int rank = 0;
+        for (int c = 0; c < P; ++c) {
+          const float tc = cdiag[c];
+          rank += (tc > ta) || (tc == ta && c < lane);
+        }
+        crank[lane] = rank;
+        if (rank == r - 1) cdiag[2 * P] = ta;
+      }
+      wave_lds_sync();
+      const float thr = cdiag[2 * P], dy = cdiag[lr];
+      const bool topy = crank[lr] < r;
+      bool bad = !topy && dy + cs >= thr;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int x = 4 * lk + v;
+        if (x != lr && (topy || crank[x] < r)) {
+          const float dx = cdiag[x], apq = fabsf(hr[v]);
+          bad = bad || (apq > 1e-6f * sqrtf(fmaxf(dx, 0.0f) * fmaxf(dy, 0.0f)) && apq > 2e-8f);
+        }
+      }
+      const bool settled = __ballot(bad) == 0;
+      wave_lds_sync();                   // cdiag is rewritten by the next test
+      return settled;
+    };
 #pragma unroll 1
     for (int sweep = 0; sweep < kJacobiSweeps; ++sweep) {
+      if (top_settled()) break;
       bool moved = false;
 #pragma unroll 1
       for (int rnd = 0; rnd < P - 1; ++rnd) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) Hm[0][(4 * lk + v) * PS + lr] = hr[v];
+        for (int v = 0; v < 4; ++v) Hm[(4 * lk + v) * PS + lr] = hr[v];
         wave_lds_sync();
         bool big = false;
         if (lane < P / 2) {
           const int x = slot_index(lane, rnd), yy = slot_index(P - 1 - lane, rnd);
           const int pp = min(x, yy), qq = max(x, yy);
-          const float app = Hm[0][pp * PS + pp], aqq = Hm[0][qq * PS + qq], apq = Hm[0][pp * PS + qq];
+          const float app = Hm[pp * PS + pp], aqq = Hm[qq * PS + qq], apq = Hm[pp * PS + qq];
           big = fabsf(apq) > 1e-6f * sqrtf(fmaxf(app, 0.0f) * fmaxf(aqq, 0.0f)) && fabsf(apq) > 2e-8f;
           float c = 1.0f, sn = 0.0f;
           if (apq != 0.0f) {
@@ -449,37 +510,39 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
       if (!moved) break;
     }
     // the eigenvalues on H's diagonal, V = (V^T)^T by rows, for the ranking and the Ritz vectors
-    const int cw = 0;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      Hm[0][(4 * lk + v) * PS + lr] = hr[v];
-      Vm[0][lr * PS + 4 * lk + v] = vt[v];
+      Hm[(4 * lk + v) * PS + lr] = hr[v];
+      Vm[lr * PS + 4 * lk + v] = vt[v];
     }
     wave_lds_sync();
     // ---- top-r Ritz values, descending, ties to the lower index (rank by counting)
     if (lane < P) {
-      const float ta = Hm[cw][lane * PS + lane];
+      const float ta = Hm[lane * PS + lane];
       int rank = 0;
       for (int c = 0; c < P; ++c) {
-        const float tc = Hm[cw][c * PS + c];
+        const float tc = Hm[c * PS + c];
         rank += (tc > ta) || (tc == ta && c < lane);
       }
       if (rank < r) { order[rank] = lane; ritzval[rank] = ta; }
     }
     wave_lds_sync();
-    // Ritz vectors w_i = W V[:, order_i], lane = row
+    // Ritz vectors w_i = W V[:, order_i], lane = row; rows r .. 3 zero
     if (lane < LB) {
-      for (int i = 0; i < r; ++i) {
-        const int col = order[i];
-        float s = 0.0f;
 #pragma unroll
-        for (int a = 0; a < P; ++a) s += Yp[lane * PS + a] * Vm[cw][a * PS + col];
+      for (int i = 0; i < 4; ++i) {
+        float s = 0.0f;
+        if (i < r) {
+          const int col = order[i];
+#pragma unroll
+          for (int a = 0; a < P; ++a) s += Yp[lane * PS + a] * Vm[a * PS + col];
+        }
         Wr[i * LB + lane] = s;
       }
     }
     wave_lds_sync();
     // xi_i = Kc^T w_i / sqrt(n): lane l owns columns EPL l .. EPL l + EPL - 1
-    const float rs = 1.0f / sqrtf((float)n);
+    const float rsn = 1.0f / sqrtf((float)n);
     const float top = ritzval[0];
     {
       float xs[4][EPL];
@@ -496,7 +559,7 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
           float4 w4[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            w4[i] = (i < r) ? *reinterpret_cast<const float4*>(Wr + i * LB + r4) : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            w4[i] = *reinterpret_cast<const float4*>(Wr + i * LB + r4);
 #pragma unroll
           for (int rr = 0; rr < 4; ++rr) {
             const int row = r4 + rr;
@@ -522,24 +585,20 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
         float kv_[16][EPL];
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
-          const int64_t off0 = kv_offset(p.kv, b, h, j * LB + r0 + rr);   // -1: a page outside the pool (zero keys)
-          const int64_t off = (off0 < 0 ? 0 : off0) + EPL * lane;
-          if (off0 < 0) {
-#pragma unroll
-            for (int c = 0; c < EPL; ++c) kv_[rr][c] = 0.0f;
-          } else if constexpr (KF32) {
+          const int64_t off = kb0 + (r0 + rr) * rs + EPL * lane;
+          if constexpr (KF32) {
             if constexpr (EPL == 2) {
-              const float2 a = *reinterpret_cast<const float2*>(static_cast<const float*>(p.kv.k) + off);
-              kv_[rr][0] = a.x; kv_[rr][1] = a.y;
+              const uint2 a = *reinterpret_cast<const uint2*>(static_cast<const float*>(p.kv.k) + off);
+              kv_[rr][0] = __uint_as_float(a.x & kmask); kv_[rr][1] = __uint_as_float(a.y & kmask);
             } else {
-              kv_[rr][0] = static_cast<const float*>(p.kv.k)[off];
+              kv_[rr][0] = __uint_as_float(reinterpret_cast<const uint32_t*>(p.kv.k)[off] & kmask);
             }
           } else {
             if constexpr (EPL == 2) {
-              const uint32_t a = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(p.kv.k) + off);
+              const uint32_t a = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(p.kv.k) + off) & kmask;
               kv_[rr][0] = bf16_lo(a); kv_[rr][1] = bf16_hi(a);
             } else {
-              kv_[rr][0] = __uint_as_float((uint32_t)static_cast<const uint16_t*>(p.kv.k)[off] << 16);
+              kv_[rr][0] = __uint_as_float(((uint32_t)static_cast<const uint16_t*>(p.kv.k)[off] << 16) & kmask);
             }
           }
         }
@@ -547,7 +606,7 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
         for (int rr = 0; rr < 16; ++rr) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const float wi = (i < r) ? Wr[i * LB + r0 + rr] : 0.0f;
+            const float wi = Wr[i * LB + r0 + rr];
 #pragma unroll
             for (int c = 0; c < EPL; ++c) xs[i][c] += (kv_[rr][c] - mc[c]) * wi;
           }
@@ -563,7 +622,7 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
         float best = -1.0f, sbest = 0.0f;
 #pragma unroll
         for (int c = 0; c < EPL; ++c) {
-          xs[i][c] = keep ? xs[i][c] * rs : 0.0f;
+          xs[i][c] = keep ? xs[i][c] * rsn : 0.0f;
           const float a = fabsf(xs[i][c]);
           if (a > best) { best = a; sbest = xs[i][c]; }
         }
@@ -592,7 +651,7 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
         pr[i] = 0.0f;
       }
       if (lane < LB) {
-        const int64_t off0 = kv_offset(p.kv, b, h, j * LB + lane);
+        const int64_t off0 = kbase < 0 ? -1 : kbase + lane * rs;
         const int64_t off = off0 < 0 ? 0 : off0;
 #pragma unroll 1
         for (int e0 = 0; e0 < D; e0 += 8) {
@@ -649,12 +708,11 @@ __device__ __forceinline__ void block_mean_wg(const StatsArgs& p, int b, int h, 
   float* mean = reinterpret_cast<float*>(pool + 8 * 256);     // [D]
   float* vmean = mean + D;                                    // [D]
   const int tid = threadIdx.x, e = tid % D, part = tid / D;
+  const int64_t kbase = kv_offset(p.kv, b, h, j * LB);     // a page holds one block
+  const int64_t rs = p.kv.table ? (int64_t)p.kv.d : p.kv.st;
   auto column_mean = [&](const uint16_t* base, float* out) {
     double s = 0.0;
-    for (int i = part; i < n; i += NH) {
-      const int64_t off = kv_offset(p.kv, b, h, j * LB + i);
-      if (off >= 0) s += (double)__uint_as_float((uint32_t)base[off + e] << 16);
-    }
+    for (int i = part; kbase >= 0 && i < n; i += NH) s += (double)__uint_as_float((uint32_t)base[kbase + i * rs + e] << 16);
     sums[part * D + e] = s;
     __syncthreads();
     if (tid < D) {

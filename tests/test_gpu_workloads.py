@@ -12,10 +12,13 @@ Two comparisons per checked (batch row, KV head) unit:
   and byte for byte against the oracle's storage encoding of the GPU's fp32
   statistics.
 * Independent descriptors (build quality): the oracle also builds its own
-  descriptors from K by exact fp64 eigendecomposition.  Scores then agree
-  within a band per factor storage type (DECISION_BAND), selections follow the
-  set rule at twice that band, the share of selected block ids that differ is
-  bounded, and attention on the oracle's selection matches the oracle.
+  descriptors from K by exact fp64 eigendecomposition.  The two sides' fp32
+  statistics, scored alike, agree within 2e-3 on every candidate (the solver's
+  accuracy, free of the storage rounding, whose encoding is checked byte for
+  byte above); at the configured storage the selections follow the set rule at
+  twice a band per factor storage type (DECISION_BAND), the share of selected
+  block ids that differ is bounded, and attention on the oracle's selection
+  matches the oracle.
 """
 
 import numpy as np
@@ -30,13 +33,16 @@ from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_records, check_sele
 
 pytestmark = pytest.mark.gpu
 
-# |sigma_gpu - sigma_oracle| bound for independently built descriptors, by the
-# factor storage type.  fp32/bf16 factors: the fixed-count iteration meets the
+# |sigma_gpu - sigma_oracle| band for independently built descriptors, by the
+# factor storage type.  fp32 factors: the fixed-count iteration meets the
 # Ky-Fan energy bound to ~1e-6 and the rank-r covariance to 1e-3 (relative
 # Frobenius) where the eigengap is >= 5 %, which moves (c^2/2) q^T Sigma_r q by
-# well under 2e-3 at these query norms.  E2M1 factors: a solver difference can
-# move an element across an E2M1 rounding boundary, changing it by one code
-# step (up to max|xi|/3) and sigma by up to ~1e-2.
+# well under 2e-3 at these query norms; the scores of the fp32 statistics are
+# held to this band.  Stored bf16 / E2M1 factors: a solver difference of ~1e-6
+# can move an element across a rounding boundary of the storage format, one
+# code step (for E2M1 up to max|xi|/3), which moved one c4 block's sigma by
+# 3.2e-2; these bands apply to the selections (set rule at twice the band) and
+# to the share of differing block ids.
 DECISION_BAND = {"f32": 2e-3, "bf16": 4e-3, "e2m1": 2e-2}
 # Largest share of selected block ids allowed to differ between the GPU's and
 # the oracle's independently built descriptors (boundary blocks whose scores
@@ -118,20 +124,24 @@ def _run_case(name, seed, units=None, **over):
         shared_exact += _shared_bytes_check(cfg, rec_u, qu, K, V, T, sel[b, h].cpu().numpy(),
                                             out[b, sl].cpu().numpy(), lse[b, sl].cpu().numpy(),
                                             scores[b, h].cpu().numpy())
+        raw = M.block_statistics(K, T, L, cfg.rank)
         res = M.decode_unit(qu, K, V, T, L, cfg.rank, cfg.budget, cfg.window, cfg.scale,
-                            cfg.mean_dtype, cfg.factor_dtype, stats=_oracle_stats(K, T, cfg))
+                            cfg.mean_dtype, cfg.factor_dtype,
+                            stats=M.stored_statistics(*raw, cfg.mean_dtype, cfg.factor_dtype))
         ora[(b, h)] = res
         nc = res["nc"]
-        sg = scores[b, h, :nc].cpu().double().numpy()
-        dev_ = float(np.max(np.abs(sg - res["sigma"][:nc]))) if nc else 0.0
+        # the solver: both sides' fp32 statistics, scored alike
+        sg = oracle_select(rec32[b, h].cpu().numpy(), qu, T, cfg32)[0]
+        so = M.group_scores(M.log_mass_estimate(qu, *M.stored_statistics(*raw, "f32", "f32")[:3], cfg.scale))
+        dev_ = float(np.max(np.abs(sg[:nc] - so[:nc]))) if nc else 0.0
         worst = max(worst, dev_)
-        assert dev_ <= band, (b, h, dev_)
+        assert dev_ <= DECISION_BAND["f32"], (b, h, dev_)
         same += check_selection(sel[b, h].cpu().numpy(), res["sigma"], nc, cfg.budget, band=2 * band)
         nd, nt = _id_diff(sel[b, h].cpu().numpy(), res["sel"])
         ndiff, ntot = ndiff + nd, ntot + nt
         sel_o[b, h] = torch.from_numpy(res["sel"].astype(np.int32))
     say(f"{name}: shared bytes: exact selections {shared_exact}/{len(units)}; independent descriptors: "
-        f"max |sigma_gpu - sigma_oracle| = {worst:.2e}, identical selections {same}/{len(units)}, "
+        f"max |sigma_gpu - sigma_oracle| at fp32 storage = {worst:.2e}, identical selections {same}/{len(units)}, "
         f"differing block ids {ndiff}/{ntot}")
     assert ndiff <= ID_DIFF_BOUND[cfg.factor_dtype] * ntot, (ndiff, ntot)
     out_o = torch.empty_like(out)
