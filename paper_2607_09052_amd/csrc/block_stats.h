@@ -90,10 +90,11 @@ __device__ __forceinline__ void store_vector_wave(const float* x, int len, int d
 }
 
 // Value of lane c of each row of 16 lanes, to every lane of that row (DPP
-// row_newbcast; c a compile-time constant).
+// row_newbcast; c a compile-time constant).  Every source lane exists, so
+// bound_ctrl changes nothing and frees the destination from holding an old value.
 template <int C>
 __device__ __forceinline__ float row_bcast(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), 0x150 + C, 0xf, 0xf, false));
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x150 + C, 0xf, 0xf, true));
 }
 
 template <int P>
@@ -134,23 +135,25 @@ __device__ __forceinline__ void cholesky_inverse(const float* Sm, float* Lm, int
     const float dk = piv * rdk;
     rdl = (li == k) ? rdk : rdl;
     const float lk = (li > k) ? row[k] * rdk : 0.0f;        // L[li][k], 0 on and above the diagonal
+    const float nlk = -lk;
     row[k] = (li == k) ? dk : ((li > k) ? lk : row[k]);
     [&]<int... cs>(std::integer_sequence<int, cs...>) {
-      ((cs > k ? (void)(row[cs] -= lk * row_bcast<cs>(row[k])) : (void)0), ...);
+      ((cs > k ? (void)(row[cs] = __builtin_fmaf(row_bcast<cs>(row[k]), nlk, row[cs])) : (void)0), ...);
     }(std::make_integer_sequence<int, P>{});
   };
   [&]<int... ks>(std::integer_sequence<int, ks...>) {
     (step(std::integral_constant<int, ks>{}), ...);
   }(std::make_integer_sequence<int, P>{});
   // X = L^-1 by forward substitution, lane c computing column c
-  float x[P];
+  float x[P], nx[P];
   auto fwd = [&](auto kc) {
     constexpr int k = decltype(kc)::value;
     float acc = (k == li) ? 1.0f : 0.0f;
     [&]<int... ms>(std::integer_sequence<int, ms...>) {
-      ((ms < k ? (void)(acc -= row_bcast<k>(row[ms]) * x[ms]) : (void)0), ...);
+      ((ms < k ? (void)(acc = __builtin_fmaf(row_bcast<k>(row[ms]), nx[ms], acc)) : (void)0), ...);
     }(std::make_integer_sequence<int, P>{});
     x[k] = acc * row_bcast<k>(rdl);
+    nx[k] = -x[k];
   };
   [&]<int... ks>(std::integer_sequence<int, ks...>) {
     (fwd(std::integral_constant<int, ks>{}), ...);

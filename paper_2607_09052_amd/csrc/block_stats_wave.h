@@ -260,17 +260,11 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     for (int t = 0; t < NT16; ++t)
 #pragma unroll
       for (int c = 0; c < KC; ++c) {
+        float x[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = g[2 * c + i / 4][t][i % 4];
         sbf16x8_t parts[3];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          float x = g[2 * c + i / 4][t][i % 4];
-#pragma unroll
-          for (int part = 0; part < 3; ++part) {
-            const uint32_t hb = f32_to_bf16_rne(x);
-            parts[part][i] = __builtin_bit_cast(__bf16, (uint16_t)hb);
-            x -= __uint_as_float(hb << 16);
-          }
-        }
+        split_bf16x8<3>(x, parts);
 #pragma unroll
         for (int part = 0; part < 3; ++part) {
           if (GLDS || part == 2) gpl[(((GLDS ? part : 0) * NT16 + t) * KC + c) * 64 + lane] = parts[part];
@@ -288,32 +282,34 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     // absorbs); the last one (exact) feeds the Rayleigh-Ritz step and takes
     // all terms down to 2^-24.
     auto product = [&](const f32x4_t* src, f32x4_t* dst, bool exact) {
-      sbf16x8_t wp[3][KC];
+      sbf16x8_t wp[KC][3];
 #pragma unroll
-      for (int c = 0; c < KC; ++c)
+      for (int c = 0; c < KC; ++c) {
+        float x[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          float x = src[2 * c + i / 4][i % 4];
-#pragma unroll
-          for (int part = 0; part < 3; ++part) {
-            const uint32_t hb = f32_to_bf16_rne(x);
-            wp[part][c][i] = __builtin_bit_cast(__bf16, (uint16_t)hb);
-            x -= __uint_as_float(hb << 16);
-          }
+        for (int i = 0; i < 8; ++i) x[i] = src[2 * c + i / 4][i % 4];
+        if (exact) {
+          split_bf16x8<3>(x, wp[c]);
+        } else {
+          sbf16x8_t two[2];
+          split_bf16x8<2>(x, two);
+          wp[c][0] = two[0];
+          wp[c][1] = two[1];
         }
+      }
 #pragma unroll
       for (int t = 0; t < NT16; ++t) {
         f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
           if (exact) {
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(2, t, c), wp[0][c], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[1][c], acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[2][c], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(2, t, c), wp[c][0], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[c][1], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[c][2], acc, 0, 0, 0);
           }
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[0][c], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[1][c], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[0][c], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[c][0], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[c][1], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[c][0], acc, 0, 0, 0);
         }
 #pragma unroll
         for (int v = 0; v < 4; ++v) dst[t][v] = acc[v] * gsc;

@@ -56,11 +56,43 @@ typedef __bf16 sbf16x8_t __attribute__((ext_vector_type(8)));
 __device__ __forceinline__ float bf16_lo(uint32_t x) { return __uint_as_float(x << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
 
-// Round-to-nearest-even fp32 -> bf16 bits (finite inputs).
+// Round-to-nearest-even fp32 -> bf16 bits, in the low half: the hardware
+// conversion, which for every finite input (denormals included) equals rounding
+// the bit pattern, u + 0x7fff + bit 16 of u, to its top half.
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return u >> 16;
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+
+typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
+typedef float f32x2v_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4v_t __attribute__((ext_vector_type(4)));
+
+// Two floats as one packed bf16 pair (a in the low half), one conversion.
+__device__ __forceinline__ uint32_t f32x2_to_bf16x2_rne(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2v_t{a, b}, bf16x2v_t));
+}
+
+// Eight floats as NP bf16 operands whose sum is each float up to the last
+// part's rounding: part k is the round-to-nearest-even of what parts 0..k-1
+// leave (the differences are exact in fp32).  NP = 3 represents every fp32
+// value exactly.
+template <int NP>
+__device__ __forceinline__ void split_bf16x8(const float (&x)[8], sbf16x8_t (&out)[NP]) {
+  float r[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = x[i];
+#pragma unroll
+  for (int k = 0; k < NP; ++k) {
+    u32x4v_t w;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t pr = f32x2_to_bf16x2_rne(r[2 * j], r[2 * j + 1]);
+      r[2 * j] -= bf16_lo(pr);
+      r[2 * j + 1] -= bf16_hi(pr);
+      w[j] = pr;
+    }
+    out[k] = __builtin_bit_cast(sbf16x8_t, w);
+  }
 }
 
 // E2M1 code (4 bits) -> value without scale: 1 sign bit, 2 exponent bits (bias 1),

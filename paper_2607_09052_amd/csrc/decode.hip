@@ -484,14 +484,13 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
   bf16x8_t qhi[KST], qlo[KST];
 #pragma unroll
   for (int kk = 0; kk < KST; ++kk) {
+    float x[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float x = (hcol < G) ? qs[hcol < G ? hcol : 0][32 * kk + 8 * lgrp + j] : 0.0f;
-      const uint32_t hb = f32_to_bf16_rne(x);
-      const uint32_t lb = f32_to_bf16_rne(x - __uint_as_float(hb << 16));
-      qhi[kk][j] = __builtin_bit_cast(__bf16, (uint16_t)hb);
-      qlo[kk][j] = __builtin_bit_cast(__bf16, (uint16_t)lb);
-    }
+    for (int j = 0; j < 8; ++j) x[j] = (hcol < G) ? qs[hcol < G ? hcol : 0][32 * kk + 8 * lgrp + j] : 0.0f;
+    bf16x8_t qp[2];
+    split_bf16x8<2>(x, qp);
+    qhi[kk] = qp[0];
+    qlo[kk] = qp[1];
   }
 
   const char* kbase = static_cast<const char*>(p.kv.k);
@@ -599,15 +598,12 @@ __device__ __forceinline__ void decode_mfma_task(const DecodeParams& p, int b, i
       // is where the score tile left that lane's probabilities, so P (split into
       // bf16 high and low parts) is the B operand as it is; V is read from LDS
       // by column.
-      bf16x8_t phi, plo;
+      float px[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float x = (j < 4) ? sc[0][j] : sc[1][j - 4];
-        const uint32_t hb = f32_to_bf16_rne(x);
-        const uint32_t lb = f32_to_bf16_rne(x - __uint_as_float(hb << 16));
-        phi[j] = __builtin_bit_cast(__bf16, (uint16_t)hb);
-        plo[j] = __builtin_bit_cast(__bf16, (uint16_t)lb);
-      }
+      for (int j = 0; j < 8; ++j) px[j] = (j < 4) ? sc[0][j] : sc[1][j - 4];
+      bf16x8_t pp[2];
+      split_bf16x8<2>(px, pp);
+      const bf16x8_t phi = pp[0], plo = pp[1];
       __builtin_amdgcn_s_waitcnt(0);       // the V tile has landed in LDS
       wave_lds_sync();
 #pragma unroll
