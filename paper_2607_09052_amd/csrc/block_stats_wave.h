@@ -17,11 +17,12 @@
 //     result of a product is the B operand of the next one, so the power
 //     iteration's products need no LDS.  Y^T Y takes the same registers as
 //     both operands.  The products Gamma W run on the bf16 matrix cores with
-//     Gamma and W each split into three bf16 parts (hi + mid + lo, the fp32
-//     value exactly).  Only the re-orthonormalisation W = Y N X^T (the
-//     Cholesky of cholesky_inverse), the Rayleigh-Ritz matrix, the Jacobi
-//     rotations and the factors go through the wave's LDS; Jacobi applies its
-//     rotations as matrix-core products on registers.
+//     Gamma and W each split into bf16 parts (hi + mid + lo, the fp32 value
+//     exactly; the early iterations take the high parts alone).  Only the
+//     re-orthonormalisation W = Y N X^T (the Cholesky of cholesky_inverse),
+//     the Rayleigh-Ritz matrix, Jacobi's stop test and the factors go through
+//     the wave's LDS; Jacobi forms its rotations from lane permutes and applies
+//     them as matrix-core products on registers.
 //   * Factors: lane l owns columns (d / 64) l .. of xi and reads those columns
 //     of every key (a second pass over the block in L2).
 #pragma once
@@ -75,8 +76,7 @@ struct WaveStatsLds {
   static constexpr size_t vm = al(hm + 4 * P * PS);        // [P][PS]
   static constexpr size_t wr = al(vm + 4 * P * PS);        // [4][LB] Ritz vectors
   static constexpr size_t xi = al(wr + 4 * 4 * LB);        // [4][D] factors
-  static constexpr size_t jac = al(xi + 4 * 4 * D);        // Jacobi rotations: c, s per pair [P/2][2]
-  static constexpr size_t chk = al(jac + 4 * 3 * P);       // Jacobi stop test: diagonal [P], ranks [P], threshold
+  static constexpr size_t chk = al(xi + 4 * 4 * D);        // Jacobi stop test: diagonal [P], ranks [P], threshold
   static constexpr size_t late = al(chk + 4 * (2 * P + 4));
   static constexpr size_t bytes = mx(late, gparts + part_bytes);
   static constexpr size_t bytes_glds = mx(late, gparts + 3 * part_bytes);
@@ -84,6 +84,10 @@ struct WaveStatsLds {
 
 template <int D, int LB, bool GLDS = false>
 constexpr size_t wave_stats_lds_bytes() { return GLDS ? WaveStatsLds<D, LB>::bytes_glds : WaveStatsLds<D, LB>::bytes; }
+
+// Power iterations whose products take only the high bf16 parts of Gamma and W
+// (the first 16 of the 22 products with Gamma).
+constexpr int kHiIters = 9;
 
 // The configurations block_stats_wave covers.
 __host__ __device__ inline bool wave_stats_applies(int r, int lsh, bool subspace) {
@@ -117,7 +121,6 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
   int* crank = reinterpret_cast<int*>(pool + Lay::chk) + P;
   float* Wr = reinterpret_cast<float*>(pool + Lay::wr);
   float* Xi = reinterpret_cast<float*>(pool + Lay::xi);
-  float* rot = reinterpret_cast<float*>(pool + Lay::jac);
   int* order = reinterpret_cast<int*>(pool + Lay::misc);
   float* ritzval = reinterpret_cast<float*>(pool + Lay::misc) + 4;
   float* skw = reinterpret_cast<float*>(pool + Lay::misc) + 8;
@@ -277,24 +280,29 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     };
     wave_lds_sync();
     // dst = (Gamma / trace) src, both in the result layout: row 16 t + 4 lk + v,
-    // column lr.  The power iteration's products take the three leading
-    // cross terms of the bf16 parts (relative error ~1e-5, which the iteration
-    // absorbs); the last one (exact) feeds the Rayleigh-Ritz step and takes
-    // all terms down to 2^-24.
-    auto product = [&](const f32x4_t* src, f32x4_t* dst, bool exact) {
+    // column lr.  Terms of the bf16 parts by iteration: the first kHiIters
+    // iterations (16 of the 22 products) take the high parts alone (relative
+    // error ~4e-3, which the later products damp out of the subspace), the
+    // next ones the three leading cross terms (~1e-5), and the last product,
+    // which feeds the Rayleigh-Ritz step, all terms down to 2^-24.
+    auto product = [&](const f32x4_t* src, f32x4_t* dst, int terms) {
       sbf16x8_t wp[KC][3];
 #pragma unroll
       for (int c = 0; c < KC; ++c) {
         float x[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) x[i] = src[2 * c + i / 4][i % 4];
-        if (exact) {
+        if (terms == 6) {
           split_bf16x8<3>(x, wp[c]);
-        } else {
+        } else if (terms == 3) {
           sbf16x8_t two[2];
           split_bf16x8<2>(x, two);
           wp[c][0] = two[0];
           wp[c][1] = two[1];
+        } else {
+          sbf16x8_t one[1];
+          split_bf16x8<1>(x, one);
+          wp[c][0] = one[0];
         }
       }
 #pragma unroll
@@ -302,13 +310,15 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
         f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int c = 0; c < KC; ++c) {
-          if (exact) {
+          if (terms == 6) {
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(2, t, c), wp[c][0], acc, 0, 0, 0);
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[c][1], acc, 0, 0, 0);
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[c][2], acc, 0, 0, 0);
           }
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[c][0], acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[c][1], acc, 0, 0, 0);
+          if (terms >= 3) {
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(1, t, c), wp[c][0], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[c][1], acc, 0, 0, 0);
+          }
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(gpart(0, t, c), wp[c][0], acc, 0, 0, 0);
         }
 #pragma unroll
@@ -343,10 +353,11 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
       for (int v = 0; v < 4; ++v) w[a][v] = init_sign(16 * a + 4 * lk + v, lr);
 #pragma unroll 1
     for (int it = 0; it <= kPowerIters; ++it) {
-      product(w, y, it == kPowerIters);
+      const int terms = it == kPowerIters ? 6 : (it < kHiIters ? 1 : 3);
+      product(w, y, terms);
       if (it == kPowerIters) break;      // the last product feeds the Rayleigh-Ritz step
       if (it >= kSinglePowerIters) {       // Gamma^2 W (W is replaced below)
-        product(y, w, false);
+        product(y, w, terms);
 #pragma unroll
         for (int t = 0; t < NT16; ++t) y[t] = w[t];
       }
@@ -386,7 +397,8 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     // [4 lk + v][lr]); a round is H <- J^T (H J) and V^T <- J^T V^T, twelve
     // matrix-core products, with J (the round's eight rotations) built in the
     // same layout.  By symmetry H's layout is also the A operand of H J.
-    // Lanes < P/2 form the rotations from H's entries, passed through LDS.
+    // Each lane forms its column's rotation from H's entries, which it takes
+    // from the lanes holding them by lane permutes.
     // bf16 keys: the factor pass's words (the lane's EPL columns of every row)
     // load during Jacobi, which does not touch memory
     constexpr bool kPre = !KF32 && !GLDS;
@@ -458,39 +470,35 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
       bool moved = false;
 #pragma unroll 1
       for (int rnd = 0; rnd < P - 1; ++rnd) {
-#pragma unroll
-        for (int v = 0; v < 4; ++v) Hm[(4 * lk + v) * PS + lr] = hr[v];
-        wave_lds_sync();
-        bool big = false;
-        if (lane < P / 2) {
-          const int x = slot_index(lane, rnd), yy = slot_index(P - 1 - lane, rnd);
-          const int pp = min(x, yy), qq = max(x, yy);
-          const float app = Hm[pp * PS + pp], aqq = Hm[qq * PS + qq], apq = Hm[pp * PS + qq];
-          big = fabsf(apq) > 1e-6f * sqrtf(fmaxf(app, 0.0f) * fmaxf(aqq, 0.0f)) && fabsf(apq) > 2e-8f;
-          float c = 1.0f, sn = 0.0f;
-          if (apq != 0.0f) {
-            const float th = (aqq - app) * __builtin_amdgcn_rcpf(2.0f * apq);
-            const float tt = (th >= 0.0f ? 1.0f : -1.0f) * __builtin_amdgcn_rcpf(fabsf(th) + sqrtf(th * th + 1.0f));
-            c = __builtin_amdgcn_rsqf(tt * tt + 1.0f);
-            sn = tt * c;
-          }
-          rot[2 * lane] = c;
-          rot[2 * lane + 1] = sn;
+        // the round's pair of this lane's column: (pp, qq), lr's partner py.
+        // The diagonal entry of column y sits in lane 16 (y / 4) + y, register
+        // y % 4; H[pp][qq] in lane 16 (pp / 4) + qq, register pp % 4 (there the
+        // column's partner's register).  Every lane forms its pair's rotation.
+        const int py = slot_index(P - 1 - index_slot(lr, rnd), rnd);
+        const int pp = min(lr, py), qq = max(lr, py);
+        auto reg = [&](int k) { return k == 0 ? hr[0] : k == 1 ? hr[1] : k == 2 ? hr[2] : hr[3]; };
+        const float dsel = reg(lr & 3), osel = reg(py & 3);
+        auto from = [&](float x, int src) {
+          return __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(x)));
+        };
+        const float app = from(dsel, 16 * (pp >> 2) + pp);
+        const float aqq = from(dsel, 16 * (qq >> 2) + qq);
+        const float apq = from(osel, 16 * (pp >> 2) + qq);
+        const bool big = fabsf(apq) > 1e-6f * sqrtf(fmaxf(app, 0.0f) * fmaxf(aqq, 0.0f)) && fabsf(apq) > 2e-8f;
+        float c = 1.0f, sn = 0.0f;
+        if (apq != 0.0f) {
+          const float th = (aqq - app) * __builtin_amdgcn_rcpf(2.0f * apq);
+          const float tt = (th >= 0.0f ? 1.0f : -1.0f) * __builtin_amdgcn_rcpf(fabsf(th) + sqrtf(th * th + 1.0f));
+          c = __builtin_amdgcn_rsqf(tt * tt + 1.0f);
+          sn = tt * c;
         }
         moved = moved || __ballot(big) != 0;
-        wave_lds_sync();
         // J[x][y]: c on the diagonal; at y = partner(x), -s if y < x else s
         f32x4_t jr;
-        {
-          const int my = index_slot(lr, rnd), mpy = P - 1 - my;
-          const int py = slot_index(mpy, rnd);
-          const int pr = min(my, mpy);
-          const float c = rot[2 * pr], sn = rot[2 * pr + 1];
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            const int x = 4 * lk + v;
-            jr[v] = (x == lr) ? c : ((x == py) ? ((lr < x) ? -sn : sn) : 0.0f);
-          }
+        for (int v = 0; v < 4; ++v) {
+          const int x = 4 * lk + v;
+          jr[v] = (x == lr) ? c : ((x == py) ? ((lr < x) ? -sn : sn) : 0.0f);
         }
         f32x4_t m4 = {0.0f, 0.0f, 0.0f, 0.0f}, h2 = m4, v2 = m4;
 #pragma unroll
