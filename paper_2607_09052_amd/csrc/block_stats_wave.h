@@ -96,10 +96,9 @@ __host__ __device__ inline bool wave_stats_applies(int r, int lsh, bool subspace
 
 // One block by the calling wave (lane = threadIdx.x % 64; every lane of the
 // wave calls it; no workgroup barrier inside).  `pool`: the wave's
-// wave_stats_lds_bytes<D, LB, GLDS>() bytes of LDS.  GLDS: Gamma's bf16 parts
-// live in LDS and the factor pass loads its keys when it runs (fewer
-// registers, for a caller that has other work in flight); the operations and
-// so the record are the same either way.
+// wave_stats_lds_bytes<D, LB, GLDS>() bytes of LDS.  GLDS: all three of
+// Gamma's bf16 parts live in LDS (fewer registers, for a caller that has other
+// work in flight); the operations and so the record are the same either way.
 template <int D, int LB, bool KF32, bool GLDS = false>
 __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int h, int j, int n, char* pool) {
   static_assert(LB == 32 || LB == 64, "blocks of 32 or 64 tokens");
@@ -399,22 +398,6 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     // same layout.  By symmetry H's layout is also the A operand of H J.
     // Each lane forms its column's rotation from H's entries, which it takes
     // from the lanes holding them by lane permutes.
-    // bf16 keys: the factor pass's words (the lane's EPL columns of every row)
-    // load during Jacobi, which does not touch memory
-    constexpr bool kPre = !KF32 && !GLDS;
-    uint32_t xraw[kPre ? LB : 1];
-    // (a block whose page is outside the pool reads page 0, which always
-    // exists, and masks the words to zero keys)
-    const uint32_t kmask = kbase < 0 ? 0u : ~0u;
-    const int64_t kb0 = kbase < 0 ? 0 : kbase;
-    if constexpr (kPre) {
-      const uint16_t* src = static_cast<const uint16_t*>(p.kv.k) + kb0 + EPL * lane;
-#pragma unroll
-      for (int row = 0; row < LB; ++row) {
-        if constexpr (EPL == 2) xraw[row] = *reinterpret_cast<const uint32_t*>(src + row * rs) & kmask;
-        else xraw[row] = src[row * rs] & kmask;
-      }
-    }
     auto slot_index = [&](int m, int rnd) { return m == 0 ? 0 : 1 + (m - 1 + rnd) % (P - 1); };
     auto index_slot = [&](int x, int rnd) { return x == 0 ? 0 : 1 + (x - 1 + (P - 1) - rnd) % (P - 1); };
     f32x4_t hr, vt;
@@ -557,35 +540,13 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int c = 0; c < EPL; ++c) xs[i][c] = 0.0f;
-      if constexpr (kPre) {
-#pragma unroll
-        for (int r4 = 0; r4 < LB; r4 += 4) {
-          float4 w4[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            w4[i] = *reinterpret_cast<const float4*>(Wr + i * LB + r4);
-#pragma unroll
-          for (int rr = 0; rr < 4; ++rr) {
-            const int row = r4 + rr;
-            float kx[EPL];
-            if constexpr (EPL == 2) {
-              kx[0] = bf16_lo(xraw[row]);
-              kx[1] = bf16_hi(xraw[row]);
-            } else {
-              kx[0] = bf16_lo(xraw[row]);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const float wi = rr == 0 ? w4[i].x : rr == 1 ? w4[i].y : rr == 2 ? w4[i].z : w4[i].w;
-#pragma unroll
-              for (int c = 0; c < EPL; ++c) xs[i][c] += (kx[c] - mc[c]) * wi;
-            }
-          }
-        }
-      }
-      // otherwise the lane's columns of 16 rows at a time, their loads in flight together
+      // the lane's columns of 16 rows at a time, their loads in flight
+      // together (a block whose page is outside the pool reads page 0, which
+      // always exists, and masks the words to zero keys)
+      const uint32_t kmask = kbase < 0 ? 0u : ~0u;
+      const int64_t kb0 = kbase < 0 ? 0 : kbase;
 #pragma unroll 1
-      for (int r0 = 0; !kPre && r0 < LB; r0 += 16) {
+      for (int r0 = 0; r0 < LB; r0 += 16) {
         float kv_[16][EPL];
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
