@@ -59,9 +59,39 @@ __device__ __forceinline__ float init_sign(int i, int p) {
   return (h & 1u) ? 1.0f : -1.0f;
 }
 
+// E2M1 scale of one vector of `len` fp32 values held in LDS: fp32(max|x|)/6,
+// by one wave (every lane gets it).
+__device__ __forceinline__ float e2m1_scale_wave(const float* x, int len, int lane) {
+  float m = 0.0f;
+  for (int e = lane; e < len; e += 64) m = fmaxf(m, fabsf(x[e]));
+  return wave_max_rows(m) / 6.0f;
+}
+
 // Encode one vector of `len` fp32 values held in LDS (`x`, len a multiple of
-// 8) into `dst` with the given storage dtype, by one wave (no barriers).  For
-// E2M1 the scale fp32(max|x|)/6 is written to *scale_dst.
+// 8) into `dst` with the given storage dtype, by one wave (no barriers); E2M1
+// codes with the given scale (e2m1_scale_wave).
+__device__ __forceinline__ void store_vector_codes_wave(const float* x, int len, int dt, uint8_t* dst, float scale,
+                                                        int lane) {
+  if (dt == DT_F32) {
+    for (int e = lane; e < len; e += 64) reinterpret_cast<float*>(dst)[e] = x[e];
+    return;
+  }
+  if (dt == DT_BF16) {
+    for (int e = lane; e < len / 2; e += 64)
+      reinterpret_cast<uint32_t*>(dst)[e] = f32x2_to_bf16x2_rne(x[2 * e], x[2 * e + 1]);
+    return;
+  }
+  for (int e = lane; e < len / 8; e += 64) {
+    uint32_t w = 0;
+    if (scale > 0.0f) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) w |= e2m1_code(x[8 * e + j], scale) << (4 * j);
+    }
+    reinterpret_cast<uint32_t*>(dst)[e] = w;
+  }
+}
+
+// The same, with the E2M1 scale written to *scale_dst.
 __device__ __forceinline__ void store_vector_wave(const float* x, int len, int dt, uint8_t* dst, float* scale_dst,
                                                   int lane) {
   if (dt == DT_F32) {

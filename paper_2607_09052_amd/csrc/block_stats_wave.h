@@ -31,22 +31,37 @@
 
 namespace cobs {
 
-// The record of a block by one wave: the header (count; scales and skew
-// coefficients default 0), then, once those stores are done, every stored
-// vector (mean, nr factors from Xi, value mean) and zeros up to the record size.
+// Largest rank the one-wave routine takes.
+constexpr int kMaxWaveRank = 4;
+
+// The record of a block by one wave: the E2M1 scales first, then the header
+// (count, scales, skew coefficients, zeros) and every stored vector (mean, nr
+// factors from Xi, value mean) with zeros up to the record size, each byte
+// written once.
 template <int D>
 __device__ __forceinline__ void write_record_wave(const StatsArgs& p, uint8_t* R, int n, int nr, const float* mean,
                                                   const float* Xi, const float* vmean, const float* skw, int lane) {
   const RecLayout lay = p.lay;
-  for (int idx = lane; idx < lay.mean_off / 4; idx += 64)
-    reinterpret_cast<uint32_t*>(R)[idx] = (idx == 0) ? (uint32_t)n : 0u;
-  __builtin_amdgcn_s_waitcnt(0);
-  if (nr > 0 && p.skew && lane < nr) reinterpret_cast<float*>(R + lay.skew_off)[lane] = skw[lane];
-  store_vector_wave(mean, D, p.mdt, R + lay.mean_off, reinterpret_cast<float*>(R + 4), lane);
+  const bool me2 = p.mdt == DT_E2M1, fe2 = p.fdt == DT_E2M1;
+  const float msc = me2 ? e2m1_scale_wave(mean, D, lane) : 0.0f;
+  const float vsc = (me2 && p.vmean) ? e2m1_scale_wave(vmean, D, lane) : 0.0f;
+  float fsc[kMaxWaveRank];
+#pragma unroll
+  for (int vi = 0; vi < kMaxWaveRank; ++vi) fsc[vi] = (fe2 && vi < nr) ? e2m1_scale_wave(&Xi[vi * D], D, lane) : 0.0f;
+  for (int idx = lane; idx < lay.mean_off / 4; idx += 64) {
+    uint32_t w = 0u;
+    if (idx == 0) w = (uint32_t)n;
+    else if (idx == 1) w = __float_as_uint(msc);
+    else if (idx == 2) w = __float_as_uint(vsc);
+    else if (idx >= 4 && idx < 4 + nr && fe2) w = __float_as_uint(idx == 4 ? fsc[0] : idx == 5 ? fsc[1] : idx == 6 ? fsc[2] : fsc[3]);
+    else if (p.skew && idx >= lay.skew_off / 4 && idx < lay.skew_off / 4 + nr) w = __float_as_uint(skw[idx - lay.skew_off / 4]);
+    reinterpret_cast<uint32_t*>(R)[idx] = w;
+  }
+  store_vector_codes_wave(mean, D, p.mdt, R + lay.mean_off, msc, lane);
   for (int vi = 0; vi < nr; ++vi)
-    store_vector_wave(&Xi[vi * D], D, p.fdt, R + lay.fac_off + vi * lay.vec_bytes,
-                      reinterpret_cast<float*>(R + 16) + vi, lane);
-  if (p.vmean) store_vector_wave(vmean, D, p.mdt, R + lay.vmean_off, reinterpret_cast<float*>(R + 8), lane);
+    store_vector_codes_wave(&Xi[vi * D], D, p.fdt, R + lay.fac_off + vi * lay.vec_bytes,
+                            vi == 0 ? fsc[0] : vi == 1 ? fsc[1] : vi == 2 ? fsc[2] : fsc[3], lane);
+  if (p.vmean) store_vector_codes_wave(vmean, D, p.mdt, R + lay.vmean_off, vsc, lane);
   // factors of a block without them, and the padding after the last vector
   const int fac_end = lay.fac_off + nr * lay.vec_bytes;
   for (int idx = fac_end / 4 + lane; idx < lay.vmean_off / 4; idx += 64) reinterpret_cast<uint32_t*>(R)[idx] = 0u;
@@ -91,7 +106,7 @@ constexpr int kHiIters = 9;
 
 // The configurations block_stats_wave covers.
 __host__ __device__ inline bool wave_stats_applies(int r, int lsh, bool subspace) {
-  return r <= 4 && (lsh == 5 || lsh == 6) && !subspace;
+  return r <= kMaxWaveRank && (lsh == 5 || lsh == 6) && !subspace;
 }
 
 // One block by the calling wave (lane = threadIdx.x % 64; every lane of the
@@ -659,37 +674,71 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
 }
 
 // A block with fewer than LB tokens (count and means only, zero factors) by a
-// 256-thread workgroup: the column means are exact fp64 sums rounded once, so
-// the record is bitwise the one block_stats_wave writes.  `pool`: at least
-// block_mean_lds_bytes<D>() bytes of LDS.
+// 256-thread workgroup.  Thread t reads 16-byte pieces (8 columns) of rows
+// t / (D/8), + 256/(D/8), ..., all of its loads (keys and values) in flight
+// together; the partial sums of the row groups meet in LDS.  The column means
+// are fp64 sums rounded once, exact (so in any order) unless the block's
+// magnitudes span > 2^29, so the record is bitwise the one block_stats_wave
+// writes.  `pool`: at least block_mean_lds_bytes<D>() bytes of LDS.
 template <int D>
-constexpr size_t block_mean_lds_bytes() { return 8 * 256 + 8 * D; }
+constexpr int block_mean_row_groups() { return 256 / (D / 8); }
+
+template <int D>
+constexpr size_t block_mean_lds_bytes() { return 8 * (size_t)block_mean_row_groups<D>() * D + 8 * D; }
 
 template <int D, int LB>
 __device__ __forceinline__ void block_mean_wg(const StatsArgs& p, int b, int h, int j, int n, char* pool) {
-  static_assert(256 % D == 0, "whole columns per thread group");
-  constexpr int NH = 256 / D;                  // threads per column
-  double* sums = reinterpret_cast<double*>(pool);             // [NH][D]
-  float* mean = reinterpret_cast<float*>(pool + 8 * 256);     // [D]
+  constexpr int TPR = D / 8;                                  // threads per row
+  constexpr int RG = block_mean_row_groups<D>();              // rows per pass
+  constexpr int NP = (LB + RG - 1) / RG;                      // passes over the block
+  double* sums = reinterpret_cast<double*>(pool);             // [RG][D]
+  float* mean = reinterpret_cast<float*>(pool + 8 * RG * D);  // [D]
   float* vmean = mean + D;                                    // [D]
-  const int tid = threadIdx.x, e = tid % D, part = tid / D;
-  const int64_t kbase = kv_offset(p.kv, b, h, j * LB);     // a page holds one block
+  const int tid = threadIdx.x, cc = tid % TPR, rg = tid / TPR;
+  const int64_t kbase = kv_offset(p.kv, b, h, j * LB);       // a page holds one block
   const int64_t rs = p.kv.table ? (int64_t)p.kv.d : p.kv.st;
-  auto column_mean = [&](const uint16_t* base, float* out) {
-    double s = 0.0;
-    for (int i = part; kbase >= 0 && i < n; i += NH) s += (double)__uint_as_float((uint32_t)base[kbase + i * rs + e] << 16);
-    sums[part * D + e] = s;
+  // rows past n (n >= 1), and a block whose page is outside the pool, read a
+  // valid row and count zero
+  const int64_t kb0 = kbase < 0 ? 0 : kbase;
+  auto load = [&](const void* base, uint4* w) {
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const int row = rg + q * RG;
+      const uint4 x = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + kb0 +
+                                                       (int64_t)min(row, n - 1) * rs + 8 * cc);
+      const bool ok = kbase >= 0 && row < n;
+      w[q] = ok ? x : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  uint4 kw[NP], vw[NP];
+  load(p.kv.k, kw);
+  if (p.vmean) load(p.kv.v, vw);
+  auto column_mean = [&](const uint4* w, float* out) {
+    double s[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s[e] = 0.0;
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const uint32_t u[4] = {w[q].x, w[q].y, w[q].z, w[q].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        s[2 * k] += (double)bf16_lo(u[k]);
+        s[2 * k + 1] += (double)bf16_hi(u[k]);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) sums[rg * D + 8 * cc + e] = s[e];
     __syncthreads();
     if (tid < D) {
       double t = 0.0;
 #pragma unroll
-      for (int q = 0; q < NH; ++q) t += sums[q * D + tid];
+      for (int q = 0; q < RG; ++q) t += sums[q * D + tid];
       out[tid] = (float)(t / (double)n);
     }
     __syncthreads();
   };
-  column_mean(static_cast<const uint16_t*>(p.kv.k), mean);
-  if (p.vmean) column_mean(static_cast<const uint16_t*>(p.kv.v), vmean);
+  column_mean(kw, mean);
+  if (p.vmean) column_mean(vw, vmean);
   if (tid < 64) {
     uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
     write_record_wave<D>(p, R, n, 0, mean, nullptr, vmean, nullptr, tid);
