@@ -1,5 +1,7 @@
-// The block statistics build kernel: one 256-thread workgroup per (batch row,
-// KV head, block) of LB tokens.
+// The block statistics build kernels, per (batch row, KV head, block) of LB
+// tokens: one 64-thread wave per block (block_stats_wave: L = 32 or 64, r <= 4,
+// full-space factors) or one 256-thread workgroup per block (block_stats: the
+// other configurations).
 #pragma once
 
 #include "block_stats.h"

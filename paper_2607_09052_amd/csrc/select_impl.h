@@ -803,9 +803,11 @@ __device__ __forceinline__ void select_refresh_task(const SelectParams& p, char*
   else select_task<D, G, 4, MDT, FDT>(p, b, h, chunk, pool);
 }
 
-// Instantiations whose registers fit three workgroups per CU without spills
-// get that cap (the routine's accumulators would otherwise push them to two);
-// the others keep the compiler's choice.
+// Instantiations whose scoring loop fits three workgroups per CU without
+// spills get that cap (the refresh routine's accumulators would otherwise push
+// them to two; with the cap, 22-25 registers of the inlined block statistics
+// go to scratch, outside the scoring loop); the others keep the compiler's
+// choice.
 template <int D, int G, int MDT, int FDT>
 constexpr bool select_refresh_capped() {
   if (MDT != DT_F32 && FDT != DT_F32) return !(D == 128 && FDT == DT_BF16);
