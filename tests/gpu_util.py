@@ -105,7 +105,25 @@ def oracle_decode(q_unit, K_unit, V_unit, T, sel, cfg):
     return M.sparse_attention(q_unit, K_unit, V_unit, U, cfg.scale)
 
 
-def check_out(out_gpu, lse_gpu, out_ora, lse_ora, kv_dtype):
+def score_slack(q_unit, K_unit, T, sel, cfg):
+    """Per query head, the largest error the bf16 score products allow in a
+    score of the attended tokens, and so in the lse: the query reaches the
+    matrix cores as two bf16 parts, each rounded to nearest at 2^-9 relative,
+    so q_hi + q_lo is within 2^-18 |q_e| of every element, the bf16 products
+    are exact in fp32, and a score c q.k moves by at most
+    2^-18 c sum_e |q_e| |k_e|; taken at 2^-17 for margin."""
+    U = M.union_tokens(T, cfg.block_size, cfg.window, sel)
+    if len(U) == 0:
+        return np.zeros(np.asarray(q_unit).shape[0])
+    qa = np.abs(np.asarray(q_unit, dtype=np.float64))
+    ka = np.abs(np.asarray(K_unit, dtype=np.float64)[U])
+    return 2.0 ** -17 * cfg.scale * (qa @ ka.T).max(axis=1)
+
+
+def check_out(out_gpu, lse_gpu, out_ora, lse_ora, kv_dtype, slack=None):
+    """Attention against the oracle: relative L2 of out per head and over the
+    heads; |lse diff| <= 1e-5 max(1, |lse|) plus, for bf16 K/V, `slack`
+    (score_slack: the bf16 split of the query)."""
     tol = OUT_TOL[kv_dtype]
     if np.all(np.isneginf(lse_ora)):
         assert np.all(out_gpu == 0) and np.all(np.isneginf(lse_gpu))
@@ -114,7 +132,10 @@ def check_out(out_gpu, lse_gpu, out_ora, lse_ora, kv_dtype):
         e = rel_l2(out_gpu[g], out_ora[g])
         assert e <= tol, (g, e)
     assert rel_l2(out_gpu, out_ora) <= tol
-    np.testing.assert_allclose(lse_gpu, lse_ora, rtol=0, atol=LSE_TOL * max(1.0, float(np.max(np.abs(lse_ora)))))
+    atol = LSE_TOL * max(1.0, float(np.max(np.abs(lse_ora))))
+    extra = np.zeros(np.asarray(lse_ora).shape) if slack is None or kv_dtype != "bf16" else np.asarray(slack)
+    err = np.abs(np.asarray(lse_gpu, dtype=np.float64) - np.asarray(lse_ora, dtype=np.float64))
+    assert np.all(err <= atol + extra), (err, atol, extra)
 
 
 def cuda(x):

@@ -14,7 +14,7 @@ from oracle import numerics as nx
 from oracle import records as R
 from paper_2607_09052_amd import cobs
 from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_selection, f64, oracle_decode,
-                            ky_fan_checks, oracle_select, rel_l2, say, sync, valid_prefix)
+                            ky_fan_checks, oracle_select, rel_l2, say, score_slack, sync, valid_prefix)
 
 pytestmark = pytest.mark.gpu
 
@@ -309,9 +309,10 @@ def test_sparse_decode_matches_oracle(d, G, kv, s, w):
     out_h, lse_h = out.cpu().numpy(), lse.cpu().numpy()
     for b in range(len(seq)):
         for h in range(Hkv):
-            o, l = oracle_decode(q[b, h * G:(h + 1) * G].double().numpy(), f64(k[b, h]), f64(v[b, h]),
-                                 int(seq[b]), sel[b, h].numpy(), cfg)
-            check_out(out_h[b, h * G:(h + 1) * G], lse_h[b, h * G:(h + 1) * G], o, l, kv)
+            qg = q[b, h * G:(h + 1) * G].double().numpy()
+            o, l = oracle_decode(qg, f64(k[b, h]), f64(v[b, h]), int(seq[b]), sel[b, h].numpy(), cfg)
+            check_out(out_h[b, h * G:(h + 1) * G], lse_h[b, h * G:(h + 1) * G], o, l, kv,
+                      score_slack(qg, f64(k[b, h]), int(seq[b]), sel[b, h].numpy(), cfg))
 
 
 @pytest.mark.parametrize("d,G,s,w", [(128, 4, 6, 256), (128, 8, 10, 100), (64, 2, 0, 128), (128, 1, 5, 0),
@@ -343,8 +344,9 @@ def test_sparse_decode_branches_match_oracle(d, G, s, w, L=64, fill="random"):
             gs = slice(h * G, (h + 1) * G)
             ref = M.branch_attention(q[b, gs].double().numpy(), f64(k[b, h]), f64(v[b, h]), int(seq[b]), L, w,
                                      sel[b, h].numpy(), cfg.scale)
-            check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16")
-            check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16")
+            slack = score_slack(q[b, gs].double().numpy(), f64(k[b, h]), int(seq[b]), sel[b, h].numpy(), cfg)
+            check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16", slack)
+            check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16", slack)
     # the log-sum-exp merge of the branches is the union's attention
     ls64, lw64 = ls.astype(np.float64), lw.astype(np.float64)
     m = np.maximum(ls64, lw64)
@@ -387,9 +389,10 @@ def test_sparse_decode_one_workgroup_per_unit():
     out_h, lse_h = out.cpu().numpy(), lse.cpu().numpy()
     for b in [0, 1, 2, 17, 40, 63]:
         for h in range(Hkv):
-            o, l = oracle_decode(q[b, h * G:(h + 1) * G].double().numpy(), f64(k[b, h]), f64(v[b, h]),
-                                 int(seq[b]), sel[b, h].numpy(), cfg)
-            check_out(out_h[b, h * G:(h + 1) * G], lse_h[b, h * G:(h + 1) * G], o, l, "bf16")
+            qg = q[b, h * G:(h + 1) * G].double().numpy()
+            o, l = oracle_decode(qg, f64(k[b, h]), f64(v[b, h]), int(seq[b]), sel[b, h].numpy(), cfg)
+            check_out(out_h[b, h * G:(h + 1) * G], lse_h[b, h * G:(h + 1) * G], o, l, "bf16",
+                      score_slack(qg, f64(k[b, h]), int(seq[b]), sel[b, h].numpy(), cfg))
 
 
 def test_sparse_decode_edge_cases():
@@ -414,7 +417,8 @@ def test_sparse_decode_edge_cases():
             nc = M.candidate_count(T, 64, wv)
             keep = valid_prefix(sel[b, 0].numpy(), nc)
             o, l = oracle_decode(q[b].double().numpy(), f64(k[b, 0]), f64(v[b, 0]), T, keep, cfg)
-            check_out(out[b].cpu().numpy(), lse[b].cpu().numpy(), o, l, "bf16")
+            check_out(out[b].cpu().numpy(), lse[b].cpu().numpy(), o, l, "bf16",
+                      score_slack(q[b].double().numpy(), f64(k[b, 0]), T, keep, cfg))
 
 
 def test_paged_kv_matches_contiguous():

@@ -21,7 +21,7 @@ from oracle import method as M
 from oracle import records as R
 from paper_2607_09052_amd import cobs
 from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_records, check_selection, f32_config, f64,
-                            oracle_decode, oracle_select, say, subspace_sigma_bound, sync)
+                            oracle_decode, oracle_select, say, score_slack, subspace_sigma_bound, sync)
 
 pytestmark = pytest.mark.gpu
 
@@ -186,7 +186,8 @@ def _check(c, data_seed, tag):
             if c["s"] > 0:
                 check_selection(sel_h[b, h], sigma, nc, c["s"])
             o, l = oracle_decode(q[b, gs].double().numpy(), f64(k[b, h]), f64(v[b, h]), T, sel_h[b, h], cfg)
-            check_out(out_h[b, gs], lse_h[b, gs], o, l, c["kv"])
+            check_out(out_h[b, gs], lse_h[b, gs], o, l, c["kv"],
+                      score_slack(q[b, gs].double().numpy(), f64(k[b, h]), T, sel_h[b, h], cfg))
             if cfg.value_mean:
                 nb = -(-T // L)
                 parts = R.decode(rec_h[b, h, :nb], d, cfg.rank, c["md"], c["fd"], cfg.skew, True, c.get("sd") or None)
@@ -245,8 +246,9 @@ def test_random_diagnostic_entry_points(seed):
                 if s > 0:
                     check_selection(sel[b, h, :s].cpu().numpy(), sigma, nc, s)
             ref = M.branch_attention(qg, Kg, f64(v[b, h]), T, L, w, sel_e[b, h].cpu().numpy(), cfg.scale)
-            check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16")
-            check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16")
+            slack = score_slack(qg, Kg, T, sel_e[b, h].cpu().numpy(), cfg)
+            check_out(hs[b, gs], ls[b, gs], ref[0], ref[1], "bf16", slack)
+            check_out(hw[b, gs], lw[b, gs], ref[2], ref[3], "bf16", slack)
 
 
 @pytest.mark.parametrize("seed", list(range(int(_N) if _N else 6)))

@@ -29,7 +29,7 @@ import synth
 from oracle import method as M
 from paper_2607_09052_amd import cobs
 from tests.gpu_util import (DEV, SIGMA_TOL, check_out, check_records, check_selection, config_from, f32_config,
-                            f64, oracle_decode, oracle_select, say, sync)
+                            f64, oracle_decode, oracle_select, say, score_slack, sync)
 
 pytestmark = pytest.mark.gpu
 
@@ -69,7 +69,7 @@ def _shared_bytes_check(cfg, rec_u, q_u, K_u, V_u, T, sel_u, out_u, lse_u, score
         assert np.all(np.abs(scores_u[:nc] - sigma[:nc]) <= SIGMA_TOL), float(np.max(np.abs(scores_u[:nc] - sigma[:nc])))
     exact = check_selection(sel_u, sigma, nc, cfg.budget)
     o, l = oracle_decode(q_u, K_u, V_u, T, sel_u, cfg)
-    check_out(out_u, lse_u, o, l, cfg.kv_dtype)
+    check_out(out_u, lse_u, o, l, cfg.kv_dtype, score_slack(q_u, K_u, T, sel_u, cfg))
     return exact
 
 
@@ -150,7 +150,9 @@ def _run_case(name, seed, units=None, **over):
     sync()
     for (b, h), res in ora.items():
         sl = slice(h * G, (h + 1) * G)
-        check_out(out_o[b, sl].cpu().numpy(), lse_o[b, sl].cpu().numpy(), res["out"], res["lse"], cfg.kv_dtype)
+        qu = f64(q[b, h * G:(h + 1) * G])
+        check_out(out_o[b, sl].cpu().numpy(), lse_o[b, sl].cpu().numpy(), res["out"], res["lse"], cfg.kv_dtype,
+                  score_slack(qu, f64(k[b, h, :T]), T, res["sel"], cfg))
     return prob, sel, ora
 
 
