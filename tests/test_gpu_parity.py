@@ -461,6 +461,57 @@ def test_paged_kv_matches_contiguous():
     assert torch.equal(outs[0], outs[1])
 
 
+
+@pytest.mark.parametrize("dt", [("bf16", "bf16"), ("e2m1", "e2m1"), ("f32", "f32")])
+def test_paged_ids_outside_the_pool_read_as_zero_keys(dt):
+    """Page ids outside [0, num_pages) are never dereferenced: the build reads
+    such a block as zero keys (a full block: its count, zero mean and zero
+    factors; the ragged newest block: its count and zero mean), and the decode
+    step's refresh of the newest block writes the same record.  Reference: the
+    contiguous cache with those blocks' keys and values zeroed."""
+    d, G, Hkv, Tmax = 128, 4, 2, 1024
+    seq = np.array([1024, 700], np.int32)
+    md, fd = dt
+    prob = _decode_problem(d, G, "bf16", seq, Hkv, Tmax, seed=31)
+    q, k, v = prob["q"], prob["k"].clone(), prob["v"].clone()
+    B, nbm = len(seq), Tmax // 64
+    cfg = _cfg(batch=B, num_q_heads=G * Hkv, num_kv_heads=Hkv, max_seq_len=Tmax, budget=4, window=100,
+               mean_dtype=md, factor_dtype=fd)
+    pages = B * nbm
+    table = torch.arange(pages, dtype=torch.int32).view(B, nbm).clone()
+    bad = [(0, 3, -1), (1, (700 - 1) // 64, pages), (1, 0, pages + 7)]   # (row, block, id outside the pool)
+    for b, j, pid in bad:
+        table[b, j] = pid
+        k[b, :, j * 64:(j + 1) * 64] = 0
+        v[b, :, j * 64:(j + 1) * 64] = 0
+    kp = prob["k"].view(B, Hkv, nbm, 64, d).permute(0, 2, 1, 3, 4).reshape(pages, Hkv, 64, d).contiguous()
+    vp = prob["v"].view(B, Hkv, nbm, 64, d).permute(0, 2, 1, 3, 4).reshape(pages, Hkv, 64, d).contiguous()
+    seq_d = torch.from_numpy(seq).to(DEV)
+    rec_c, rec_p = cobs.new_summaries(cfg, DEV), cobs.new_summaries(cfg, DEV)
+    say(f"paged ids outside the pool: build {md}/{fd}")
+    cobs.cobs_build_block_stats(cfg, k.to(DEV), v.to(DEV), seq_d, rec_c)
+    cobs.cobs_build_block_stats(cfg, kp.to(DEV), vp.to(DEV), seq_d, rec_p, block_table=table.to(DEV), num_pages=pages)
+    sync()
+    assert torch.equal(rec_c, rec_p)
+    # the zeroed blocks: their counts, zero means and factors
+    L, r = 64, cfg.rank
+    for b, j, _ in bad:
+        n = min(L, int(seq[b]) - j * L)
+        for h in range(Hkv):
+            parts = R.decode(rec_p[b, h, j:j + 1].cpu().numpy(), d, r, md, fd, False, False, None)
+            assert int(parts[0][0]) == n
+            assert np.all(parts[1][0] == 0) and np.all(parts[2][0] == 0)
+    # the decode step refreshes the newest blocks (one of them outside the pool) to the same records
+    rec_s = rec_p.clone()
+    for b in range(B):
+        rec_s[b, :, (int(seq[b]) - 1) // 64] = 0
+    out = torch.empty((B, G * Hkv, d), dtype=torch.float32, device=DEV)
+    say(f"paged ids outside the pool: step {md}/{fd}")
+    cobs.cobs_decode_step(cfg, q.to(DEV), kp.to(DEV), vp.to(DEV), seq_d, rec_s, out,
+                          cobs.new_workspace(cfg, cobs.OP_STEP, DEV), block_table=table.to(DEV), num_pages=pages)
+    sync()
+    assert torch.equal(rec_s, rec_p)
+
 # -------------------------------------------------------- block statistics --
 
 def _stats_cache(law, d, nblk, tail, seed, L=64):
