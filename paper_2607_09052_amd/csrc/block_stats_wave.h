@@ -1,6 +1,6 @@
 // Block statistics of one block by one wave (Sec. 5.3, Gram trick of
 // Sec. 5.6, storage of Sec. 5.5), for blocks of LB = 32 or 64 tokens with
-// rank r <= 4 and full-space factors: the method of block_stats (16
+// rank r <= 4 and full-space or subspace factors: the method of block_stats (16
 // power-iteration columns, the same counts of products, pivot rule and Jacobi
 // termination), laid out so that a wave needs no workgroup barrier and several
 // blocks stream through a CU at once.
@@ -25,6 +25,12 @@
 //     them as matrix-core products on registers.
 //   * Factors: lane l owns columns (d / 64) l .. of xi and reads those columns
 //     of every key (a second pass over the block in L2).
+//   * Subspace factors (FD < D, Sec. 5.4): the Gram operands are the
+//     projected centred keys Kc U (U = basis of head h, D x FD), formed by
+//     v_mfma_f32_16x16x4_f32 with U's rows as A and the key rows as B; each
+//     result tile is the operand of one Gram k-step with the feature index
+//     permuted.  The factor pass forms Kc^T w / sqrt(n) as above, then
+//     xi_ss = U^T xi, on which the sign rule and the record work.
 #pragma once
 
 #include "block_stats.h"
@@ -36,9 +42,9 @@ constexpr int kMaxWaveRank = 4;
 
 // The record of a block by one wave: the E2M1 scales first, then the header
 // (count, scales, skew coefficients, zeros) and every stored vector (mean, nr
-// factors from Xi, value mean) with zeros up to the record size, each byte
-// written once.
-template <int D>
+// factors of FD elements from Xi, value mean) with zeros up to the record
+// size, each byte written once.
+template <int D, int FD = D>
 __device__ __forceinline__ void write_record_wave(const StatsArgs& p, uint8_t* R, int n, int nr, const float* mean,
                                                   const float* Xi, const float* vmean, const float* skw, int lane) {
   const RecLayout lay = p.lay;
@@ -47,7 +53,7 @@ __device__ __forceinline__ void write_record_wave(const StatsArgs& p, uint8_t* R
   const float vsc = (me2 && p.vmean) ? e2m1_scale_wave(vmean, D, lane) : 0.0f;
   float fsc[kMaxWaveRank];
 #pragma unroll
-  for (int vi = 0; vi < kMaxWaveRank; ++vi) fsc[vi] = (fe2 && vi < nr) ? e2m1_scale_wave(&Xi[vi * D], D, lane) : 0.0f;
+  for (int vi = 0; vi < kMaxWaveRank; ++vi) fsc[vi] = (fe2 && vi < nr) ? e2m1_scale_wave(&Xi[vi * FD], FD, lane) : 0.0f;
   for (int idx = lane; idx < lay.mean_off / 4; idx += 64) {
     uint32_t w = 0u;
     if (idx == 0) w = (uint32_t)n;
@@ -59,7 +65,7 @@ __device__ __forceinline__ void write_record_wave(const StatsArgs& p, uint8_t* R
   }
   store_vector_codes_wave(mean, D, p.mdt, R + lay.mean_off, msc, lane);
   for (int vi = 0; vi < nr; ++vi)
-    store_vector_codes_wave(&Xi[vi * D], D, p.fdt, R + lay.fac_off + vi * lay.vec_bytes,
+    store_vector_codes_wave(&Xi[vi * FD], FD, p.fdt, R + lay.fac_off + vi * lay.vec_bytes,
                             vi == 0 ? fsc[0] : vi == 1 ? fsc[1] : vi == 2 ? fsc[2] : fsc[3], lane);
   if (p.vmean) store_vector_codes_wave(vmean, D, p.mdt, R + lay.vmean_off, vsc, lane);
   // factors of a block without them, and the padding after the last vector
@@ -92,7 +98,8 @@ struct WaveStatsLds {
   static constexpr size_t wr = al(vm + 4 * P * PS);        // [4][LB] Ritz vectors
   static constexpr size_t xi = al(wr + 4 * 4 * LB);        // [4][D] factors
   static constexpr size_t chk = al(xi + 4 * 4 * D);        // Jacobi stop test: diagonal [P], ranks [P], threshold
-  static constexpr size_t late = al(chk + 4 * (2 * P + 4));
+  static constexpr size_t xss = al(chk + 4 * (2 * P + 4)); // [4][<= D] subspace factors
+  static constexpr size_t late = al(xss + 4 * 4 * D);
   static constexpr size_t bytes = mx(late, gparts + part_bytes);
   static constexpr size_t bytes_glds = mx(late, gparts + 3 * part_bytes);
 };
@@ -104,9 +111,10 @@ constexpr size_t wave_stats_lds_bytes() { return GLDS ? WaveStatsLds<D, LB>::byt
 // (the first 16 of the 22 products with Gamma).
 constexpr int kHiIters = 9;
 
-// The configurations block_stats_wave covers.
-__host__ __device__ inline bool wave_stats_applies(int r, int lsh, bool subspace) {
-  return r <= kMaxWaveRank && (lsh == 5 || lsh == 6) && !subspace;
+// The configurations block_stats_wave covers (full-space factors, or
+// subspace factors of 32, 64 or 96 elements).
+__host__ __device__ inline bool wave_stats_applies(int r, int lsh) {
+  return r <= kMaxWaveRank && (lsh == 5 || lsh == 6);
 }
 
 // One block by the calling wave (lane = threadIdx.x % 64; every lane of the
@@ -114,10 +122,18 @@ __host__ __device__ inline bool wave_stats_applies(int r, int lsh, bool subspace
 // wave_stats_lds_bytes<D, LB, GLDS>() bytes of LDS.  GLDS: all three of
 // Gamma's bf16 parts live in LDS (fewer registers, for a caller that has other
 // work in flight); the operations and so the record are the same either way.
-template <int D, int LB, bool KF32, bool GLDS = false>
+// FD < D: subspace factors (Sec. 5.4) of FD elements with the basis U_Q of
+// p.basis ([Hkv][D][FD]): the Gram matrix of the projected centred keys
+// Kc U_Q (formed on the matrix cores inside the Gram loop: the projection's
+// result tiles are the Gram product's operands), the same eigenproblem, and
+// xi^ss = U_Q^T xi from the full-space factor pass (xi^ss = (Kc U_Q)^T w / sqrt(n)).
+template <int D, int LB, bool KF32, bool GLDS = false, int FD = D>
 __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int h, int j, int n, char* pool) {
   static_assert(LB == 32 || LB == 64, "blocks of 32 or 64 tokens");
   static_assert(D == 64 || D == 128, "d = 64 or 128");
+  static_assert(FD == D || (FD % 32 == 0 && FD < D), "subspace factors of 32, 64 or 96 elements");
+  constexpr bool SS = FD < D;
+  constexpr int FT = SS ? FD / 16 : 1;          // 16-feature tiles of the projected keys
   using Lay = WaveStatsLds<D, LB>;
   constexpr int P = Lay::P, PS = Lay::PS;
   constexpr int NT16 = LB / 16;                 // 16-row tiles of the block
@@ -135,6 +151,8 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
   int* crank = reinterpret_cast<int*>(pool + Lay::chk) + P;
   float* Wr = reinterpret_cast<float*>(pool + Lay::wr);
   float* Xi = reinterpret_cast<float*>(pool + Lay::xi);
+  float* Xs = reinterpret_cast<float*>(pool + Lay::xss);
+  const float* Uh = SS ? p.basis + (size_t)h * D * FD : nullptr;
   int* order = reinterpret_cast<int*>(pool + Lay::misc);
   float* ritzval = reinterpret_cast<float*>(pool + Lay::misc) + 4;
   float* skw = reinterpret_cast<float*>(pool + Lay::misc) + 8;
@@ -223,12 +241,24 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
   const bool factors = (n == LB) && (r > 0);
   uint8_t* R = p.rec + (((int64_t)b * p.hkv + h) * p.nbmax + j) * p.lay.total;
   if (factors) {
-    // ---- Gram matrix Kc Kc^T: g[t][u][v] = Gamma[16 t + 4 lk + v][16 u + lr]
+    // ---- Gram matrix Kc Kc^T (subspace: (Kc U)(Kc U)^T):
+    // g[t][u][v] = Gamma[16 t + 4 lk + v][16 u + lr]
     f32x4_t g[NT16][NT16];
+    auto zero_gram = [&]() {
 #pragma unroll
-    for (int t = 0; t < NT16; ++t)
+      for (int t = 0; t < NT16; ++t)
 #pragma unroll
-      for (int u = 0; u < NT16; ++u) g[t][u] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int u = 0; u < NT16; ++u) g[t][u] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    };
+    if constexpr (!SS) zero_gram();
+    // subspace: kp[a][t][v] = (Kc U)[16 t + lr][16 a + 4 lk + v], the result
+    // tiles of U^T Kc^T (A = U^T with lane (lk, lr) giving U[k][16 a + lr], B =
+    // Kc^T, k the lane group's key column of the k-step)
+    f32x4_t kp[FT][SS ? NT16 : 1];
+#pragma unroll
+    for (int a = 0; a < FT; ++a)
+#pragma unroll
+      for (int t = 0; t < (SS ? NT16 : 1); ++t) kp[a][t] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
     // the keys again (L2), chunk q + 1 in flight while chunk q is multiplied
     Raw rcur[NT16], rnext[NT16];
     load_raw(p.kv.k, 0, rnext);
@@ -246,13 +276,40 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
       for (int t = 0; t < NT16; ++t)
 #pragma unroll
         for (int e = 0; e < 8; ++e) x[t][e] -= mm[e];
+      if constexpr (SS) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
+        for (int e = 0; e < 8; ++e) {
+          const float* urow = Uh + (size_t)(lk * CPL + 8 * q + e) * FD + lr;
 #pragma unroll
-        for (int t = 0; t < NT16; ++t)
+          for (int a = 0; a < FT; ++a) {
+            const float ua = urow[16 * a];
 #pragma unroll
-          for (int u = 0; u < NT16; ++u)
-            g[t][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[t][e], x[u][e], g[t][u], 0, 0, 0);
+            for (int t = 0; t < NT16; ++t)
+              kp[a][t] = __builtin_amdgcn_mfma_f32_16x16x4f32(ua, x[t][e], kp[a][t], 0, 0, 0);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+#pragma unroll
+          for (int t = 0; t < NT16; ++t)
+#pragma unroll
+            for (int u = 0; u < NT16; ++u)
+              g[t][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(x[t][e], x[u][e], g[t][u], 0, 0, 0);
+      }
+    }
+    if constexpr (SS) {
+      // Gamma = Kp Kp^T: at k-step (a, v) lane group lk gives feature 16 a + 4 lk + v
+      zero_gram();
+#pragma unroll
+      for (int a = 0; a < FT; ++a)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+          for (int t = 0; t < NT16; ++t)
+#pragma unroll
+            for (int u = 0; u < NT16; ++u)
+              g[t][u] = __builtin_amdgcn_mfma_f32_16x16x4f32(kp[a][t][v], kp[a][u][v], g[t][u], 0, 0, 0);
     }
     float diag = 0.0f;
 #pragma unroll
@@ -592,26 +649,80 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
           }
         }
       }
-      // sign: the largest-magnitude entry positive (lowest index on ties): the
-      // lane's first largest entry, the wave's largest magnitude, the lowest
-      // lane holding it
+      if constexpr (SS) {
+        // the full-space vectors into LDS, then xi^ss = U^T xi: lane l owns
+        // features l and l + 64 (< FD)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (i >= r) break;
-        const bool keep = ritzval[i] > 1e-6f * top && top > 0.0f;
-        float best = -1.0f, sbest = 0.0f;
+        for (int i = 0; i < 4; ++i) {
+          const bool keep = i < r && ritzval[i] > 1e-6f * top && top > 0.0f;
 #pragma unroll
-        for (int c = 0; c < EPL; ++c) {
-          xs[i][c] = keep ? xs[i][c] * rsn : 0.0f;
-          const float a = fabsf(xs[i][c]);
-          if (a > best) { best = a; sbest = xs[i][c]; }
+          for (int c = 0; c < EPL; ++c) Xi[i * D + EPL * lane + c] = keep ? xs[i][c] * rsn : 0.0f;
         }
-        const float m = wave_max_rows(best);
-        const uint64_t holders = __ballot(best == m);
-        const int src = (int)__builtin_ctzll(holders);
-        const float pivot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sbest), src));
+        wave_lds_sync();
+        constexpr int FPL = (FD + 63) / 64;
+        float ys[4][FPL];
 #pragma unroll
-        for (int c = 0; c < EPL; ++c) Xi[i * D + EPL * lane + c] = (pivot < 0.0f) ? -xs[i][c] : xs[i][c];
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int c = 0; c < FPL; ++c) ys[i][c] = 0.0f;
+#pragma unroll 1
+        for (int e = 0; e < D; e += 4) {
+          float4 xe[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) xe[i] = *reinterpret_cast<const float4*>(Xi + i * D + e);
+#pragma unroll
+          for (int c = 0; c < FPL; ++c) {
+            const int f = lane + 64 * c;
+            if (f < FD) {
+#pragma unroll
+              for (int ee = 0; ee < 4; ++ee) {
+                const float u = Uh[(size_t)(e + ee) * FD + f];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                  ys[i][c] += u * (ee == 0 ? xe[i].x : ee == 1 ? xe[i].y : ee == 2 ? xe[i].z : xe[i].w);
+              }
+            }
+          }
+        }
+        // sign over the FD entries (the lane's entry l precedes its entry l + 64)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (i >= r) break;
+          const float a0 = fabsf(ys[i][0]);
+          const float a1 = (FPL > 1 && lane + 64 < FD) ? fabsf(ys[i][FPL - 1]) : -1.0f;
+          const float m = wave_max_rows(fmaxf(a0, a1));
+          const uint64_t h0 = __ballot(a0 == m), h1 = __ballot(a1 == m);
+          const float pivot =
+              h0 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ys[i][0]), (int)__builtin_ctzll(h0)))
+                 : __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ys[i][FPL - 1]), (int)__builtin_ctzll(h1)));
+#pragma unroll
+          for (int c = 0; c < FPL; ++c) {
+            const int f = lane + 64 * c;
+            if (f < FD) Xs[i * FD + f] = (pivot < 0.0f) ? -ys[i][c] : ys[i][c];
+          }
+        }
+      } else {
+        // sign: the largest-magnitude entry positive (lowest index on ties): the
+        // lane's first largest entry, the wave's largest magnitude, the lowest
+        // lane holding it
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          if (i >= r) break;
+          const bool keep = ritzval[i] > 1e-6f * top && top > 0.0f;
+          float best = -1.0f, sbest = 0.0f;
+#pragma unroll
+          for (int c = 0; c < EPL; ++c) {
+            xs[i][c] = keep ? xs[i][c] * rsn : 0.0f;
+            const float a = fabsf(xs[i][c]);
+            if (a > best) { best = a; sbest = xs[i][c]; }
+          }
+          const float m = wave_max_rows(best);
+          const uint64_t holders = __ballot(best == m);
+          const int src = (int)__builtin_ctzll(holders);
+          const float pivot = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(sbest), src));
+#pragma unroll
+          for (int c = 0; c < EPL; ++c) Xi[i * D + EPL * lane + c] = (pivot < 0.0f) ? -xs[i][c] : xs[i][c];
+        }
       }
     }
     wave_lds_sync();
@@ -620,15 +731,46 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
       // z_t^3 with z_t = (xi_i . kc_t) / |xi_i|^2, the projection on u_i
       // standardised by its deviation; the r projections of a token together
       float lam[4], pr[4];
+      if constexpr (SS) {
+        // subspace: the projection of a projected key on xi^ss_i is u_i . kc with
+        // u_i = U xi^ss_i (into Xi, the lane's EPL rows of U), and lam_i = |xi^ss_i|^2
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float nrm = 0.0f;
-        if (i < r) {
-#pragma unroll
-          for (int c = 0; c < EPL; ++c) nrm += Xi[i * D + EPL * lane + c] * Xi[i * D + EPL * lane + c];
+        for (int i = 0; i < 4; ++i) {
+          float nrm = 0.0f;
+          if (i < r) {
+            for (int f = lane; f < FD; f += 64) nrm += Xs[i * FD + f] * Xs[i * FD + f];
+          }
+          lam[i] = wave_sum_rows(nrm);
+          pr[i] = 0.0f;
         }
-        lam[i] = wave_sum_rows(nrm);
-        pr[i] = 0.0f;
+#pragma unroll
+        for (int c = 0; c < EPL; ++c) {
+          const int e = EPL * lane + c;
+          float uu[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll 2
+          for (int f = 0; f < FD; f += 4) {
+            const float4 u = *reinterpret_cast<const float4*>(Uh + (size_t)e * FD + f);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float4 xsv = *reinterpret_cast<const float4*>(Xs + i * FD + f);
+              uu[i] += u.x * xsv.x + u.y * xsv.y + u.z * xsv.z + u.w * xsv.w;
+            }
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) Xi[i * D + e] = (i < r) ? uu[i] : 0.0f;
+        }
+        wave_lds_sync();
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float nrm = 0.0f;
+          if (i < r) {
+#pragma unroll
+            for (int c = 0; c < EPL; ++c) nrm += Xi[i * D + EPL * lane + c] * Xi[i * D + EPL * lane + c];
+          }
+          lam[i] = wave_sum_rows(nrm);
+          pr[i] = 0.0f;
+        }
       }
       if (lane < LB) {
         const int64_t off0 = kbase < 0 ? -1 : kbase + lane * rs;
@@ -670,7 +812,7 @@ __device__ __forceinline__ void block_stats_wave(const StatsArgs& p, int b, int 
     }
   }
 
-  write_record_wave<D>(p, R, n, factors ? r : 0, mean, Xi, vmean, skw, lane);
+  write_record_wave<D, FD>(p, R, n, factors ? r : 0, mean, SS ? Xs : Xi, vmean, skw, lane);
 }
 
 // A block with fewer than LB tokens (count and means only, zero factors) by a

@@ -32,7 +32,7 @@ hipError_t launch_build_ss(const BuildParams& p, int d, dim3 grid, hipStream_t s
 
 hipError_t launch_build(const BuildParams& p, int d, dim3 grid, hipStream_t st) {
   if (p.basis) return launch_build_ss(p, d, grid, st);
-  if (wave_stats_applies(p.r, p.kv.lsh, false))
+  if (wave_stats_applies(p.r, p.kv.lsh))
     return d == 128 ? launch_build_wave<128>(p, grid, st) : launch_build_wave<64>(p, grid, st);
   const bool big = build_big_basis(p);
   if (d == 128) return big ? launch_build_dp<128, 32, false>(p, grid, st) : launch_build_dp<128, 16, false>(p, grid, st);
