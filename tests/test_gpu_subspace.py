@@ -40,17 +40,20 @@ def _cfg(d, sd, L, kv, r, md, fd, T, basis, G=4, B=2, Hkv=2, s=8, w=128, **kw):
 
 
 BUILD_CASES = [
-    # d, s', L, K/V, r, mean, factor, skew, key law
-    (128, 96, 64, "bf16", 4, "bf16", "e2m1", False, "c4"),
-    (128, 32, 32, "f32", 2, "e2m1", "bf16", True, "c5"),
-    (64, 32, 128, "bf16", 4, "bf16", "bf16", False, "c5"),
-    (128, 64, 128, "bf16", 3, "e2m1", "e2m1", True, "c3"),
-    (128, 96, 64, "f32", 1, "bf16", "e2m1", True, "c2"),
+    # d, s', L, K/V, r, mean, factor, skew, key law, value means
+    (128, 96, 64, "bf16", 4, "bf16", "e2m1", False, "c4", False),
+    (128, 32, 32, "f32", 2, "e2m1", "bf16", True, "c5", False),
+    (64, 32, 128, "bf16", 4, "bf16", "bf16", False, "c5", False),
+    (128, 64, 128, "bf16", 3, "e2m1", "e2m1", True, "c3", False),
+    (128, 96, 64, "f32", 1, "bf16", "e2m1", True, "c2", False),
+    (128, 64, 64, "bf16", 4, "e2m1", "e2m1", True, "c4", True),
+    (128, 64, 32, "bf16", 3, "bf16", "bf16", False, "c3", True),
+    (64, 32, 64, "bf16", 2, "f32", "e2m1", False, "c5", True),
 ]
 
 
-@pytest.mark.parametrize("d,sd,L,kv,r,md,fd,skew,law", BUILD_CASES)
-def test_subspace_build_matches_oracle(d, sd, L, kv, r, md, fd, skew, law):
+@pytest.mark.parametrize("d,sd,L,kv,r,md,fd,skew,law,vm", BUILD_CASES)
+def test_subspace_build_matches_oracle(d, sd, L, kv, r, md, fd, skew, law, vm):
     T, B, Hkv, G = 2048, 2, 2, 4
     U, _, _ = _basis(Hkv, d, sd, G, seed=700 + sd + L)
     basis = torch.from_numpy(U.astype(np.float32)).contiguous().to(DEV)
@@ -59,17 +62,17 @@ def test_subspace_build_matches_oracle(d, sd, L, kv, r, md, fd, skew, law):
     k, v = prob["k"].to(DEV), prob["v"].to(DEV)
     lens = [T, T - L - 5]
     seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
-    cfg = _cfg(d, sd, L, kv, r, md, fd, T, basis, G=G, B=B, Hkv=Hkv, skew=skew)
+    cfg = _cfg(d, sd, L, kv, r, md, fd, T, basis, G=G, B=B, Hkv=Hkv, skew=skew, value_mean=vm)
     cfg32 = f32_config(cfg)
     rec, rec32 = cobs.new_summaries(cfg, DEV), cobs.new_summaries(cfg32, DEV)
-    say(f"subspace build d={d} s'={sd} L={L} {kv} r={r} {md}/{fd} skew={skew} law={law}")
+    say(f"subspace build d={d} s'={sd} L={L} {kv} r={r} {md}/{fd} skew={skew} law={law} value means={vm}")
     cobs.cobs_build_block_stats(cfg, k, v, seq, rec)
     cobs.cobs_build_block_stats(cfg32, k, v, seq, rec32)
     sync()
     for b, Tb in enumerate(lens):
         for h in range(Hkv):
             check_records(cfg, rec[b, h].cpu().numpy(), rec32[b, h].cpu().numpy(), f64(prob["k"][b, h]), Tb,
-                          U=U[h])
+                          V_unit=f64(prob["v"][b, h]) if vm else None, U=U[h])
 
 
 SELECT_CASES = [
@@ -125,25 +128,40 @@ def test_subspace_select_matches_oracle(d, sd, G, L, md, fd, skew, ssq):
     assert moved > 1e-2, moved
 
 
-@pytest.mark.parametrize("L,t0", [(64, 3000), (64, 3008), (32, 2999)])
-def test_subspace_decode_step_is_build_select_decode(L, t0):
+STEP_CASES = [
+    # L, newest length, s', K/V, skew, value means
+    (64, 3000, 96, "bf16", False, False),
+    (64, 3008, 96, "bf16", False, False),
+    (32, 2999, 96, "bf16", False, False),
+    (64, 2999, 64, "bf16", True, True),
+    (32, 3008, 64, "bf16", False, True),
+    (64, 3001, 32, "f32", True, False),
+    (32, 2976, 32, "f32", False, True),
+]
+
+
+@pytest.mark.parametrize("L,t0,sd,kv,skew,vm", STEP_CASES)
+def test_subspace_decode_step_is_build_select_decode(L, t0, sd, kv, skew, vm):
     """The step with subspace factors (build of the newest block, query
-    projection, selection, attention) equals the separate calls bitwise."""
-    d, sd, G, Hkv, B, s, w = 128, 96, 4, 4, 2, 10, 300
-    U, rot, sig = _basis(Hkv, d, sd, G, seed=900 + L)
+    projection, selection, attention) equals the separate calls bitwise, for a
+    partial or a full newest block."""
+    d, G, Hkv, B, s, w = 128, 4, 4, 2, 10, 300
+    U, rot, sig = _basis(Hkv, d, sd, G, seed=900 + L + sd)
     basis = torch.from_numpy(U.astype(np.float32)).contiguous().to(DEV)
     prob = synth.make_problem("c3", seed=910 + L, B=B, Hq=G * Hkv, Hkv=Hkv, T=3000, s=s, w=w, L=L)
     T_max = 3008
-    cfg = _cfg(d, sd, L, "bf16", 4, "bf16", "e2m1", T_max, basis, G=G, B=B, Hkv=Hkv, s=s, w=w)
-    k = torch.zeros((B, Hkv, T_max, d), dtype=torch.bfloat16)
+    cfg = _cfg(d, sd, L, kv, 4, "bf16", "e2m1", T_max, basis, G=G, B=B, Hkv=Hkv, s=s, w=w, skew=skew,
+               value_mean=vm)
+    dt = torch.bfloat16 if kv == "bf16" else torch.float32
+    k = torch.zeros((B, Hkv, T_max, d), dtype=dt)
     v = torch.zeros_like(k)
-    k[:, :, :3000], v[:, :, :3000] = prob["k"][:, :, :3000], prob["v"][:, :, :3000]
+    k[:, :, :3000], v[:, :, :3000] = prob["k"][:, :, :3000].to(dt), prob["v"][:, :, :3000].to(dt)
     k, v = k.to(DEV), v.to(DEV)
     q = synth.subspace_queries(rot, sig, B, G, seed=920).to(DEV)
     lens = [t0, 2049]
     seq = torch.tensor(lens, dtype=torch.int32, device=DEV)
     rec0 = cobs.new_summaries(cfg, DEV)
-    say(f"subspace step L={L} T={t0}")
+    say(f"subspace step L={L} T={t0} s'={sd} {kv} skew={skew} value means={vm}")
     cobs.cobs_build_block_stats(cfg, k, v, seq, rec0)
     rec1 = rec0.clone()
     for b, T in enumerate(lens):
