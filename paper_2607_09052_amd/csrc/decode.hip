@@ -96,7 +96,8 @@ __device__ __forceinline__ void decode_prologue(const DecodeParams& p, int b, in
   const int32_t* sl = p.sel + (int64_t)unit * p.s;
   const int it = first + tid;
   const int seg = it / items_per_block<PT>(p.lsh);
-  const int selv = (p.s > 0) ? sl[(tid < cnt && seg < p.s) ? seg : 0] : 0;
+  // (an index independent of the row length, so the load does not wait for it)
+  const int selv = (p.s > 0) ? sl[min(seg, p.s - 1)] : 0;
   int kv = p.s;                 // first entry breaking the ascending run of candidates
   for (int i = tid; i < p.s; i += NT) {
     const int bi = sl[i], prev = sl[i > 0 ? i - 1 : 0];
