@@ -21,10 +21,13 @@ start at staggered phases, so one step in 64 is the step that fills a block
 and recomputes its covariance factors (the other steps refresh the partial
 block's mean).  To measure HBM rather than the 256 MB last-level cache the
 steps rotate over M independent copies of the layer (K/V cache, descriptors,
-queries) that together read >= 2 GB per sweep.  Steps are replayed from HIP
-graphs (a whole sweep, and a partial sweep for the remainder), so exactly W
-untimed and then exactly K timed steps run, without host launch overhead;
-fill_cycle_us is the mean over all 64 phases from a longer replay.
+queries) that together read >= 2 GB per sweep, and M >= 8: a sweep is one HIP
+graph, as a decode step's graph spans a model's layers, so each replay's fixed
+launch cost (about 10-14 us on MI355X) is shared by at least 8 layer-steps.
+Steps are replayed from those graphs (a whole sweep, and a partial sweep for
+the remainder), so exactly W untimed and then exactly K timed steps run,
+without host launch overhead; fill_cycle_us is the mean over all 64 phases
+from a longer replay.
 
 Each workload reports the metric (us per decode step per layer), GB/s on the
 step's algorithmic bytes, the roofline of its dominant kernel (timed on its own
@@ -350,7 +353,7 @@ def run_workload(name, args, dev, with_cpu):
     ab = {k_: float(np.mean([x[k_] for x in per_phase])) for k_ in per_phase[0]}
     ab_fill = per_phase[-1]
 
-    copies = args.copies or max(2, math.ceil(2e9 / ab["step"]))
+    copies = args.copies or max(8, math.ceil(2e9 / ab["step"]))
     layers = [(prob["q"], prob["k"], prob["v"], rec)]
     for _ in range(copies - 1):
         layers.append(tuple(x.clone() for x in layers[0]))
@@ -534,7 +537,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workloads", default="c3,c2,c4,c5,c4ss",
                     help="comma-separated workloads; the first is the headline line")
-    ap.add_argument("--copies", type=int, default=0, help="layer copies to rotate (0: >= 2 GB per sweep)")
+    ap.add_argument("--copies", type=int, default=0, help="layer copies to rotate (0: >= 2 GB per sweep, and >= 8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "hbm_traffic.txt"),
                     help="rocprofv3 HBM traffic summary ('traffic <workload> <kernel> <read> <written>' lines)")
